@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Throughput benchmark of the PNN training path on one MI355X.
+
+A step is one pass of the whole hot path over the workload's synthetic training set: every
+child network (CN) trains `epochs` epochs on its own slice (forward, output and hidden
+errors, SGD updates), with the scheduled merges (average, and broadcast between epochs).
+Inputs are resident in HBM before the timed region; initialisation and evaluation are
+outside it (evaluation is timed separately and reported as `eval_ms`).
+
+Printed: one JSON line with samples/s over all CNs (N * epochs / step time), the roofline
+position of the dominant kernel (measured with HIP events around every launch in an extra,
+untimed step), and the CPU oracle timed on the host cores as a baseline.
+
+Default workload: 784-128-10 sigmoid MLP, K = 4 CNs, per-sample SGD, 60,000 samples,
+1 epoch + merge (workload index 1).  --workload selects another.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import pnn_inputs as I  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 (vector with packed FMA, and matrix)
+BF16_PEAK_TFLOPS = 2500.0      # MI355X bf16 dense matrix
+
+
+def kernel_work(w, name: str, launches: int, N: int):
+    """Algorithmic work of one launch of a library kernel: (bound, flops, bytes).
+
+    Counts follow the method's arithmetic per sample and per CN (no padding, no extra work
+    of the implementation):
+      per-sample plan, with H hidden, O outputs, In inputs, chunk T, K CNs:
+        psgd_chunk  T steps of K CNs: second-layer forward, hidden error and update
+                    (3 * 2*H*O), biases (2*O + 2*H), and the first layer's running
+                    input-sum correction of the chunked form (2*H per earlier sample of the
+                    chunk, (T-1)/2 on average);
+        psgd_p      P = W1 x_t for T samples of K CNs: 2*H*In per sample;
+        psgd_upd    W1 -= eta * sum_t d1_t x_t^T for T samples of K CNs: 2*H*In per sample;
+        psgd_gram   x_t . x_s for the T*T pairs of each chunk: 2*In per pair.
+      merge: reads K*P floats and writes P (and K*P with broadcast) -- HBM bound.
+    """
+    s = w.sizes
+    K = w.replicas
+    if name.startswith("psgd"):
+        H, O, In = s[1], s[2], s[0]
+        T = 128
+        while T > 16 and T * H > 16384:
+            T //= 2
+        nk = -(-N // K)
+        nch = -(-nk // T)
+        steps_per_launch = N / nch  # samples of all CNs handled per chunk launch
+        if name == "psgd_chunk":
+            per = 3 * 2 * H * O + 2 * O + 2 * H + 2 * H * (T - 1) / 2
+            return "alu", steps_per_launch * per, steps_per_launch * (H * 4 * 3)
+        if name in ("psgd_p", "psgd_upd"):
+            return "mfma", steps_per_launch * 2 * H * In, steps_per_launch * In * 4 + K * H * In * 4 * 2
+        if name == "psgd_gram":
+            return "mfma", N * T * 2 * In, N * In * 4
+    if name == "merge":
+        P = w.param_count()
+        return "hbm", 0.0, (K * P + P) * 4.0
+    return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("this build runs on one GPU only: the CNs of a PNN are independent until the merge, "
+              "so a multi-GPU run would only split the CNs across GPUs and all-reduce at the merge; "
+              "no multi-GPU path is built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2304_09590_amd import pnn as B
+
+    w = I.WORKLOADS[args.workload]
+    N = w.n_train
+    t0 = time.time()
+    X, y = I.train_set(w)
+    Xt, yt = I.test_set(w)
+    th0 = I.init_params(w)
+    print(f"[bench] workload {w.name}: data ready in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    xd = torch.from_numpy(X).cuda()
+    yd = torch.from_numpy(y).cuda()
+    xtd = torch.from_numpy(Xt).cuda()
+    ytd = torch.from_numpy(yt).cuda()
+    net = B.PNN(B.config_from_workload(w), th0)
+
+    def step():
+        for e in range(w.epochs):
+            net.train_epoch(xd, yd, stream=stream)
+            if w.merge_every_epoch:
+                net.merge(broadcast=True, stream=stream)
+        if not w.merge_every_epoch:
+            net.merge(broadcast=False, stream=stream)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        print(f"[bench] warmup step {i} done", file=sys.stderr, flush=True)
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    samples = N * w.epochs
+    value = samples / (ms / 1e3)
+    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # evaluation (outside the step)
+    pred = torch.empty(len(yt), dtype=torch.int32, device="cuda")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    correct = net.infer(xtd, pred, which=-1, y=ytd, count=True, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    eval_ms = e0.elapsed_time(e1)
+
+    # per-kernel device time in one extra step
+    net.profile(True)
+    step()
+    torch.cuda.synchronize()
+    prof = net.profile_read()
+    net.profile(False)
+    kernels = {k: {"ms_total": round(v[0], 4), "launches": v[1], "avg_us": round(1e3 * v[0] / max(v[1], 1), 3)}
+               for k, v in prof.items()}
+    dom = max(prof.items(), key=lambda kv: kv[1][0])[0] if prof else None
+    roofline = None
+    if dom is not None:
+        tot, n_l = prof[dom]
+        avg_s = tot / 1e3 / n_l
+        wk = kernel_work(w, dom, n_l, N)
+        if wk is not None:
+            bound, flops, byts = wk
+            if bound == "hbm":
+                ach, peak, unit = byts / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+            else:
+                peak = BF16_PEAK_TFLOPS if w.precision == I.BF16_MIXED and bound == "mfma" else FP32_PEAK_TFLOPS
+                ach, unit = flops / avg_s / 1e12, "TFLOP/s"
+            roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 4), "peak": peak, "unit": unit,
+                        "frac": round(ach / peak, 6), "traffic": None, "avg_us": round(avg_s * 1e6, 3)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        cores = len(os.sched_getaffinity(0))
+        threads = max(1, min(w.replicas, cores))
+        o = O.Oracle.from_workload(w)
+        # bounded sample: the first n_s rows of every CN's slice, one epoch
+        per = -(-N // w.replicas)
+        n_s = per if w.batch == 1 and w.sizes[1] <= 128 else max(w.batch, min(per, 400))
+        n_s = min(n_s, per)
+        idx = np.concatenate([np.arange(s, s + min(n_s, ln)) for s, ln in
+                              (o.shard(N, k) for k in range(w.replicas))])
+        th = o.replicate(th0)
+        # the sample keeps the slicing: each CN gets its own n_s rows
+        Xs, ys = X[idx], y[idx]
+        t1 = time.time()
+        o.train_epoch(th, Xs, ys, threads=threads)
+        dt = time.time() - t1
+        cpu = {"value": round(len(idx) / dt, 2), "unit": "samples/s", "cores": threads, "kind": "oracle",
+               "sample": f"{len(idx)} samples ({min(n_s, per)} per CN x {w.replicas} CNs), 1 epoch, fp64, "
+                         f"{threads} threads, {dt:.1f}s"}
+
+    out = {
+        "metric": "training samples/sec (all K replicas) + % of HBM/MFMA roofline",
+        "value": round(value, 2),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.precision == I.BF16_MIXED else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "sizes": list(w.sizes), "replicas": w.replicas, "batch": w.batch,
+                   "epochs": w.epochs, "n_train": N, "lr": w.lr,
+                   "merge": "every epoch" if w.merge_every_epoch else "end"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "eval_ms": round(eval_ms, 3),
+        "eval_accuracy": round(correct / len(yt), 4),
+        "kernels": kernels,
+    }
+    print(json.dumps(out), flush=True)
+    net.close()
+
+
+if __name__ == "__main__":
+    main()

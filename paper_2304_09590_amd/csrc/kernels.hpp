@@ -1,0 +1,704 @@
+// kernels.hpp -- CDNA4 (gfx950) kernels of the PNN hot path.
+//
+// Every kernel is batched over the K child networks (CNs): blockIdx.z (or x) selects the
+// CN, whose parameters sit at theta + z * pstride in the padded device layout, and whose
+// data slice is the contiguous row range given by shard_start/shard_len below.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pnn {
+
+enum { ACT_SIGMOID = 0, ACT_TANH = 1, ACT_RELU = 2, ACT_LEAKY = 3, ACT_SOFTMAX = 4 };
+enum { LOSS_MSE = 0, LOSS_XENT = 1 };
+
+typedef uint16_t bf16_t;  // bfloat16 storage
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+
+constexpr int MAX_OUT = 16;  // widest output layer handled by the row kernels
+
+// ------------------------------------------------------------------------------------
+// slices of the data set (contiguous, the first N mod K slices one row longer)
+
+__device__ __host__ inline int64_t shard_len(int64_t n, int k_total, int k) {
+    return n / k_total + (k < n % k_total ? 1 : 0);
+}
+__device__ __host__ inline int64_t shard_start(int64_t n, int k_total, int k) {
+    const int64_t q = n / k_total, r = n % k_total;
+    return (int64_t)k * q + (k < r ? k : r);
+}
+
+// ------------------------------------------------------------------------------------
+// bfloat16 conversion, round to nearest even
+
+__device__ inline bf16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (bf16_t)((u >> 16) | 0x40);  // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+__device__ inline float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+template <typename T> __device__ inline float to_f(T v);
+template <> __device__ inline float to_f<float>(float v) { return v; }
+template <> __device__ inline float to_f<bf16_t>(bf16_t v) { return bf2f(v); }
+template <typename T> __device__ inline T from_f(float v);
+template <> __device__ inline float from_f<float>(float v) { return v; }
+template <> __device__ inline bf16_t from_f<bf16_t>(float v) { return f2bf(v); }
+
+// ------------------------------------------------------------------------------------
+// activations.  The rectifiers store z < 0 with its sign (a negative zero for ReLU), so
+// that phi'(z) can be read back from the stored activation alone, with phi'(0) = 1.
+
+__device__ inline float act_fn(int a, float z) {
+    switch (a) {
+    case ACT_SIGMOID: return 1.0f / (1.0f + expf(-z));
+    case ACT_TANH: return tanhf(z);
+    case ACT_RELU: return z >= 0.0f ? z + 0.0f : -0.0f;
+    case ACT_LEAKY: return z >= 0.0f ? z + 0.0f : 0.01f * z;
+    default: return z;
+    }
+}
+// phi'(z) from x = phi(z)
+__device__ inline float act_deriv(int a, float x) {
+    switch (a) {
+    case ACT_SIGMOID: return x * (1.0f - x);
+    case ACT_TANH: return 1.0f - x * x;
+    case ACT_RELU: return signbit(x) ? 0.0f : 1.0f;
+    case ACT_LEAKY: return signbit(x) ? 0.01f : 1.0f;
+    default: return 1.0f;
+    }
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// ------------------------------------------------------------------------------------
+// Batched GEMM on the matrix cores.
+//
+//   C[z](m, n) (op)= sum_k A[z](m, k) * B[z](k, n)
+//
+// An operand is a row-major matrix with leading dimension ld.  A_KC: A(m,k) = A[m*ld + k]
+// (rows are m); otherwise A(m,k) = A[k*ld + m] (rows are k).  B_KC: B(k,n) = B[n*ld + k]
+// (rows are n); otherwise B(k,n) = B[k*ld + n] (rows are k).  An operand flagged xrows
+// addresses rows of the caller's data set: row r of CN z is data row
+// shard_start(z) + r0(z) + r; otherwise row r is at ptr + z*zstride + r*ld.
+//
+// The batch index z covers CN and, for chunked launches, a chunk: cn = z / zdiv,
+// r0 = r0_base + (z % zdiv) * r0_step.  Dimensions flagged in sample_dims (bit 0 = m,
+// 1 = n, 2 = k) run over the rows of the current step and are cut to
+// valid = clamp(shard_len(cn) - r0, 0, step_rows); others run to M, N, Kd.
+//
+// fp32: v_mfma_f32_16x16x4_f32.  bf16: v_mfma_f32_16x16x32_bf16, operands converted to
+// bf16 (round to nearest even) while staged into LDS; accumulation is fp32 in both.
+
+enum { EPI_STORE = 0, EPI_FWD = 1, EPI_BWD = 2, EPI_UPD = 3 };
+
+struct Operand {
+    const void* ptr;
+    int64_t zstride;
+    int64_t ld;
+    int xrows;
+};
+
+struct GemmArgs {
+    int M, N, Kd;
+    Operand a, b;
+    // output / in-place target
+    void* c;
+    int64_t c_z, c_ld;
+    // batch -> (CN, step rows)
+    int64_t n_total;
+    int k_rep;
+    int zdiv;
+    int64_t r0_base, r0_step;
+    int step_rows;
+    int sample_dims;
+    // split of the contraction: blockIdx.z = z * ksplit + slice; slice s covers
+    // [s*kchunk, (s+1)*kchunk) and writes C + s * c_split (EPI_STORE only)
+    int ksplit, kchunk;
+    int64_t c_split;
+    // epilogue
+    const float* bias;      // EPI_FWD: bias[n] (+ z * bias_z)
+    int64_t bias_z;
+    float* ubias;           // EPI_UPD: bias[m] updated with the row sums of A (+ z * bias_z)
+    int act;
+    const void* aux;        // EPI_BWD: activation x^l, same layout as C
+    float lr;
+    int scale_per_batch;    // EPI_UPD: scale = lr / valid (1) or lr (0)
+    bf16_t* shadow;         // EPI_UPD: bf16 copy of the updated target (+ z * c_z), nullable
+};
+
+template <bool BF> struct GemmTile;
+template <> struct GemmTile<false> { static constexpr int BK = 16, LDK = 20; typedef float T; };
+template <> struct GemmTile<true> { static constexpr int BK = 32, LDK = 40; typedef bf16_t T; };
+
+__device__ inline void gemm_zinfo(const GemmArgs& g, int z, int& cn, int64_t& r0, int& valid) {
+    cn = z / g.zdiv;
+    r0 = g.r0_base + (int64_t)(z % g.zdiv) * g.r0_step;
+    int64_t v = shard_len(g.n_total, g.k_rep, cn) - r0;
+    valid = (int)(v < 0 ? 0 : (v > g.step_rows ? g.step_rows : v));
+}
+
+__device__ inline const char* operand_row(const Operand& o, int elem, int z, int cn, int64_t xbase, int64_t r) {
+    const char* p = (const char*)o.ptr;
+    if (o.xrows) return p + (size_t)((xbase + r) * o.ld) * elem;
+    return p + (size_t)(z * o.zstride + r * o.ld) * elem;
+}
+
+// Stage a BR x BK tile (rows r0t.., k k0..) of an operand whose rows are the tile's
+// non-contraction index ("KC" layout) into lds[row][k].
+template <bool BF, typename TS>
+__device__ inline void stage_kc(typename GemmTile<BF>::T* lds, const Operand& o, int z, int cn, int64_t xbase,
+                                int row0, int rows_valid, int k0, int k_valid, int tid) {
+    constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
+    if constexpr (!BF) {
+        // 64 rows x 16 k fp32: one float4 per thread
+        const int r = tid >> 2, kq = (tid & 3) * 4;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row0 + r < rows_valid && k0 + kq < k_valid)
+            v = *(const float4*)(operand_row(o, 4, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 4);
+        *(float4*)(lds + r * LDK + kq) = v;
+    } else if constexpr (sizeof(TS) == 4) {
+        // 64 rows x 32 k from fp32: two float4 per thread, converted
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int idx = tid + h * 256, r = idx >> 3, kq = (idx & 7) * 4;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (row0 + r < rows_valid && k0 + kq < k_valid)
+                v = *(const float4*)(operand_row(o, 4, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 4);
+            bf16_t* d = lds + r * LDK + kq;
+            d[0] = f2bf(v.x); d[1] = f2bf(v.y); d[2] = f2bf(v.z); d[3] = f2bf(v.w);
+        }
+    } else {
+        // 64 rows x 32 k from bf16: one 16-byte load per thread
+        const int r = tid >> 2, kq = (tid & 3) * 8;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (row0 + r < rows_valid && k0 + kq < k_valid)
+            v = *(const uint4*)(operand_row(o, 2, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 2);
+        *(uint4*)(lds + r * LDK + kq) = v;
+    }
+    (void)BK;
+}
+
+// Stage a tile from an operand whose rows are the contraction index ("NC" layout):
+// element (t, k) = row k, column t; stored transposed into lds[t][k].
+template <bool BF, typename TS>
+__device__ inline void stage_nc(typename GemmTile<BF>::T* lds, const Operand& o, int z, int cn, int64_t xbase,
+                                int col0, int cols_valid, int k0, int k_valid, int tid) {
+    constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
+    // BK rows (k) x 64 columns; 4 consecutive columns per access
+#pragma unroll
+    for (int h = 0; h < BK / 16; ++h) {
+        const int idx = tid + h * 256, k = idx >> 4, cq = (idx & 15) * 4;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        if (k0 + k < k_valid && col0 + cq < cols_valid) {
+            const char* row = operand_row(o, sizeof(TS), z, cn, xbase, k0 + k);
+            if constexpr (sizeof(TS) == 4) {
+                float4 q = *(const float4*)(row + (size_t)(col0 + cq) * 4);
+                v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+            } else {
+                uint2 q = *(const uint2*)(row + (size_t)(col0 + cq) * 2);
+                v[0] = bf2f((bf16_t)(q.x & 0xffff)); v[1] = bf2f((bf16_t)(q.x >> 16));
+                v[2] = bf2f((bf16_t)(q.y & 0xffff)); v[3] = bf2f((bf16_t)(q.y >> 16));
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if constexpr (BF) lds[(cq + j) * LDK + k] = f2bf(v[j]);
+            else lds[(cq + j) * LDK + k] = v[j];
+        }
+    }
+}
+
+template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
+    typedef typename GemmTile<BF>::T LT;
+    constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
+    __shared__ __attribute__((aligned(16))) LT As[64 * LDK];
+    __shared__ __attribute__((aligned(16))) LT Bs[64 * LDK];
+    __shared__ float rowsum[64];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int zz = blockIdx.z / g.ksplit, slice = blockIdx.z % g.ksplit;
+    int cn, valid;
+    int64_t r0;
+    gemm_zinfo(g, zz, cn, r0, valid);
+    const int Mv = (g.sample_dims & 1) ? valid : g.M;
+    const int Nv = (g.sample_dims & 2) ? valid : g.N;
+    const int Kv = (g.sample_dims & 4) ? valid : g.Kd;
+    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+    if (m0 >= Mv || n0 >= Nv) return;
+    const int kbeg = slice * g.kchunk;
+    const int kend = min(Kv, kbeg + g.kchunk);
+    const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
+    const bool do_rowsum = (EPI == EPI_UPD) && g.ubias != nullptr && blockIdx.x == 0;
+    if (do_rowsum && tid < 64) rowsum[tid] = 0.f;
+
+    f4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+        if constexpr (A_KC) stage_kc<BF, TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+        else stage_nc<BF, TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+        if constexpr (B_KC) stage_kc<BF, TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+        else stage_nc<BF, TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+        __syncthreads();
+        if (do_rowsum && tid < 64) {
+            float s = 0.f;
+#pragma unroll
+            for (int k = 0; k < BK; ++k) s += (float)to_f<LT>(As[tid * LDK + k]);
+            rowsum[tid] += s;
+        }
+        const int rl = lane & 15, kg = lane >> 4;
+        if constexpr (!BF) {
+            f4 av[2], bv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) av[i] = *(const f4*)(As + (wm * 32 + i * 16 + rl) * LDK + kg * 4);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) bv[j] = *(const f4*)(Bs + (wn * 32 + j * 16 + rl) * LDK + kg * 4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][q], bv[j][q], acc[i][j], 0, 0, 0);
+        } else {
+            bf8v av[2], bv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) av[i] = *(const bf8v*)(As + (wm * 32 + i * 16 + rl) * LDK + kg * 8);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) bv[j] = *(const bf8v*)(Bs + (wn * 32 + j * 16 + rl) * LDK + kg * 8);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+
+    // epilogue: lane holds C rows 4*(lane/16)+r, column lane%16 of each 16x16 block
+    float scale = g.lr;
+    if (EPI == EPI_UPD && g.scale_per_batch) scale = valid > 0 ? g.lr / (float)valid : 0.f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + wm * 32 + i * 16 + (lane >> 4) * 4 + r;
+                const int n = n0 + wn * 32 + j * 16 + (lane & 15);
+                if (m >= Mv || n >= Nv) continue;
+                const float v = acc[i][j][r];
+                const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+                if constexpr (EPI == EPI_STORE) {
+                    ((float*)g.c)[ci + (size_t)slice * g.c_split] = v;
+                } else if constexpr (EPI == EPI_FWD) {
+                    const float zv = v + g.bias[(size_t)cn * g.bias_z + n];
+                    ((TO*)g.c)[ci] = from_f<TO>(act_fn(g.act, zv));
+                } else if constexpr (EPI == EPI_BWD) {
+                    const float x = to_f<TO>(((const TO*)g.aux)[ci]);
+                    ((TO*)g.c)[ci] = from_f<TO>(v * act_deriv(g.act, x));
+                } else {  // EPI_UPD: in-place W -= scale * acc (master fp32)
+                    float* W = (float*)g.c;
+                    const float w = W[ci] - scale * v;
+                    W[ci] = w;
+                    if (g.shadow) g.shadow[ci] = f2bf(w);
+                }
+            }
+    if (do_rowsum && tid < 64 && m0 + tid < Mv) {
+        float* b = g.ubias + (size_t)cn * g.bias_z;
+        b[m0 + tid] -= scale * rowsum[tid];
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Output layer, one wavefront per sample row: z = W x + b over <= 16 outputs, the output
+// activation (eq. (3), softmax eq. (5)), then either the output error (training, eq. (9)
+// or (10)) or the predicted class and the correct count (inference).
+
+struct RowArgs {
+    const void* x;  // input activations: xrows (data set) or workspace [z][rows][ld]
+    int x_xrows;
+    int64_t x_z, x_ld;
+    const void* w;  // W_L [O][H] (+ z * w_z): fp32 master or bf16 shadow
+    int64_t w_z;
+    const float* bias;  // b_L (+ z * bias_z)
+    int64_t bias_z;
+    int H, O, act, loss;
+    int64_t n_total;
+    int k_rep;
+    int64_t r0;
+    int step_rows;
+    const int32_t* y;  // labels (data-set rows)
+    void* delta;       // training: [z][rows][O] output error (TD)
+    int64_t d_z;
+    float* out;        // inference: [rows][O] outputs (nullable)
+    int32_t* pred;     // inference: [rows] argmax
+    unsigned long long* correct;  // inference: count of pred == y (nullable)
+};
+
+template <typename TX, typename TW, typename TD, bool TRAIN>
+__global__ __launch_bounds__(256) void out_layer_kernel(RowArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int z = blockIdx.z;
+    int64_t v = shard_len(a.n_total, a.k_rep, z) - a.r0;
+    const int valid = (int)(v < 0 ? 0 : (v > a.step_rows ? a.step_rows : v));
+    if (row >= valid) return;
+    const int64_t drow = shard_start(a.n_total, a.k_rep, z) + a.r0 + row;  // data-set row
+    const TX* x = a.x_xrows ? (const TX*)a.x + (size_t)drow * a.x_ld
+                            : (const TX*)a.x + (size_t)z * a.x_z + (size_t)row * a.x_ld;
+    const TW* W = (const TW*)a.w + (size_t)z * a.w_z;
+    float acc[MAX_OUT];
+#pragma unroll
+    for (int o = 0; o < MAX_OUT; ++o) acc[o] = 0.f;
+    for (int i = lane; i < a.H; i += 64) {
+        float xi = to_f<TX>(x[i]);
+        if constexpr (sizeof(TW) == 2 && sizeof(TX) == 4) xi = bf2f(f2bf(xi));  // bf16 operand
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o)
+            if (o < a.O) acc[o] += to_f<TW>(W[(size_t)o * a.H + i]) * xi;
+    }
+    const float* b = a.bias + (size_t)z * a.bias_z;
+    float zo[MAX_OUT], xo[MAX_OUT];
+#pragma unroll
+    for (int o = 0; o < MAX_OUT; ++o) zo[o] = (o < a.O) ? wave_sum(acc[o]) + b[o] : 0.f;
+    if (a.act == ACT_SOFTMAX) {
+        float m = zo[0];
+#pragma unroll
+        for (int o = 1; o < MAX_OUT; ++o) if (o < a.O) m = fmaxf(m, zo[o]);
+        float s = 0.f;
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) { xo[o] = (o < a.O) ? expf(zo[o] - m) : 0.f; s += xo[o]; }
+        const float inv = 1.0f / s;
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) xo[o] *= inv;
+    } else {
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) xo[o] = act_fn(a.act, zo[o]);
+    }
+    if constexpr (TRAIN) {
+        const int label = a.y[drow];
+        TD* d = (TD*)a.delta + (size_t)z * a.d_z + (size_t)row * a.O;
+        if (lane < a.O) {
+            float xv = 0.f;
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) if (o == lane) xv = xo[o];
+            const float e = (lane == label) ? 1.0f : 0.0f;
+            const float dv = (a.loss == LOSS_XENT) ? (xv - e) : (xv - e) * act_deriv(a.act, xv);
+            d[lane] = from_f<TD>(dv);
+        }
+    } else {
+        int best = 0;
+        float bv = xo[0];
+#pragma unroll
+        for (int o = 1; o < MAX_OUT; ++o) if (o < a.O && xo[o] > bv) { bv = xo[o]; best = o; }
+        if (lane == 0) {
+            a.pred[drow] = best;
+            if (a.correct && a.y && a.y[drow] == best) atomicAdd(a.correct, 1ull);
+        }
+        if (a.out && lane < a.O) {
+            float xv = 0.f;
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) if (o == lane) xv = xo[o];
+            a.out[(size_t)drow * a.O + lane] = xv;
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Hidden error behind a narrow layer (eq. (11)): d_l[r][i] = (sum_o d_{l+1}[r][o] W[o][i])
+// * phi'(x_l[r][i]), for a next layer of <= 16 neurons.  Thread per (row, i).
+
+struct BwdSmallArgs {
+    const void* dnext;  // [z][rows][O]
+    int64_t dn_z;
+    const void* w;      // W_{l+1} [O][H] (+ z * w_z)
+    int64_t w_z;
+    const void* x;      // x_l [z][rows][H]
+    void* d;            // d_l [z][rows][H]
+    int64_t xz;         // z stride of x and d
+    int H, O, act;
+    int64_t n_total;
+    int k_rep;
+    int64_t r0;
+    int step_rows;
+};
+
+template <typename TD, typename TW>
+__global__ __launch_bounds__(256) void bwd_small_kernel(BwdSmallArgs a) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int row = blockIdx.y, z = blockIdx.z;
+    int64_t v = shard_len(a.n_total, a.k_rep, z) - a.r0;
+    const int valid = (int)(v < 0 ? 0 : (v > a.step_rows ? a.step_rows : v));
+    if (row >= valid || i >= a.H) return;
+    const TD* dn = (const TD*)a.dnext + (size_t)z * a.dn_z + (size_t)row * a.O;
+    const TW* W = (const TW*)a.w + (size_t)z * a.w_z;
+    float s = 0.f;
+    for (int o = 0; o < a.O; ++o) s += to_f<TD>(dn[o]) * to_f<TW>(W[(size_t)o * a.H + i]);
+    const size_t xi = (size_t)z * a.xz + (size_t)row * a.H + i;
+    const float x = to_f<TD>(((const TD*)a.x)[xi]);
+    ((TD*)a.d)[xi] = from_f<TD>(s * act_deriv(a.act, x));
+}
+
+// ------------------------------------------------------------------------------------
+// Update of a narrow layer (<= 16 neurons), eq. (12)-(13) averaged over the batch:
+// W[o][i] -= lr / B_t * sum_r d[r][o] x[r][i];  b[o] -= lr / B_t * sum_r d[r][o].
+// Thread per input column i, all outputs in registers.
+
+struct UpdSmallArgs {
+    const void* d;  // [z][rows][O]
+    int64_t d_z;
+    const void* x;  // previous activations: xrows (data set) or [z][rows][H]
+    int x_xrows;
+    int64_t x_z, x_ld;
+    float* w;       // W [O][H] (+ z * w_z), fp32 master
+    bf16_t* shadow; // nullable, same indexing as w
+    float* bias;    // b [O] (+ z * bias_z)
+    int64_t w_z, bias_z;
+    int H, O;
+    float lr;
+    int64_t n_total;
+    int k_rep;
+    int64_t r0;
+    int step_rows;
+};
+
+template <typename TD, typename TX>
+__global__ __launch_bounds__(256) void upd_small_kernel(UpdSmallArgs a) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int z = blockIdx.z;
+    int64_t v = shard_len(a.n_total, a.k_rep, z) - a.r0;
+    const int valid = (int)(v < 0 ? 0 : (v > a.step_rows ? a.step_rows : v));
+    if (valid == 0) return;
+    const float scale = a.lr / (float)valid;
+    const TD* d = (const TD*)a.d + (size_t)z * a.d_z;
+    const int64_t xb = shard_start(a.n_total, a.k_rep, z) + a.r0;
+    if (i < a.H) {
+        float acc[MAX_OUT];
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) acc[o] = 0.f;
+        for (int r = 0; r < valid; ++r) {
+            const TX* xr = a.x_xrows ? (const TX*)a.x + (size_t)(xb + r) * a.x_ld
+                                     : (const TX*)a.x + (size_t)z * a.x_z + (size_t)r * a.x_ld;
+            float xv = to_f<TX>(xr[i]);
+            if constexpr (sizeof(TD) == 2 && sizeof(TX) == 4) xv = bf2f(f2bf(xv));  // bf16 operand
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o)
+                if (o < a.O) acc[o] += to_f<TD>(d[(size_t)r * a.O + o]) * xv;
+        }
+        float* W = a.w + (size_t)z * a.w_z;
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o)
+            if (o < a.O) {
+                const size_t wi = (size_t)o * a.H + i;
+                const float w = W[wi] - scale * acc[o];
+                W[wi] = w;
+                if (a.shadow) a.shadow[(size_t)z * a.w_z + wi] = f2bf(w);
+            }
+    }
+    if (blockIdx.x == 0 && threadIdx.x < a.O) {
+        const int o = threadIdx.x;
+        float s = 0.f;
+        for (int r = 0; r < valid; ++r) s += to_f<TD>(d[(size_t)r * a.O + o]);
+        a.bias[(size_t)z * a.bias_z + o] -= scale * s;
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Combination by averaging: merged[p] = (sum_k theta_k[p]) / K with the sum in fp64 and k
+// ascending; optionally broadcast back to every CN; bf16 shadows refreshed.  Four
+// consecutive parameters per thread.
+
+struct MergeArgs {
+    float* theta;       // [K][pstride]
+    float* merged;      // [pstride]
+    bf16_t* shadow;     // [K][pstride] or null
+    bf16_t* mshadow;    // [pstride] or null
+    int64_t pstride;    // multiple of 4
+    int K;
+    int broadcast;
+};
+
+__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
+    const int64_t p = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (p >= a.pstride) return;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    for (int k = 0; k < a.K; ++k) {
+        const float4 v = *(const float4*)(a.theta + (size_t)k * a.pstride + p);
+        s0 += (double)v.x; s1 += (double)v.y; s2 += (double)v.z; s3 += (double)v.w;
+    }
+    const double inv = (double)a.K;
+    const float4 m = make_float4((float)(s0 / inv), (float)(s1 / inv), (float)(s2 / inv), (float)(s3 / inv));
+    *(float4*)(a.merged + p) = m;
+    if (a.mshadow) {
+        a.mshadow[p] = f2bf(m.x); a.mshadow[p + 1] = f2bf(m.y); a.mshadow[p + 2] = f2bf(m.z); a.mshadow[p + 3] = f2bf(m.w);
+    }
+    if (a.broadcast) {
+        for (int k = 0; k < a.K; ++k) {
+            *(float4*)(a.theta + (size_t)k * a.pstride + p) = m;
+            if (a.shadow) {
+                bf16_t* s = a.shadow + (size_t)k * a.pstride + p;
+                s[0] = f2bf(m.x); s[1] = f2bf(m.y); s[2] = f2bf(m.z); s[3] = f2bf(m.w);
+            }
+        }
+    }
+}
+
+// fp32 -> bf16 copy of a whole parameter block (shadow refresh after init / set)
+__global__ __launch_bounds__(256) void to_bf16_kernel(const float* src, bf16_t* dst, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) dst[i] = f2bf(src[i]);
+}
+
+// ------------------------------------------------------------------------------------
+// Per-sample stochastic gradient descent of a one-hidden-layer network, chunked.
+//
+// Within a chunk of T consecutive samples t of one CN, the first-layer weights evolve as
+// W1_t = W1_c - eta * sum_{s<t} d1_s x_s^T (W1_c: weights at the chunk start), so the
+// first-layer input sum is exactly
+//     z1_t = W1_t x_t + b1_t = P[t] + b1_t - eta * sum_{s<t} d1_s (x_s . x_t)
+// with P[t] = W1_c x_t and the Gram matrix G[t][s] = x_s . x_t computed on the matrix
+// cores beforehand.  This kernel runs the T sequential steps of one CN per workgroup:
+// the small second layer (W2, b2) and b1 are updated in registers after every sample,
+// exactly as eq. (12)-(13) prescribe, and the first-layer errors d1_t are written out so
+// that the rank-T update of W1 (= the T rank-1 updates summed) is one more GEMM.
+// Thread h owns hidden neuron h and column h of W2.
+
+struct PsgdArgs {
+    float* theta;         // [K][pstride]
+    int64_t pstride, off_b1, off_w2, off_b2;
+    const float* ppart;   // split partial sums of P: [ksplit][K][T][H]
+    int ksplit;
+    int64_t ppart_split;  // elements between splits
+    const float* gram;    // [K][nch][T][T]
+    int nch, c;           // number of chunks, this chunk
+    const int32_t* y;     // data-set labels
+    float* d1;            // out: [K][T][H]
+    int64_t n_total;
+    int k_rep;
+    int H, O, act1, act2, loss;
+    float lr;
+};
+
+template <int T>
+__global__ __launch_bounds__(1024) void psgd_chunk_kernel(PsgdArgs a) {
+    extern __shared__ float smem[];
+    const int z = blockIdx.x;
+    const int h = threadIdx.x, lane = h & 63, wave = h >> 6, nwaves = blockDim.x >> 6;
+    const bool live = h < a.H;
+    const int64_t nz = shard_len(a.n_total, a.k_rep, z);
+    const int64_t r0 = (int64_t)a.c * T;
+    const int tc = (int)(nz - r0 < 0 ? 0 : (nz - r0 > T ? T : nz - r0));
+    if (tc == 0) return;
+    const int H = a.H, O = a.O;
+    float* Pl = smem;                       // [T][H]
+    float* hist = smem + T * H;             // [T][H]
+    float* red = smem + 2 * T * H;          // [2][16 waves][MAX_OUT]
+
+    // sum the split partials of P = W1_c x_t
+    for (int idx = threadIdx.x; idx < tc * H; idx += blockDim.x) {
+        const int t = idx / H, hh = idx % H;
+        float s = 0.f;
+        for (int sp = 0; sp < a.ksplit; ++sp)
+            s += a.ppart[(size_t)sp * a.ppart_split + ((size_t)z * T + t) * H + hh];
+        Pl[t * H + hh] = s;
+    }
+    __syncthreads();
+
+    float* th = a.theta + (size_t)z * a.pstride;
+    float b1 = live ? th[a.off_b1 + h] : 0.f;
+    float w2[MAX_OUT], b2[MAX_OUT];
+#pragma unroll
+    for (int o = 0; o < MAX_OUT; ++o) {
+        w2[o] = (live && o < O) ? th[a.off_w2 + (size_t)o * H + h] : 0.f;
+        b2[o] = (o < O) ? th[a.off_b2 + o] : 0.f;
+    }
+    const float* G = a.gram + ((size_t)z * a.nch + a.c) * T * T;
+    const int32_t* y = a.y + shard_start(a.n_total, a.k_rep, z) + r0;
+    float* dout = a.d1 + (size_t)z * T * H;
+    const float lr = a.lr;
+
+    for (int t = 0; t < tc; ++t) {
+        float a1 = 0.f;
+        if (live) {
+            float corr = 0.f;
+            const float* Gt = G + (size_t)t * T;
+            for (int s = 0; s < t; ++s) corr += hist[s * H + h] * Gt[s];
+            const float z1 = Pl[t * H + h] + b1 - lr * corr;
+            a1 = act_fn(a.act1, z1);
+        }
+        float zo[MAX_OUT];
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) zo[o] = wave_sum(w2[o] * a1);
+        float* rb = red + (t & 1) * 16 * MAX_OUT;
+        if (lane == 0) {
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) rb[wave * MAX_OUT + o] = zo[o];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) {
+            float s = 0.f;
+            for (int w = 0; w < nwaves; ++w) s += rb[w * MAX_OUT + o];
+            zo[o] = s + b2[o];
+        }
+        // output activation and error (eq. (3), (5), (9), (10))
+        float xo[MAX_OUT];
+        if (a.act2 == ACT_SOFTMAX) {
+            float m = zo[0];
+#pragma unroll
+            for (int o = 1; o < MAX_OUT; ++o) if (o < O) m = fmaxf(m, zo[o]);
+            float s = 0.f;
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) { xo[o] = (o < O) ? expf(zo[o] - m) : 0.f; s += xo[o]; }
+            const float inv = 1.0f / s;
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) xo[o] *= inv;
+        } else {
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) xo[o] = act_fn(a.act2, zo[o]);
+        }
+        const int label = y[t];
+        float d2[MAX_OUT];
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) {
+            const float e = (o == label) ? 1.0f : 0.0f;
+            d2[o] = (o < O) ? ((a.loss == LOSS_XENT) ? (xo[o] - e) : (xo[o] - e) * act_deriv(a.act2, xo[o])) : 0.f;
+        }
+        // hidden error with the pre-update W2 (eq. (11)), then the updates (eq. (12)-(13))
+        float back = 0.f;
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) back += w2[o] * d2[o];
+        const float d1 = live ? back * act_deriv(a.act1, a1) : 0.f;
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) {
+            w2[o] -= lr * d2[o] * a1;
+            b2[o] -= lr * d2[o];
+        }
+        if (live) {
+            b1 -= lr * d1;
+            hist[t * H + h] = d1;
+            dout[(size_t)t * H + h] = d1;
+        }
+    }
+    if (live) {
+        th[a.off_b1 + h] = b1;
+        for (int o = 0; o < O; ++o) th[a.off_w2 + (size_t)o * H + h] = w2[o];
+    }
+    if (h == 0)
+        for (int o = 0; o < O; ++o) th[a.off_b2 + o] = b2[o];
+}
+
+}  // namespace pnn

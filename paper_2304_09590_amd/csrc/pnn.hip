@@ -1,0 +1,758 @@
+// pnn.hip -- host orchestration and C ABI of the MI355X PNN library (declared in pnn.h).
+//
+// Device layout: every network (each of the K CNs and the merged one) is a padded
+// parameter block of `pstride` floats; W_l and b_l start at 64-float (256-byte) aligned
+// offsets, so every row of every matrix can be read with 16-byte loads.  The K CN blocks
+// are contiguous ([K][pstride]).  In bf16-mixed precision a bf16 shadow of every block
+// ([K][pstride] plus one for the merged network) holds the weights used as GEMM operands.
+//
+// Training plans:
+//  * per-sample SGD of a one-hidden-layer fp32 network (B = 1, L = 2, hidden <= 1024,
+//    outputs <= 16): chunked plan -- Gram matrices of each chunk of T samples, then per
+//    chunk P = W1 x_t (GEMM), the T sequential steps (psgd_chunk_kernel), and the rank-T
+//    update of W1 (GEMM).
+//  * everything else: mini-batch plan -- per batch step, forward GEMMs with fused bias and
+//    activation, output layer with fused output error, hidden errors (GEMM with fused
+//    phi'), and weight-gradient GEMMs with the SGD update (and bias update) fused into the
+//    epilogue.  B = 1 runs this plan with batches of one sample.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../include/pnn.h"
+#include "kernels.hpp"
+
+using namespace pnn;
+
+namespace {
+
+thread_local std::string g_init_error;
+
+struct ProfRec {
+    const char* name;
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct pnn_net {
+    pnn_config cfg;
+    int L = 0;
+    int sizes[9] = {0};
+    int act[8] = {0};
+    int64_t P = 0;        // packed parameters per network
+    int64_t pstride = 0;  // padded block
+    int64_t off_w[8] = {0}, off_b[8] = {0};
+    bool bf16 = false;
+    int device = 0;
+    bool broken = false;
+    std::string err;
+
+    float* theta = nullptr;    // [K][pstride]
+    float* merged = nullptr;   // [pstride]
+    bf16_t* shadow = nullptr;  // [K][pstride]
+    bf16_t* mshadow = nullptr; // [pstride]
+
+    // mini-batch workspace: activations x_l (l = 1..L-1) and errors d_l (l = 1..L), [K][B][s_l]
+    void* act_ws[9] = {nullptr};
+    void* del_ws[9] = {nullptr};
+    // inference workspace: [rows][s_l], l = 1..L-1
+    void* inf_ws[9] = {nullptr};
+    int inf_rows = 0;
+    unsigned long long* d_correct = nullptr;
+
+    // chunked per-sample plan
+    bool psgd = false;
+    int T = 0, ksplit = 1, kchunk = 0;
+    float* ppart = nullptr;  // [ksplit][K][T][H]
+    float* d1 = nullptr;     // [K][T][H]
+    float* gram = nullptr;   // [K][nch][T][T]
+    size_t gram_elems = 0;
+
+    // profiling
+    bool prof = false;
+    std::vector<ProfRec> pending;
+    std::vector<hipEvent_t> free_events;
+    std::map<std::string, std::pair<double, int64_t>> prof_acc;
+    std::vector<std::string> prof_names_store;
+};
+
+namespace {
+
+pnn_status fail(pnn_net* n, pnn_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (n) n->err = buf;
+    else g_init_error = buf;
+    return s;
+}
+
+#define HIP_TRY(net, call)                                                                         \
+    do {                                                                                           \
+        hipError_t e_ = (call);                                                                    \
+        if (e_ != hipSuccess) {                                                                    \
+            if (net) (net)->broken = true;                                                         \
+            return fail(net, PNN_EHIP, "%s failed: %s", #call, hipGetErrorString(e_));            \
+        }                                                                                          \
+    } while (0)
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+pnn_status check_config(const pnn_config* c, std::string* why) {
+    auto bad = [&](const char* m) { if (why) *why = m; return PNN_EINVAL; };
+    if (!c) return bad("config is NULL");
+    if (c->n_layers < 1 || c->n_layers > 8) return bad("n_layers must be in 1..8");
+    for (int l = 0; l <= c->n_layers; ++l)
+        if (c->sizes[l] < 1) return bad("every layer size must be >= 1");
+    for (int l = 0; l < c->n_layers; ++l)
+        if (c->sizes[l] % 8 != 0) return bad("input and hidden layer sizes must be multiples of 8");
+    if (c->sizes[c->n_layers] > MAX_OUT) return bad("the output layer may have at most 16 neurons");
+    for (int l = 0; l < c->n_layers; ++l) {
+        if (c->act[l] < 0 || c->act[l] > 4) return bad("unknown activation");
+        if (c->act[l] == PNN_SOFTMAX && l != c->n_layers - 1) return bad("softmax is allowed on the output layer only");
+    }
+    const int out_act = c->act[c->n_layers - 1];
+    if (c->loss != PNN_LOSS_MSE && c->loss != PNN_LOSS_XENT) return bad("unknown loss");
+    if (out_act == PNN_SOFTMAX && c->loss != PNN_LOSS_XENT) return bad("a softmax output needs the cross-entropy loss");
+    if (c->loss == PNN_LOSS_XENT && out_act != PNN_SOFTMAX && out_act != PNN_SIGMOID)
+        return bad("the cross-entropy loss needs a sigmoid or softmax output");
+    if (c->precision != PNN_FP32 && c->precision != PNN_BF16_MIXED) return bad("unknown precision");
+    if (c->replicas < 1) return bad("replicas must be >= 1");
+    if (c->batch < 1) return bad("batch must be >= 1");
+    if (!std::isfinite(c->lr) || c->lr < 0.0f) return bad("lr must be finite and >= 0");
+    return PNN_OK;
+}
+
+int64_t packed_count(const pnn_config* c) {
+    int64_t p = 0;
+    for (int l = 0; l < c->n_layers; ++l) p += (int64_t)c->sizes[l + 1] * c->sizes[l] + c->sizes[l + 1];
+    return p;
+}
+
+template <typename T>
+pnn_status dev_alloc(pnn_net* n, T** p, size_t elems) {
+    if (elems == 0) elems = 1;
+    hipError_t e = hipMalloc((void**)p, elems * sizeof(T));
+    if (e != hipSuccess) {
+        *p = nullptr;
+        return fail(n, PNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", elems * sizeof(T), hipGetErrorString(e));
+    }
+    e = hipMemset(*p, 0, elems * sizeof(T));
+    if (e != hipSuccess) return fail(n, PNN_EHIP, "hipMemset failed: %s", hipGetErrorString(e));
+    return PNN_OK;
+}
+
+// ---------------------------------------------------------------------------------------
+// profiling hooks
+
+void prof_begin(pnn_net* n, hipStream_t s, hipEvent_t* ev) {
+    if (!n->prof) return;
+    if (n->free_events.empty()) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) { *ev = nullptr; return; }
+        n->free_events.push_back(e);
+    }
+    *ev = n->free_events.back();
+    n->free_events.pop_back();
+    (void)hipEventRecord(*ev, s);
+}
+void prof_end(pnn_net* n, hipStream_t s, hipEvent_t a, const char* name) {
+    if (!n->prof || !a) return;
+    if (n->free_events.empty()) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        n->free_events.push_back(e);
+    }
+    hipEvent_t b = n->free_events.back();
+    n->free_events.pop_back();
+    (void)hipEventRecord(b, s);
+    n->pending.push_back({name, a, b});
+}
+void prof_drain(pnn_net* n) {
+    for (auto& r : n->pending) {
+        (void)hipEventSynchronize(r.b);
+        float ms = 0.f;
+        (void)hipEventElapsedTime(&ms, r.a, r.b);
+        auto& acc = n->prof_acc[r.name];
+        acc.first += ms;
+        acc.second += 1;
+        n->free_events.push_back(r.a);
+        n->free_events.push_back(r.b);
+    }
+    n->pending.clear();
+}
+
+// ---------------------------------------------------------------------------------------
+// launch helpers
+
+struct Launch {
+    pnn_net* n;
+    hipStream_t s;
+    hipEvent_t ev = nullptr;
+    const char* name;
+    Launch(pnn_net* n_, hipStream_t s_, const char* nm) : n(n_), s(s_), name(nm) { prof_begin(n, s, &ev); }
+    pnn_status done() {
+        hipError_t e = hipGetLastError();
+        prof_end(n, s, ev, name);
+        if (e != hipSuccess) {
+            n->broken = true;
+            return fail(n, PNN_EHIP, "launch of %s failed: %s", name, hipGetErrorString(e));
+        }
+        return PNN_OK;
+    }
+};
+
+GemmArgs gemm_base(const pnn_net* n, int M, int N, int Kd, int64_t n_total, int64_t r0, int step_rows, int sample_dims) {
+    GemmArgs g;
+    memset(&g, 0, sizeof g);
+    g.M = M; g.N = N; g.Kd = Kd;
+    g.n_total = n_total;
+    g.k_rep = n->cfg.replicas;
+    g.zdiv = 1;
+    g.r0_base = r0;
+    g.r0_step = 0;
+    g.step_rows = step_rows;
+    g.sample_dims = sample_dims;
+    g.ksplit = 1;
+    g.kchunk = 1 << 30;
+    return g;
+}
+
+template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO>
+pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const char* name) {
+    // shapes the kernel assumes: 16-byte loads along contiguous dimensions
+    const int vec = BF ? 8 : 4;
+    if ((A_KC || B_KC) && (g.sample_dims & 4) == 0 && g.Kd % vec != 0)
+        return fail(n, PNN_EINVAL, "%s: contraction length %d is not a multiple of %d", name, g.Kd, vec);
+    if (g.kchunk % GemmTile<BF>::BK != 0 && g.ksplit > 1)
+        return fail(n, PNN_EINVAL, "%s: split chunk %d is not a multiple of the tile depth", name, g.kchunk);
+    if ((!A_KC && g.M % 4 != 0) || (!B_KC && g.N % 4 != 0))
+        return fail(n, PNN_EINVAL, "%s: M=%d / N=%d not a multiple of 4", name, g.M, g.N);
+    // 4-wide loads run along columns of NC operands and along k of KC operands: none of
+    // those may be a dimension cut to the rows of a step
+    if ((!A_KC && (g.sample_dims & 1)) || (!B_KC && (g.sample_dims & 2)) || ((A_KC || B_KC) && (g.sample_dims & 4)))
+        return fail(n, PNN_EINVAL, "%s: vector loads along a sample dimension", name);
+    dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, (unsigned)(Z * g.ksplit));
+    if (grid.x == 0 || grid.y == 0 || grid.z == 0 || grid.y > 65535 || grid.z > 65535)
+        return fail(n, PNN_EINVAL, "%s: bad grid %u x %u x %u", name, grid.x, grid.y, grid.z);
+    Launch l(n, s, name);
+    gemm_kernel<BF, TA, TB, A_KC, B_KC, EPI, TO><<<grid, 256, 0, s>>>(g);
+    return l.done();
+}
+
+Operand opnd(const void* p, int64_t zs, int64_t ld, int xrows) {
+    Operand o;
+    o.ptr = p; o.zstride = zs; o.ld = ld; o.xrows = xrows;
+    return o;
+}
+
+#define TRY(x) do { pnn_status st_ = (x); if (st_ != PNN_OK) return st_; } while (0)
+
+// ---------------------------------------------------------------------------------------
+// mini-batch plan: one batch step of every CN
+
+template <bool BF>
+pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t N, int64_t r0, hipStream_t s) {
+    typedef typename std::conditional<BF, bf16_t, float>::type TH;  // hidden activations / errors
+    const int L = n->L, B = n->cfg.batch, K = n->cfg.replicas;
+    const int64_t ps = n->pstride;
+    const void* Wop = BF ? (const void*)n->shadow : (const void*)n->theta;  // operand weights
+    const int64_t wz = ps;
+
+    // forward, hidden layers (eq. (2)-(3))
+    for (int l = 1; l <= L - 1; ++l) {
+        GemmArgs g = gemm_base(n, B, n->sizes[l], n->sizes[l - 1], N, r0, B, 1);
+        if (l == 1) g.a = opnd(X, 0, n->sizes[0], 1);
+        else g.a = opnd(n->act_ws[l - 1], (int64_t)B * n->sizes[l - 1], n->sizes[l - 1], 0);
+        g.b = opnd((const char*)Wop + n->off_w[l - 1] * (BF ? 2 : 4), wz, n->sizes[l - 1], 0);
+        g.c = n->act_ws[l]; g.c_z = (int64_t)B * n->sizes[l]; g.c_ld = n->sizes[l];
+        g.bias = n->theta + n->off_b[l - 1]; g.bias_z = ps;
+        g.act = n->act[l - 1];
+        if (l == 1) TRY((run_gemm<BF, float, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
+        else TRY((run_gemm<BF, TH, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
+    }
+    // output layer and output error (eq. (3), (5), (9)-(10))
+    {
+        RowArgs a;
+        memset(&a, 0, sizeof a);
+        if (L == 1) { a.x = X; a.x_xrows = 1; a.x_ld = n->sizes[0]; }
+        else { a.x = n->act_ws[L - 1]; a.x_z = (int64_t)B * n->sizes[L - 1]; a.x_ld = n->sizes[L - 1]; }
+        a.w = (const char*)Wop + n->off_w[L - 1] * (BF ? 2 : 4); a.w_z = wz;
+        a.bias = n->theta + n->off_b[L - 1]; a.bias_z = ps;
+        a.H = n->sizes[L - 1]; a.O = n->sizes[L]; a.act = n->act[L - 1]; a.loss = n->cfg.loss;
+        a.n_total = N; a.k_rep = K; a.r0 = r0; a.step_rows = B;
+        a.y = Y;
+        a.delta = n->del_ws[L]; a.d_z = (int64_t)B * n->sizes[L];
+        dim3 grid((B + 3) / 4, 1, K);
+        Launch lc(n, s, "out_layer");
+        if (L == 1) out_layer_kernel<float, TH, TH, true><<<grid, 256, 0, s>>>(a);
+        else out_layer_kernel<TH, TH, TH, true><<<grid, 256, 0, s>>>(a);
+        TRY(lc.done());
+    }
+    // hidden errors, back to front, with the pre-update weights (eq. (11))
+    for (int l = L - 1; l >= 1; --l) {
+        const int Hl = n->sizes[l], On = n->sizes[l + 1];
+        if (On <= MAX_OUT) {
+            BwdSmallArgs a;
+            memset(&a, 0, sizeof a);
+            a.dnext = n->del_ws[l + 1]; a.dn_z = (int64_t)B * On;
+            a.w = (const char*)Wop + n->off_w[l] * (BF ? 2 : 4); a.w_z = wz;
+            a.x = n->act_ws[l]; a.d = n->del_ws[l]; a.xz = (int64_t)B * Hl;
+            a.H = Hl; a.O = On; a.act = n->act[l - 1];
+            a.n_total = N; a.k_rep = K; a.r0 = r0; a.step_rows = B;
+            dim3 grid((Hl + 255) / 256, B, K);
+            Launch lc(n, s, "bwd_small");
+            bwd_small_kernel<TH, TH><<<grid, 256, 0, s>>>(a);
+            TRY(lc.done());
+        } else {
+            GemmArgs g = gemm_base(n, B, Hl, On, N, r0, B, 1);
+            g.a = opnd(n->del_ws[l + 1], (int64_t)B * On, On, 0);
+            g.b = opnd((const char*)Wop + n->off_w[l] * (BF ? 2 : 4), wz, Hl, 0);
+            g.c = n->del_ws[l]; g.c_z = (int64_t)B * Hl; g.c_ld = Hl;
+            g.aux = n->act_ws[l];
+            g.act = n->act[l - 1];
+            TRY((run_gemm<BF, TH, TH, true, false, EPI_BWD, TH>(n, s, g, K, "bwd_gemm")));
+        }
+    }
+    // updates, eq. (12)-(13) averaged over the batch
+    for (int l = 1; l <= L; ++l) {
+        const int In = n->sizes[l - 1], Out = n->sizes[l];
+        if (Out <= MAX_OUT) {
+            UpdSmallArgs a;
+            memset(&a, 0, sizeof a);
+            a.d = n->del_ws[l]; a.d_z = (int64_t)B * Out;
+            if (l == 1) { a.x = X; a.x_xrows = 1; a.x_ld = In; }
+            else { a.x = n->act_ws[l - 1]; a.x_z = (int64_t)B * In; a.x_ld = In; }
+            a.w = n->theta + n->off_w[l - 1]; a.w_z = ps;
+            a.shadow = BF ? n->shadow + n->off_w[l - 1] : nullptr;
+            a.bias = n->theta + n->off_b[l - 1]; a.bias_z = ps;
+            a.H = In; a.O = Out; a.lr = n->cfg.lr;
+            a.n_total = N; a.k_rep = K; a.r0 = r0; a.step_rows = B;
+            dim3 grid((In + 255) / 256, 1, K);
+            Launch lc(n, s, "upd_small");
+            if (l == 1) upd_small_kernel<TH, float><<<grid, 256, 0, s>>>(a);
+            else upd_small_kernel<TH, TH><<<grid, 256, 0, s>>>(a);
+            TRY(lc.done());
+        } else {
+            GemmArgs g = gemm_base(n, Out, In, B, N, r0, B, 4);
+            g.a = opnd(n->del_ws[l], (int64_t)B * Out, Out, 0);
+            if (l == 1) g.b = opnd(X, 0, In, 1);
+            else g.b = opnd(n->act_ws[l - 1], (int64_t)B * In, In, 0);
+            g.c = n->theta + n->off_w[l - 1]; g.c_z = ps; g.c_ld = In;
+            g.ubias = n->theta + n->off_b[l - 1]; g.bias_z = ps;
+            g.lr = n->cfg.lr; g.scale_per_batch = 1;
+            g.shadow = BF ? n->shadow + n->off_w[l - 1] : nullptr;
+            if (l == 1) TRY((run_gemm<BF, TH, float, false, false, EPI_UPD, float>(n, s, g, K, "upd_gemm")));
+            else TRY((run_gemm<BF, TH, TH, false, false, EPI_UPD, float>(n, s, g, K, "upd_gemm")));
+        }
+    }
+    return PNN_OK;
+}
+
+// ---------------------------------------------------------------------------------------
+// chunked per-sample plan
+
+pnn_status psgd_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
+    const int K = n->cfg.replicas, T = n->T, H = n->sizes[1], In = n->sizes[0];
+    const int64_t nmax = shard_len(N, K, 0);
+    const int nch = (int)((nmax + T - 1) / T);
+    const size_t need = (size_t)K * nch * T * T;
+    if (need > n->gram_elems) {
+        if (n->gram) (void)hipFree(n->gram);
+        n->gram = nullptr;
+        n->gram_elems = 0;
+        TRY(dev_alloc(n, &n->gram, need));
+        n->gram_elems = need;
+    }
+    // Gram matrices of every chunk: G[t][s] = x_t . x_s
+    {
+        GemmArgs g = gemm_base(n, T, T, In, N, 0, T, 3);
+        g.a = opnd(X, 0, In, 1);
+        g.b = opnd(X, 0, In, 1);
+        g.zdiv = nch; g.r0_step = T;
+        g.c = n->gram; g.c_z = (int64_t)T * T; g.c_ld = T;
+        TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K * nch, "psgd_gram")));
+    }
+    auto run_p = [&](int c) -> pnn_status {
+        GemmArgs g = gemm_base(n, T, H, In, N, (int64_t)c * T, T, 1);
+        g.a = opnd(X, 0, In, 1);
+        g.b = opnd(n->theta + n->off_w[0], n->pstride, In, 0);
+        g.c = n->ppart; g.c_z = (int64_t)T * H; g.c_ld = H;
+        g.ksplit = n->ksplit; g.kchunk = n->kchunk; g.c_split = (int64_t)K * T * H;
+        return run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K, "psgd_p");
+    };
+    TRY(run_p(0));
+    const int threads = (int)round_up(H, 64);
+    const size_t smem = (size_t)(2 * T * H + 2 * 16 * MAX_OUT) * sizeof(float);
+    for (int c = 0; c < nch; ++c) {
+        PsgdArgs a;
+        memset(&a, 0, sizeof a);
+        a.theta = n->theta; a.pstride = n->pstride;
+        a.off_b1 = n->off_b[0]; a.off_w2 = n->off_w[1]; a.off_b2 = n->off_b[1];
+        a.ppart = n->ppart; a.ksplit = n->ksplit; a.ppart_split = (int64_t)K * T * H;
+        a.gram = n->gram; a.nch = nch; a.c = c;
+        a.y = Y; a.d1 = n->d1;
+        a.n_total = N; a.k_rep = K;
+        a.H = H; a.O = n->sizes[2]; a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
+        a.lr = n->cfg.lr;
+        {
+            Launch lc(n, s, "psgd_chunk");
+            switch (T) {
+            case 128: psgd_chunk_kernel<128><<<K, threads, smem, s>>>(a); break;
+            case 64: psgd_chunk_kernel<64><<<K, threads, smem, s>>>(a); break;
+            case 32: psgd_chunk_kernel<32><<<K, threads, smem, s>>>(a); break;
+            default: psgd_chunk_kernel<16><<<K, threads, smem, s>>>(a); break;
+            }
+            TRY(lc.done());
+        }
+        // W1 -= eta * sum_t d1_t x_t^T  (the chunk's T rank-1 updates)
+        {
+            GemmArgs g = gemm_base(n, H, In, T, N, (int64_t)c * T, T, 4);
+            g.a = opnd(n->d1, (int64_t)T * H, H, 0);
+            g.b = opnd(X, 0, In, 1);
+            g.c = n->theta + n->off_w[0]; g.c_z = n->pstride; g.c_ld = In;
+            g.lr = n->cfg.lr; g.scale_per_batch = 0;
+            TRY((run_gemm<false, float, float, false, false, EPI_UPD, float>(n, s, g, K, "psgd_upd")));
+        }
+        if (c + 1 < nch) TRY(run_p(c + 1));
+    }
+    return PNN_OK;
+}
+
+pnn_status refresh_shadows(pnn_net* n, hipStream_t s) {
+    if (!n->bf16) return PNN_OK;
+    const int64_t tot = (int64_t)n->cfg.replicas * n->pstride;
+    {
+        Launch l(n, s, "to_bf16");
+        to_bf16_kernel<<<(unsigned)((tot + 255) / 256), 256, 0, s>>>(n->theta, n->shadow, tot);
+        TRY(l.done());
+    }
+    Launch l(n, s, "to_bf16");
+    to_bf16_kernel<<<(unsigned)((n->pstride + 255) / 256), 256, 0, s>>>(n->merged, n->mshadow, n->pstride);
+    return l.done();
+}
+
+void pack(const pnn_net* n, const float* padded, float* flat) {
+    int64_t o = 0;
+    for (int l = 0; l < n->L; ++l) {
+        const int64_t nw = (int64_t)n->sizes[l + 1] * n->sizes[l];
+        memcpy(flat + o, padded + n->off_w[l], nw * sizeof(float));
+        o += nw;
+        memcpy(flat + o, padded + n->off_b[l], n->sizes[l + 1] * sizeof(float));
+        o += n->sizes[l + 1];
+    }
+}
+void unpack(const pnn_net* n, const float* flat, float* padded) {
+    memset(padded, 0, n->pstride * sizeof(float));
+    int64_t o = 0;
+    for (int l = 0; l < n->L; ++l) {
+        const int64_t nw = (int64_t)n->sizes[l + 1] * n->sizes[l];
+        memcpy(padded + n->off_w[l], flat + o, nw * sizeof(float));
+        o += nw;
+        memcpy(padded + n->off_b[l], flat + o, n->sizes[l + 1] * sizeof(float));
+        o += n->sizes[l + 1];
+    }
+}
+
+void free_all(pnn_net* n) {
+    auto f = [](void* p) { if (p) (void)hipFree(p); };
+    f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
+    for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
+    f(n->d_correct); f(n->ppart); f(n->d1); f(n->gram);
+    for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+    for (auto e : n->free_events) (void)hipEventDestroy(e);
+}
+
+pnn_status usable(pnn_net* n) {
+    if (!n) return PNN_EINVAL;
+    if (n->broken) return fail(n, PNN_ESTATE, "the handle is unusable after an earlier device failure");
+    int dev = -1;
+    (void)hipGetDevice(&dev);
+    if (dev != n->device) HIP_TRY(n, hipSetDevice(n->device));
+    return PNN_OK;
+}
+
+}  // namespace
+
+// =======================================================================================
+// C ABI
+
+extern "C" {
+
+pnn_status pnn_config_check(const pnn_config* cfg) { return check_config(cfg, nullptr); }
+
+int64_t pnn_param_count(const pnn_config* cfg) {
+    if (check_config(cfg, nullptr) != PNN_OK) return 0;
+    return packed_count(cfg);
+}
+
+pnn_status pnn_shard(int64_t N, int32_t K, int32_t k, int64_t* start, int64_t* len) {
+    if (!start || !len || K < 1 || k < 0 || k >= K || N < 0) return PNN_EINVAL;
+    *start = shard_start(N, K, k);
+    *len = shard_len(N, K, k);
+    return PNN_OK;
+}
+
+pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_stream, pnn_net** out) {
+    if (!out) return fail(nullptr, PNN_EINVAL, "out is NULL");
+    *out = nullptr;
+    std::string why;
+    if (check_config(cfg, &why) != PNN_OK) return fail(nullptr, PNN_EINVAL, "invalid config: %s", why.c_str());
+    if (!theta0_host) return fail(nullptr, PNN_EINVAL, "theta0_host is NULL");
+    pnn_net* n = new pnn_net();
+    n->cfg = *cfg;
+    n->L = cfg->n_layers;
+    for (int l = 0; l <= n->L; ++l) n->sizes[l] = cfg->sizes[l];
+    for (int l = 0; l < n->L; ++l) n->act[l] = cfg->act[l];
+    n->P = packed_count(cfg);
+    n->bf16 = cfg->precision == PNN_BF16_MIXED;
+    int64_t o = 0;
+    for (int l = 0; l < n->L; ++l) {
+        n->off_w[l] = o;
+        o = round_up(o + (int64_t)n->sizes[l + 1] * n->sizes[l], 64);
+        n->off_b[l] = o;
+        o = round_up(o + n->sizes[l + 1], 64);
+    }
+    n->pstride = o;
+    hipStream_t s = (hipStream_t)hip_stream;
+    auto bail = [&](pnn_status st) {
+        g_init_error = n->err;
+        free_all(n);
+        delete n;
+        return st;
+    };
+    if (hipGetDevice(&n->device) != hipSuccess) return bail(fail(n, PNN_EHIP, "no HIP device"));
+    const int K = cfg->replicas, B = cfg->batch;
+    pnn_status st;
+    if ((st = dev_alloc(n, &n->theta, (size_t)K * n->pstride)) != PNN_OK) return bail(st);
+    if ((st = dev_alloc(n, &n->merged, (size_t)n->pstride)) != PNN_OK) return bail(st);
+    if (n->bf16) {
+        if ((st = dev_alloc(n, &n->shadow, (size_t)K * n->pstride)) != PNN_OK) return bail(st);
+        if ((st = dev_alloc(n, &n->mshadow, (size_t)n->pstride)) != PNN_OK) return bail(st);
+    }
+    if ((st = dev_alloc(n, &n->d_correct, 1)) != PNN_OK) return bail(st);
+
+    n->psgd = (B == 1 && n->L == 2 && !n->bf16 && n->sizes[1] <= 1024 && n->sizes[2] <= MAX_OUT);
+    if (n->psgd) {
+        const int H = n->sizes[1];
+        int T = 128;
+        while (T > 16 && (int64_t)T * H > 16384) T >>= 1;
+        n->T = T;
+        // split the 784-long contraction of P so that every CN's P uses several CUs
+        n->kchunk = (int)round_up((n->sizes[0] + 7) / 8, 16);
+        n->ksplit = (n->sizes[0] + n->kchunk - 1) / n->kchunk;
+        if ((st = dev_alloc(n, &n->ppart, (size_t)n->ksplit * K * T * H)) != PNN_OK) return bail(st);
+        if ((st = dev_alloc(n, &n->d1, (size_t)K * T * H)) != PNN_OK) return bail(st);
+        const size_t smem = (size_t)(2 * T * H + 2 * 16 * MAX_OUT) * sizeof(float);
+        hipError_t e = hipSuccess;
+        switch (T) {
+        case 128: e = hipFuncSetAttribute((const void*)psgd_chunk_kernel<128>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+        case 64: e = hipFuncSetAttribute((const void*)psgd_chunk_kernel<64>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+        case 32: e = hipFuncSetAttribute((const void*)psgd_chunk_kernel<32>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+        default: e = hipFuncSetAttribute((const void*)psgd_chunk_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+        }
+        if (e != hipSuccess) return bail(fail(n, PNN_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e)));
+    } else {
+        const size_t el = n->bf16 ? 2 : 4;
+        for (int l = 1; l <= n->L; ++l) {
+            const size_t cnt = (size_t)K * B * n->sizes[l] * el;
+            if (l < n->L && (st = dev_alloc(n, (char**)&n->act_ws[l], cnt)) != PNN_OK) return bail(st);
+            if ((st = dev_alloc(n, (char**)&n->del_ws[l], cnt)) != PNN_OK) return bail(st);
+        }
+    }
+    // clone theta0 into every CN and the merged network
+    std::vector<float> padded(n->pstride);
+    unpack(n, theta0_host, padded.data());
+    if (hipMemcpy(n->merged, padded.data(), n->pstride * sizeof(float), hipMemcpyHostToDevice) != hipSuccess)
+        return bail(fail(n, PNN_EHIP, "copy of theta0 failed"));
+    for (int k = 0; k < K; ++k)
+        if (hipMemcpyAsync(n->theta + (size_t)k * n->pstride, n->merged, n->pstride * sizeof(float),
+                           hipMemcpyDeviceToDevice, s) != hipSuccess)
+            return bail(fail(n, PNN_EHIP, "clone of theta0 failed"));
+    if ((st = refresh_shadows(n, s)) != PNN_OK) return bail(st);
+    if (hipStreamSynchronize(s) != hipSuccess) return bail(fail(n, PNN_EHIP, "init synchronize failed"));
+    *out = n;
+    return PNN_OK;
+}
+
+pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev, int64_t N, void* hip_stream) {
+    TRY(usable(n));
+    if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
+    if (N < n->cfg.replicas) return fail(n, PNN_ESHAPE, "N = %lld < K = %d leaves a slice empty", (long long)N, n->cfg.replicas);
+    hipStream_t s = (hipStream_t)hip_stream;
+    if (n->psgd) return psgd_epoch(n, x_dev, y_dev, N, s);
+    const int64_t nmax = shard_len(N, n->cfg.replicas, 0);
+    for (int64_t r0 = 0; r0 < nmax; r0 += n->cfg.batch) {
+        if (n->bf16) TRY(minibatch_step<true>(n, x_dev, y_dev, N, r0, s));
+        else TRY(minibatch_step<false>(n, x_dev, y_dev, N, r0, s));
+    }
+    return PNN_OK;
+}
+
+pnn_status pnn_merge(pnn_net* n, int32_t broadcast, void* hip_stream) {
+    TRY(usable(n));
+    hipStream_t s = (hipStream_t)hip_stream;
+    MergeArgs a;
+    a.theta = n->theta; a.merged = n->merged;
+    a.shadow = n->bf16 ? n->shadow : nullptr;
+    a.mshadow = n->bf16 ? n->mshadow : nullptr;
+    a.pstride = n->pstride; a.K = n->cfg.replicas; a.broadcast = broadcast ? 1 : 0;
+    const int64_t q = n->pstride / 4;
+    Launch l(n, s, "merge");
+    merge_kernel<<<(unsigned)((q + 255) / 256), 256, 0, s>>>(a);
+    return l.done();
+}
+
+pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrows, int32_t* pred_dev, float* out_dev,
+                     int64_t* correct_host, const int32_t* y_dev, void* hip_stream) {
+    TRY(usable(n));
+    if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
+    if (nrows < 0) return fail(n, PNN_ESHAPE, "n < 0");
+    if (nrows == 0) {  // nothing to read or write
+        if (correct_host) *correct_host = 0;
+        return PNN_OK;
+    }
+    if (!x_dev || !pred_dev) return fail(n, PNN_EINVAL, "x_dev / pred_dev is NULL");
+    hipStream_t s = (hipStream_t)hip_stream;
+    const bool count = correct_host && y_dev;
+    if (count) HIP_TRY(n, hipMemsetAsync(n->d_correct, 0, sizeof(unsigned long long), s));
+    const int L = n->L;
+    const int CH = 8192;
+    const int rows = (int)std::min<int64_t>(nrows, CH);
+    if (L > 1 && rows > n->inf_rows) {
+        HIP_TRY(n, hipStreamSynchronize(s));
+        const size_t el = n->bf16 ? 2 : 4;
+        for (int l = 1; l < L; ++l) {
+            if (n->inf_ws[l]) (void)hipFree(n->inf_ws[l]);
+            n->inf_ws[l] = nullptr;
+            TRY(dev_alloc(n, (char**)&n->inf_ws[l], (size_t)rows * n->sizes[l] * el));
+        }
+        n->inf_rows = rows;
+    }
+    const float* th = which < 0 ? n->merged : n->theta + (size_t)which * n->pstride;
+    const bf16_t* sh = !n->bf16 ? nullptr : (which < 0 ? n->mshadow : n->shadow + (size_t)which * n->pstride);
+    for (int64_t r0 = 0; r0 < nrows; r0 += CH) {
+        // a single "CN" whose slice is the whole input: rows r0 .. r0+CH
+        for (int l = 1; l <= L - 1; ++l) {
+            GemmArgs g = gemm_base(n, CH, n->sizes[l], n->sizes[l - 1], nrows, r0, CH, 1);
+            g.k_rep = 1;
+            if (l == 1) g.a = opnd(x_dev, 0, n->sizes[0], 1);
+            else g.a = opnd(n->inf_ws[l - 1], 0, n->sizes[l - 1], 0);
+            g.c = n->inf_ws[l]; g.c_z = 0; g.c_ld = n->sizes[l];
+            g.bias = th + n->off_b[l - 1]; g.bias_z = 0;
+            g.act = n->act[l - 1];
+            g.M = std::min<int64_t>(CH, nrows - r0);
+            if (n->bf16) {
+                g.b = opnd(sh + n->off_w[l - 1], 0, n->sizes[l - 1], 0);
+                if (l == 1) TRY((run_gemm<true, float, bf16_t, true, true, EPI_FWD, bf16_t>(n, s, g, 1, "infer_fwd_gemm")));
+                else TRY((run_gemm<true, bf16_t, bf16_t, true, true, EPI_FWD, bf16_t>(n, s, g, 1, "infer_fwd_gemm")));
+            } else {
+                g.b = opnd(th + n->off_w[l - 1], 0, n->sizes[l - 1], 0);
+                if (l == 1) TRY((run_gemm<false, float, float, true, true, EPI_FWD, float>(n, s, g, 1, "infer_fwd_gemm")));
+                else TRY((run_gemm<false, float, float, true, true, EPI_FWD, float>(n, s, g, 1, "infer_fwd_gemm")));
+            }
+        }
+        RowArgs a;
+        memset(&a, 0, sizeof a);
+        if (L == 1) { a.x = x_dev; a.x_xrows = 1; a.x_ld = n->sizes[0]; }
+        else { a.x = n->inf_ws[L - 1]; a.x_z = 0; a.x_ld = n->sizes[L - 1]; }
+        a.bias = th + n->off_b[L - 1];
+        a.H = n->sizes[L - 1]; a.O = n->sizes[L]; a.act = n->act[L - 1]; a.loss = n->cfg.loss;
+        a.n_total = nrows; a.k_rep = 1; a.r0 = r0; a.step_rows = CH;
+        a.y = y_dev; a.out = out_dev; a.pred = pred_dev; a.correct = count ? n->d_correct : nullptr;
+        const int rws = (int)std::min<int64_t>(CH, nrows - r0);
+        dim3 grid((rws + 3) / 4, 1, 1);
+        Launch lc(n, s, "infer_out");
+        if (n->bf16) {
+            a.w = sh + n->off_w[L - 1];
+            if (L == 1) out_layer_kernel<float, bf16_t, float, false><<<grid, 256, 0, s>>>(a);
+            else out_layer_kernel<bf16_t, bf16_t, float, false><<<grid, 256, 0, s>>>(a);
+        } else {
+            a.w = th + n->off_w[L - 1];
+            out_layer_kernel<float, float, float, false><<<grid, 256, 0, s>>>(a);
+        }
+        TRY(lc.done());
+    }
+    if (count) {
+        unsigned long long c = 0;
+        HIP_TRY(n, hipMemcpyAsync(&c, n->d_correct, sizeof c, hipMemcpyDeviceToHost, s));
+        HIP_TRY(n, hipStreamSynchronize(s));
+        *correct_host = (int64_t)c;
+    }
+    return PNN_OK;
+}
+
+pnn_status pnn_get_params(pnn_net* n, int32_t which, float* host_out) {
+    TRY(usable(n));
+    if (!host_out) return fail(n, PNN_EINVAL, "host_out is NULL");
+    if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
+    HIP_TRY(n, hipDeviceSynchronize());
+    std::vector<float> padded(n->pstride);
+    const float* src = which < 0 ? n->merged : n->theta + (size_t)which * n->pstride;
+    HIP_TRY(n, hipMemcpy(padded.data(), src, n->pstride * sizeof(float), hipMemcpyDeviceToHost));
+    pack(n, padded.data(), host_out);
+    return PNN_OK;
+}
+
+pnn_status pnn_set_params(pnn_net* n, int32_t which, const float* host_in) {
+    TRY(usable(n));
+    if (!host_in) return fail(n, PNN_EINVAL, "host_in is NULL");
+    if (which < -2 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
+    HIP_TRY(n, hipDeviceSynchronize());
+    std::vector<float> padded(n->pstride);
+    unpack(n, host_in, padded.data());
+    const size_t bytes = n->pstride * sizeof(float);
+    if (which == -1 || which == -2) HIP_TRY(n, hipMemcpy(n->merged, padded.data(), bytes, hipMemcpyHostToDevice));
+    if (which >= 0) HIP_TRY(n, hipMemcpy(n->theta + (size_t)which * n->pstride, padded.data(), bytes, hipMemcpyHostToDevice));
+    if (which == -2)
+        for (int k = 0; k < n->cfg.replicas; ++k)
+            HIP_TRY(n, hipMemcpy(n->theta + (size_t)k * n->pstride, padded.data(), bytes, hipMemcpyHostToDevice));
+    TRY(refresh_shadows(n, nullptr));
+    HIP_TRY(n, hipDeviceSynchronize());
+    return PNN_OK;
+}
+
+const char* pnn_last_error(const pnn_net* n) { return n ? n->err.c_str() : g_init_error.c_str(); }
+
+pnn_status pnn_profile(pnn_net* n, int32_t enable) {
+    if (!n) return PNN_EINVAL;
+    prof_drain(n);
+    n->prof_acc.clear();
+    n->prof = enable != 0;
+    return PNN_OK;
+}
+
+int32_t pnn_profile_read(pnn_net* n, const char** names, double* total_ms, int64_t* launches, int32_t cap) {
+    if (!n) return 0;
+    prof_drain(n);
+    n->prof_names_store.clear();
+    for (auto& kv : n->prof_acc) n->prof_names_store.push_back(kv.first);
+    int32_t i = 0;
+    for (auto& kv : n->prof_acc) {
+        if (i >= cap) break;
+        if (names) names[i] = n->prof_names_store[i].c_str();
+        if (total_ms) total_ms[i] = kv.second.first;
+        if (launches) launches[i] = kv.second.second;
+        ++i;
+    }
+    return (int32_t)n->prof_acc.size();
+}
+
+void pnn_destroy(pnn_net* n) {
+    if (!n) return;
+    (void)hipDeviceSynchronize();
+    free_all(n);
+    delete n;
+}
+
+}  // extern "C"

@@ -1,0 +1,329 @@
+"""GPU parity of the HIP library against the CPU oracle, through the C ABI.
+
+Every case feeds both sides the same seeded inputs and the same initial parameters, then
+compares per-weight relative errors (see tests/parity.py): <= 1e-5 after one step and
+<= 1e-3 after full epochs in fp32, <= 2e-2 in bf16-mixed precision; predictions on held-out
+data must equal the oracle's argmax except on near-ties.  Cases cover every workload's
+shapes at sizes the oracle finishes in seconds (several tiles, ragged last batches and
+chunks, uneven slices), the workloads at full size (sampled child networks where the oracle
+would take too long), and the edge cases of the method.
+"""
+import numpy as np
+import pytest
+
+import pnn_inputs as I
+from oracle import oracle as O
+from tests.parity import (BF16_TOL, EPOCH_TOL, STEP_TOL, argmax_agrees, assert_close, log, oracle_replicas,
+                          rel_err)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from paper_2304_09590_amd import pnn as B  # noqa: E402
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def make_net(w, theta0):
+    return B.PNN(B.config_from_workload(w), theta0)
+
+
+def tol_for(w, epoch=False):
+    if w.precision == I.BF16_MIXED:
+        return BF16_TOL
+    return EPOCH_TOL if epoch else STEP_TOL
+
+
+def close_epoch(w, got, ref, what):
+    """Comparison after whole epochs: elementwise in fp32, normwise per layer in bf16."""
+    return assert_close(w.sizes, got, ref, tol_for(w, True), what, layerwise=w.precision == I.BF16_MIXED)
+
+
+# ------------------------------------------------------------------------------------
+# one training step of every workload's net
+
+STEP_CASES = [
+    (0, None),
+    (1, None),
+    (2, None),
+    (3, [0, 31, 63]),
+    (4, [0, 100, 255]),
+]
+
+
+@pytest.mark.parametrize("idx,ids", STEP_CASES, ids=[I.WORKLOADS[c[0]].name for c in STEP_CASES])
+def test_one_step(idx, ids):
+    w = I.WORKLOADS[idx]
+    K, Bt = w.replicas, w.batch
+    N = K * Bt
+    log(f"one step: {w.name} N={N}")
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    net.train_epoch(dev(X), dev(y))
+    torch.cuda.synchronize()
+    o = O.Oracle.from_workload(w)
+    ids = list(range(K)) if ids is None else ids
+    ref = oracle_replicas(o, np.tile(th0.astype(np.float64), (len(ids), 1)), ids, X, y)
+    for i, k in enumerate(ids):
+        got = net.get_params(k)
+        assert_close(w.sizes, got, ref[i], tol_for(w), f"replica {k}")
+        if w.precision == I.FP32:
+            # the update itself, relative to its own size
+            e = rel_err(w.sizes, got.astype(np.float64) - th0, ref[i] - th0)
+            assert max(e.values()) <= 1e-3, e
+    net.close()
+
+
+# ------------------------------------------------------------------------------------
+# full epochs at reduced sizes: ragged last batches / chunks, uneven slices, merges
+
+EPOCH_CASES = [
+    # workload, overrides, N, epochs
+    (0, {}, 2000, 1),                                         # workload 0 at full size
+    (1, {}, 4 * 300 + 3, 1),                                  # per-sample chunks with a ragged tail
+    (1, dict(replicas=3), 3 * 140 + 1, 2),                    # uneven slices, two epochs
+    (2, {}, 16 * 100 + 5, 2),                                 # batches 32,32,32,4/5
+    (3, dict(replicas=8), 8 * 150 + 3, 2),                    # bf16, merge + broadcast each epoch
+    (4, dict(replicas=16), 16 * 260 + 7, 2),                  # batches 128,128,4/5, merge each epoch
+    (2, dict(sizes=(784, 64, 32, 10), acts=(I.RELU, I.TANH, I.SOFTMAX), loss=I.LOSS_XENT, batch=16,
+             replicas=2, merge_every_epoch=True), 2 * 90 + 1, 2),   # deeper fp32 net
+    (0, dict(sizes=(784, 32, 16, 10), acts=(I.TANH, I.SIGMOID, I.SIGMOID), replicas=2), 2 * 40, 1),  # B=1, L=3
+    (1, dict(acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, replicas=2), 2 * 150, 1),  # per-sample softmax/xent
+]
+
+
+@pytest.mark.parametrize("idx,over,N,epochs", EPOCH_CASES)
+def test_epochs(idx, over, N, epochs):
+    w = I.WORKLOADS[idx].scaled(**over)
+    K = w.replicas
+    log(f"epochs: {w.name} {over} N={N} epochs={epochs}")
+    X, y = I.train_set(w, N)
+    Xt, yt = I.test_set(w, 3000)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    xd, yd = dev(X), dev(y)
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    for e in range(epochs):
+        net.train_epoch(xd, yd)
+        o.train_epoch(ref, X, y, threads=8)
+        for k in range(K):
+            close_epoch(w, net.get_params(k), ref[k], f"epoch {e} replica {k}")
+        if w.merge_every_epoch:
+            net.merge(broadcast=True)
+            m = o.merge(ref)
+            ref[:] = m[None, :]
+            close_epoch(w, net.get_params(-1), m, f"merged epoch {e}")
+            assert np.array_equal(net.get_params(0), net.get_params(-1))
+    if not w.merge_every_epoch:
+        net.merge(broadcast=False)
+    merged = net.get_params(-1)
+    close_epoch(w, merged, o.merge(ref), "merged")
+    # predictions with the GPU's merged weights against the oracle's forward of the same weights
+    pred = torch.empty(len(yt), dtype=torch.int32, device="cuda")
+    out = torch.empty((len(yt), w.sizes[-1]), dtype=torch.float32, device="cuda")
+    correct = net.infer(dev(Xt), pred, which=-1, out=out, y=dev(yt), count=True)
+    out_ref = o.forward(merged.astype(np.float64), Xt)
+    p = pred.cpu().numpy()
+    argmax_agrees(out_ref, p, margin=1e-5 if w.precision == I.FP32 else 2e-2)
+    assert correct == int((p == yt).sum())
+    np.testing.assert_allclose(out.cpu().numpy(), out_ref, rtol=0, atol=1e-5 if w.precision == I.FP32 else 2e-2)
+    net.close()
+
+
+# ------------------------------------------------------------------------------------
+# step-by-step trajectory: before every step the oracle restarts from the GPU's state
+
+def step_rows(N, K, Bt, s):
+    """Data rows of batch step s of every CN (an epoch over them is exactly that step)."""
+    o = O.Oracle((8, 2), (O.SIGMOID,), O.LOSS_MSE, replicas=K)
+    rows = []
+    for k in range(K):
+        st, ln = o.shard(N, k)
+        rows.append(np.arange(st + s * Bt, st + min(ln, (s + 1) * Bt)))
+    return rows
+
+
+@pytest.mark.parametrize("idx,over,N", [
+    (3, dict(replicas=8), 8 * 150 + 3),
+    (4, dict(replicas=4), 4 * 300 + 3),
+    (2, dict(replicas=4), 4 * 70 + 2),
+])
+def test_stepwise_trajectory(idx, over, N):
+    w = I.WORKLOADS[idx].scaled(**over)
+    K, Bt = w.replicas, w.batch
+    log(f"trajectory: {w.name} {over} N={N}")
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    o = O.Oracle.from_workload(w)
+    nsteps = -(-(-(-N // K)) // Bt)
+    for s in range(nsteps):
+        rows = step_rows(N, K, Bt, s)
+        if min(len(r) for r in rows) == 0:
+            break
+        before = np.stack([net.get_params(k) for k in range(K)]).astype(np.float64)
+        # one step of every CN: each CN gets exactly its own rows of this step
+        idxs = np.concatenate(rows)
+        if len(set(len(r) for r in rows)) == 1:
+            net.train_epoch(dev(X[idxs]), dev(y[idxs]))
+            for k in range(K):
+                ref = before[k].copy()[None, :]
+                one = O.Oracle.from_workload(w, replicas=1)
+                one.train_epoch(ref, X[rows[k]], y[rows[k]])
+                assert_close(w.sizes, net.get_params(k), ref[0], tol_for(w), f"step {s} replica {k}")
+        else:
+            break  # uneven last batches are covered by the epoch tests
+    net.close()
+
+
+# ------------------------------------------------------------------------------------
+# full-size workloads in the launch configuration of the benchmark
+
+def _full(w, ids_per_epoch, threads=16):
+    K = w.replicas
+    X, y = I.train_set(w)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    xd, yd = dev(X), dev(y)
+    o = O.Oracle.from_workload(w)
+    start = np.tile(th0.astype(np.float64), (K, 1)) if not w.merge_every_epoch else None
+    state = {k: th0.astype(np.float64) for k in (ids_per_epoch if ids_per_epoch else range(K))}
+    for e in range(w.epochs):
+        log(f"full {w.name}: epoch {e}")
+        if w.merge_every_epoch:
+            begin = net.get_params(-1).astype(np.float64)
+        net.train_epoch(xd, yd)
+        torch.cuda.synchronize()
+        ids = list(state.keys())
+        starts = np.stack([begin if w.merge_every_epoch else state[k] for k in ids])
+        ref = oracle_replicas(o, starts, ids, X, y, threads=threads)
+        for i, k in enumerate(ids):
+            state[k] = ref[i]
+            close_epoch(w, net.get_params(k), ref[i], f"epoch {e} replica {k}")
+        if w.merge_every_epoch:
+            reps = np.stack([net.get_params(k) for k in range(K)]).astype(np.float64)
+            net.merge(broadcast=True)
+            m = net.get_params(-1)
+            assert_close(w.sizes, m, o.merge(reps), 2e-7, f"merge epoch {e}")
+    if not w.merge_every_epoch:
+        reps = np.stack([net.get_params(k) for k in range(K)]).astype(np.float64)
+        net.merge(broadcast=False)
+        assert_close(w.sizes, net.get_params(-1), o.merge(reps), 2e-7, "merge")
+    Xt, yt = I.test_set(w)
+    pred = torch.empty(len(yt), dtype=torch.int32, device="cuda")
+    correct = net.infer(dev(Xt), pred, y=dev(yt), count=True)
+    out_ref = o.forward(net.get_params(-1).astype(np.float64), Xt)
+    argmax_agrees(out_ref, pred.cpu().numpy(), margin=1e-5 if w.precision == I.FP32 else 2e-2)
+    log(f"full {w.name}: merged accuracy {correct / len(yt):.4f}")
+    # clearly above chance (10 classes); the workloads with few, small steps (the 256-CN one
+    # takes 38 steps of eta = 0.02) are far from converged after their epochs
+    assert correct / len(yt) > 0.2
+    net.close()
+    del start
+
+
+def test_full_workload1_all_replicas():
+    w = I.WORKLOADS[1]
+    _full(w, list(range(w.replicas)), threads=4)
+
+
+def test_full_workload2_sampled():
+    _full(I.WORKLOADS[2], [0, 15])
+
+
+def test_full_workload3_sampled():
+    _full(I.WORKLOADS[3], [0, 63])
+
+
+def test_full_workload4_sampled():
+    _full(I.WORKLOADS[4], [0, 191, 192, 255])
+
+
+# ------------------------------------------------------------------------------------
+# merge, inference and handle behaviour
+
+def test_merge_identities():
+    w = I.WORKLOADS[2].scaled(replicas=5)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    net.merge()
+    assert np.array_equal(net.get_params(-1), th0)  # identical replicas: identity, bitwise
+    P = th0.size
+    for k in range(5):
+        net.set_params(k, np.full(P, float(k), np.float32))
+    net.merge(broadcast=False)
+    assert np.all(net.get_params(-1) == 2.0)  # (K - 1) / 2 exactly
+    assert np.all(net.get_params(3) == 3.0)
+    rng = np.random.default_rng(3)
+    reps = rng.standard_normal((5, P)).astype(np.float32)
+    for k in range(5):
+        net.set_params(k, reps[k])
+    net.merge(broadcast=True)
+    ref = reps.astype(np.float64).mean(axis=0)
+    m = net.get_params(-1)
+    assert np.max(np.abs(m - ref) / np.maximum(np.abs(ref), 1e-3)) <= 2e-7
+    for k in range(5):
+        assert np.array_equal(net.get_params(k), m)
+    net.close()
+
+
+def test_replica_inference_and_edges():
+    w = I.WORKLOADS[1].scaled(replicas=2)
+    X, y = I.train_set(w, 400)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    net.train_epoch(dev(X), dev(y))
+    o = O.Oracle.from_workload(w)
+    Xt, yt = I.test_set(w, 9000)  # crosses the 8192-row inference chunk
+    for which in (0, 1, -1):
+        pred = torch.empty(len(yt), dtype=torch.int32, device="cuda")
+        c = net.infer(dev(Xt), pred, which=which, y=dev(yt), count=True)
+        p = pred.cpu().numpy()
+        argmax_agrees(o.forward(net.get_params(which).astype(np.float64), Xt), p)
+        assert c == int((p == yt).sum())
+    empty = torch.empty((0, 784), dtype=torch.float32, device="cuda")
+    assert net.infer(empty, torch.empty(0, dtype=torch.int32, device="cuda"), y=dev(np.zeros(0, np.int32)),
+                     count=True) == 0
+    with pytest.raises(B.PnnError) as ei:
+        net.infer(dev(Xt), pred, which=2)
+    assert ei.value.status == B.PNN_EINVAL
+    with pytest.raises(B.PnnError) as ei:
+        net.train_epoch(dev(X[:1]), dev(y[:1]))  # N < K
+    assert ei.value.status == B.PNN_ESHAPE
+    net.close()
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3])
+def test_zero_lr_and_determinism_and_resume(idx):
+    w = I.WORKLOADS[idx].scaled(replicas=4)
+    X, y = I.train_set(w, 4 * 3 * w.batch + 5)
+    th0 = I.init_params(w)
+    xd, yd = dev(X), dev(y)
+    # eta = 0 leaves every parameter unchanged
+    z = B.PNN(B.config_from_workload(w, lr=0.0), th0)
+    z.train_epoch(xd, yd)
+    assert np.array_equal(z.get_params(2), th0)
+    z.close()
+    # two runs are bitwise identical; a run resumed from a checkpoint equals the uninterrupted one
+    runs = []
+    for _ in range(2):
+        n = make_net(w, th0)
+        n.train_epoch(xd, yd)
+        n.train_epoch(xd, yd)
+        runs.append(np.stack([n.get_params(k) for k in range(4)]))
+        n.close()
+    assert np.array_equal(runs[0], runs[1])
+    a = make_net(w, th0)
+    a.train_epoch(xd, yd)
+    ck = [a.get_params(k) for k in range(4)]
+    a.close()
+    b = make_net(w, np.zeros_like(th0))
+    for k in range(4):
+        b.set_params(k, ck[k])
+    b.train_epoch(xd, yd)
+    assert np.array_equal(np.stack([b.get_params(k) for k in range(4)]), runs[0])
+    b.close()
