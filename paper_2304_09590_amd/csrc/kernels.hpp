@@ -103,6 +103,7 @@ struct Operand {
     int64_t zstride;
     int64_t ld;
     int xrows;
+    int64_t xshift;  // xrows only: row offset added to the step's first data row
 };
 
 struct GemmArgs {
@@ -146,7 +147,7 @@ __device__ inline void gemm_zinfo(const GemmArgs& g, int z, int& cn, int64_t& r0
 
 __device__ inline const char* operand_row(const Operand& o, int elem, int z, int cn, int64_t xbase, int64_t r) {
     const char* p = (const char*)o.ptr;
-    if (o.xrows) return p + (size_t)((xbase + r) * o.ld) * elem;
+    if (o.xrows) return p + (size_t)((xbase + o.xshift + r) * o.ld) * elem;
     return p + (size_t)(z * o.zstride + r * o.ld) * elem;
 }
 
@@ -699,6 +700,513 @@ __global__ __launch_bounds__(1024) void psgd_chunk_kernel(PsgdArgs a) {
     }
     if (h == 0)
         for (int o = 0; o < O; ++o) th[a.off_b2 + o] = b2[o];
+}
+
+}  // namespace pnn
+
+namespace pnn {
+
+// ------------------------------------------------------------------------------------
+// Cross-lane helpers (DPP, within rows of 16 lanes)
+
+template <int CTRL>
+__device__ inline float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+constexpr int DPP_ROW_MIRROR = 0x140;       // lane i <-> 15 - i
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;  // lane i <-> 7 - i within each half row
+constexpr int DPP_XOR2 = 0x4E;              // quad_perm [2,3,0,1]
+constexpr int DPP_XOR1 = 0xB1;              // quad_perm [1,0,3,2]
+
+// Reduce-scatter of 16 values over each row of 16 lanes: afterwards lane i of a row holds
+// the row's sum of v[i & 15].  Four pairing rounds; every pair of partners agrees on the
+// lane bits split so far and differs in the bit split now.
+__device__ inline float row_reduce_scatter16(const float (&v)[16], int lane) {
+    const bool b3 = lane & 8, b2 = lane & 4, b1 = lane & 2, b0 = lane & 1;
+    float a[8], b[4], c[2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float send = b3 ? v[j] : v[j + 8], keep = b3 ? v[j + 8] : v[j];
+        a[j] = keep + dpp<DPP_ROW_MIRROR>(send);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float send = b2 ? a[j] : a[j + 4], keep = b2 ? a[j + 4] : a[j];
+        b[j] = keep + dpp<DPP_ROW_HALF_MIRROR>(send);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const float send = b1 ? b[j] : b[j + 2], keep = b1 ? b[j + 2] : b[j];
+        c[j] = keep + dpp<DPP_XOR2>(send);
+    }
+    const float send = b0 ? c[0] : c[1], keep = b0 ? c[1] : c[0];
+    return keep + dpp<DPP_XOR1>(send);
+}
+__device__ inline float row_allmax16(float v) {
+    v = fmaxf(v, dpp<DPP_ROW_MIRROR>(v));
+    v = fmaxf(v, dpp<DPP_ROW_HALF_MIRROR>(v));
+    v = fmaxf(v, dpp<DPP_XOR2>(v));
+    return fmaxf(v, dpp<DPP_XOR1>(v));
+}
+__device__ inline float row_allsum16(float v) {
+    v += dpp<DPP_ROW_MIRROR>(v);
+    v += dpp<DPP_ROW_HALF_MIRROR>(v);
+    v += dpp<DPP_XOR2>(v);
+    return v + dpp<DPP_XOR1>(v);
+}
+__device__ inline float readlane_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+
+// Activations of the sequential per-sample steps, on the hardware exp2 and reciprocal
+// (about 1e-6 relative error for |z| < 10).
+__device__ inline float act_fast(int a, float z) {
+    switch (a) {
+    case ACT_SIGMOID: return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+    case ACT_TANH: return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * z) + 1.0f);
+    case ACT_RELU: return z >= 0.0f ? z + 0.0f : -0.0f;
+    case ACT_LEAKY: return z >= 0.0f ? z + 0.0f : 0.01f * z;
+    default: return z;
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Bounded cross-workgroup waits (device-scope release/acquire on a counter in global
+// memory).  Thread 0 polls; on expiry of `limit` polls, or when another workgroup has
+// raised the abort flag, every thread gets `false` and the caller leaves its loop, so the
+// grid always drains.
+
+__device__ inline bool wait_geq(int* flag, int target, int* abort, long limit) {
+    __shared__ int ok;
+    if (threadIdx.x == 0) {
+        int good = 1;
+        long it = 0;
+        // relaxed polls (coherent loads, no cache maintenance); one acquire fence afterwards
+        while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            if (__hip_atomic_load(abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) { good = 0; break; }
+            if (++it > limit) {
+                __hip_atomic_store(abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                good = 0;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        ok = good;
+    }
+    __syncthreads();
+    const bool r = ok != 0;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    __syncthreads();
+    return r;
+}
+
+// The workgroup barrier makes every wave's stores complete; thread 0's release fence then
+// publishes them before the flag update.
+__device__ inline void signal_add(int* flag, int v) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __hip_atomic_fetch_add(flag, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+__device__ inline void signal_set(int* flag, int v) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __hip_atomic_store(flag, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Per-sample stochastic gradient descent of a one-hidden-layer fp32 network: one
+// persistent launch per epoch.
+//
+// Chunked form of the sequential steps (see psgd_chunk_kernel).  With W1^(c) the
+// first-layer weights before chunk c, the first-layer input sum of step t of chunk c is
+//   z1_t = Q_c[t] + b1_t - eta * ( sum_{s in chunk c-1} d1_s GX_c[t][s]
+//                                 + sum_{s < t in chunk c} d1_s G_c[t][s] )
+// where Q_c[t] = W1^(c-1) x_t (for c = 0: W1^(0) x_t), G_c[t][s] = x_t . x_s within the
+// chunk and GX_c[t][s] = x_t . x_s against the previous chunk.  Q_c therefore needs the
+// first-layer errors only up to chunk c-2, and is computed while chunk c-1 runs.
+//
+// Grid (cooperative, all workgroups co-resident, 256 threads each):
+//   blockIdx < K: the sequential workgroup of CN k.  Waves 0..HW/64-1 own one hidden
+//     neuron per lane (W2 column and b1 in registers); the other "helper" waves compute,
+//     one step ahead, the already-known part (s <= t-2) of the next step's in-chunk
+//     correction.  At chunk start all four waves compute the previous-chunk correction on
+//     the matrix cores.
+//   blockIdx >= K: tile workgroups.  Tile (k, rb) keeps W1[16 rows][all inputs] of CN k in
+//     registers for the epoch, laid out as the B operand of v_mfma_f32_16x16x4_f32 (lane l:
+//     row 16 rb + l % 16, inputs 16 ib + 4 (l / 16) + q).  It publishes Q_0 and Q_1, then for
+//     each later chunk waits for the previous chunk's errors, applies
+//     W1 -= eta * sum_t d1_t x_t^T (a product whose accumulator layout equals the register
+//     layout) and publishes the next Q.
+
+struct PsgdPArgs {
+    float* theta;
+    int64_t pstride, off_w1, off_b1, off_w2, off_b2;
+    const float* X;
+    const int32_t* y;
+    int64_t n_total;
+    int k_rep;
+    const float* gram;   // [K][nch][T][T]   within each chunk
+    const float* gramx;  // [K][nch-1][T][T] chunk c (rows) against chunk c-1, c >= 1
+    int nch;
+    float* qbuf;         // [2][K][T][H]  by chunk parity
+    float* d1;           // [2][K][T][H]  by chunk parity
+    int* flags;          // qready[K], dready[K], abort
+    int H, O, In, act1, act2, loss, nrb;
+    float lr;
+    long spin_limit;
+};
+
+constexpr int MAX_IB = 13;  // input blocks of 16 per wave of a tile (4 waves x 13 x 16 >= 784)
+
+template <int T, int HW, int A1, int A2, int LS, int OC>
+__device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& a, int k, float* smem) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int H = a.H, K = a.k_rep;
+    const int O = OC < 16 ? OC : a.O;
+    const int act1 = A1 >= 0 ? A1 : a.act1;
+    const int act2 = A2 >= 0 ? A2 : a.act2;
+    const int loss = LS >= 0 ? LS : a.loss;
+    constexpr int nlive = HW >> 6;
+    const bool live = tid < HW;
+    const int h = live ? tid : (tid - HW) % HW;
+    const int part = live ? 0 : (tid - HW) / HW;
+    const bool hv = h < H;
+    constexpr int TS = T + 4;  // row stride of the transposed error history
+    float* Pl = smem;                    // [T][HW]
+    float* histA = Pl + T * HW;          // [2][HW][TS]
+    float* Gl = histA + 2 * HW * TS;     // [T][T]
+    float* GXl = Gl + T * T;             // [T][T]
+    float* red = GXl + T * T;            // [2][16 outputs][16 rows]
+    float* cpre = red + 2 * 256;         // [2][3][HW]
+    int* ylds = (int*)(cpre + 6 * HW);   // [T]
+
+    const int64_t nz = shard_len(a.n_total, K, k), xs = shard_start(a.n_total, K, k);
+    const int nchk = (int)((nz + T - 1) / T);
+    float* th = a.theta + (size_t)k * a.pstride;
+    float b1 = (live && hv) ? th[a.off_b1 + h] : 0.f;
+    float w2[OC];
+#pragma unroll
+    for (int o = 0; o < OC; ++o) w2[o] = (live && hv && o < O) ? th[a.off_w2 + (size_t)o * H + h] : 0.f;
+    const int ol = lane & 15;
+    float b2v = (ol < O) ? th[a.off_b2 + ol] : 0.f;
+    int* qready = a.flags + k;
+    int* dready = a.flags + K + k;
+    int* abort = a.flags + 2 * K;
+    const float lr = a.lr;
+    // padding neurons h >= H must read zero errors in the previous-chunk correction
+    for (int i = tid; i < 2 * HW * TS; i += 256) histA[i] = 0.f;
+
+    for (int c = 0; c < nchk; ++c) {
+        const int tc = __builtin_amdgcn_readfirstlane((int)min<int64_t>(T, nz - (int64_t)c * T));
+        float* hist = histA + (c & 1) * HW * TS;
+        const float* histp = histA + ((c + 1) & 1) * HW * TS;
+        if (!wait_geq(qready, a.nrb * (c + 1), abort, a.spin_limit)) return;
+        {
+            // Q rows, Gram blocks and labels into LDS (float4, loads issued before stores)
+            const float* Q = a.qbuf + ((size_t)(c & 1) * K + k) * T * H;
+            const float* G = a.gram + ((size_t)k * a.nch + c) * T * T;
+            const float* GX = a.gramx + ((size_t)k * (a.nch - 1) + (c - 1)) * T * T;
+            float4 gv[T * T / 1024], gx[T * T / 1024];
+#pragma unroll
+            for (int j = 0; j < T * T / 1024; ++j) {
+                gv[j] = *(const float4*)(G + 4 * (tid + 256 * j));
+                gx[j] = c > 0 ? *(const float4*)(GX + 4 * (tid + 256 * j)) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            const int hq = HW / 4, nidx = tc * hq;
+            for (int base = 0; base < nidx; base += 4 * 256) {
+                float4 v[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int idx = base + u * 256 + tid, t = idx / hq, h4 = (idx % hq) * 4;
+                    v[u] = (idx < nidx && h4 < H) ? *(const float4*)(Q + (size_t)t * H + h4) : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int idx = base + u * 256 + tid, t = idx / hq, h4 = (idx % hq) * 4;
+                    if (idx < nidx) *(float4*)(Pl + t * HW + h4) = v[u];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < T * T / 1024; ++j) {
+                *(float4*)(Gl + 4 * (tid + 256 * j)) = gv[j];
+                *(float4*)(GXl + 4 * (tid + 256 * j)) = gx[j];
+            }
+            for (int idx = tid; idx < tc; idx += 256) ylds[idx] = a.y[xs + (int64_t)c * T + idx];
+        }
+        __syncthreads();
+        if (c > 0) {
+            // previous-chunk correction on the matrix cores:
+            // Pl[t][h] -= eta * sum_s GX[t][s] d1prev_s[h]   (output tiles 16 t x 16 h)
+            const int ntiles = 4 * (HW / 16) * (T / 64);
+            for (int tt = wave; tt < ntiles; tt += 4) {
+                const int mt = tt % (T / 16), nt = tt / (T / 16);
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+                const int r16 = lane & 15, g = lane >> 4;
+#pragma unroll
+                for (int sl = 0; sl < T / 16; ++sl) {
+                    const float4 av = *(const float4*)(GXl + (mt * 16 + r16) * T + sl * 16 + 4 * g);
+                    const float4 bv = *(const float4*)(histp + (nt * 16 + r16) * TS + sl * 16 + 4 * g);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = mt * 16 + 4 * g + r, hh = nt * 16 + r16;
+                    Pl[t * HW + hh] -= lr * acc[r];
+                }
+            }
+            __syncthreads();
+        }
+
+        // Steps in blocks of 16.  At the start of block b the errors of block b-1 are folded
+        // into the input sums of every later row of the chunk on the matrix cores, so a
+        // step's in-chunk correction only needs the earlier steps of its own block.
+        float corr = 0.f, dprev = 0.f;
+        float pl_next = live ? Pl[h] : 0.f;
+        for (int t = 0; t < tc; ++t) {
+            const int bs = t & ~15;  // first step of this block
+            if (t > 0 && t == bs) {
+                __syncthreads();  // errors of the finished block are in LDS
+                const int sb = bs - 16;
+                const int nmt = (T - bs) >> 4, ntl = nmt * (HW / 16);
+                const int r16 = lane & 15, g = lane >> 4;
+                for (int tt = wave; tt < ntl; tt += 4) {
+                    const int mt = (bs >> 4) + tt % nmt, nt = tt / nmt;
+                    const float4 av = *(const float4*)(Gl + (mt * 16 + r16) * T + sb + 4 * g);
+                    const float4 bv = *(const float4*)(hist + (nt * 16 + r16) * TS + sb + 4 * g);
+                    f4 acc = {0.f, 0.f, 0.f, 0.f};
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) Pl[(mt * 16 + 4 * g + r) * HW + nt * 16 + r16] -= lr * acc[r];
+                }
+                __syncthreads();
+                pl_next = live ? Pl[t * HW + h] : 0.f;
+            }
+            float a1 = 0.f;
+            if (live) {
+                const float z1 = pl_next + b1 - lr * corr;
+                pl_next = (t + 1 < tc) ? Pl[(t + 1) * HW + h] : 0.f;  // prefetch the next step's input sum
+                a1 = hv ? act_fast(act1, z1) : 0.f;
+                float p[16];
+#pragma unroll
+                for (int o = 0; o < 16; ++o) p[o] = o < OC ? w2[o < OC ? o : 0] * a1 : 0.f;
+                const float v = row_reduce_scatter16(p, lane);
+                red[(t & 1) * 256 + ol * 16 + wave * 4 + (lane >> 4)] = v;
+            } else if (part == 0 && hv) {
+                // helper: in-block part of the next step's correction, sum over s in
+                // [bs1, t-2] of d1_s G[t+1][s] (at most 14 terms: four masked float4 groups)
+                const int t1 = t + 1, bs1 = t1 & ~15;
+                float sum = 0.f;
+                if (t1 < tc && t - 2 >= bs1) {
+                    const float* g = Gl + t1 * T + bs1;
+                    const float* hr = hist + h * TS + bs1;
+                    const int last = t - 2 - bs1;  // highest offset included
+                    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (4 * q <= last) {
+                            const float4 hv4 = *(const float4*)(hr + 4 * q), gv4 = *(const float4*)(g + 4 * q);
+                            acc.x += hv4.x * gv4.x;
+                            acc.y += (4 * q + 1 <= last) ? hv4.y * gv4.y : 0.f;
+                            acc.z += (4 * q + 2 <= last) ? hv4.z * gv4.z : 0.f;
+                            acc.w += (4 * q + 3 <= last) ? hv4.w * gv4.w : 0.f;
+                        }
+                    }
+                    sum = (acc.x + acc.y) + (acc.z + acc.w);
+                }
+                cpre[((t + 1) & 1) * HW + h] = sum;
+            }
+            __syncthreads();
+            if (live) {
+                // every operand of this phase is read up front
+                const float4* rr = (const float4*)(red + (t & 1) * 256 + ol * 16);
+                const float4 r0 = rr[0];
+                const float4 r1 = nlive > 1 ? rr[1] : make_float4(0.f, 0.f, 0.f, 0.f);
+                const int label = ylds[t];
+                float cp = 0.f, g0 = 0.f, g1 = 0.f;
+                const int bs1 = (t + 1) & ~15;
+                if (t + 1 < tc) {
+                    cp = cpre[((t + 1) & 1) * HW + h];
+                    const float* g = Gl + (t + 1) * T;
+                    g1 = t >= bs1 ? g[t] : 0.f;
+                    g0 = t - 1 >= bs1 ? g[t - 1] : 0.f;
+                }
+                const float z2 = b2v + ((r0.x + r0.y) + (r0.z + r0.w)) + ((r1.x + r1.y) + (r1.z + r1.w));
+                float x2;
+                if (act2 == ACT_SOFTMAX) {
+                    const float m = row_allmax16(ol < O ? z2 : -INFINITY);
+                    const float e = ol < O ? __expf(z2 - m) : 0.f;
+                    x2 = e * __builtin_amdgcn_rcpf(row_allsum16(e));
+                } else {
+                    x2 = act_fast(act2, z2);
+                }
+                const float e = (ol == label) ? 1.0f : 0.0f;
+                float d2 = (loss == LOSS_XENT) ? (x2 - e) : (x2 - e) * act_deriv(act2, x2);
+                d2 = ol < O ? d2 : 0.f;
+                b2v -= lr * d2;
+                float bk[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int o = 0; o < OC; ++o) {
+                    const float d2o = readlane_f(d2, o);
+                    bk[o & 3] += w2[o] * d2o;
+                    w2[o] -= (lr * d2o) * a1;
+                }
+                const float back = (bk[0] + bk[1]) + (bk[2] + bk[3]);
+                const float d1 = hv ? back * act_deriv(act1, a1) : 0.f;
+                b1 -= lr * d1;
+                hist[h * TS + t] = d1;
+                corr = cp + dprev * g0 + d1 * g1;
+                dprev = d1;
+            }
+        }
+        // publish the chunk's first-layer errors
+        __syncthreads();
+        float* dout = a.d1 + ((size_t)(c & 1) * K + k) * T * H;
+        for (int idx = tid; idx < tc * H; idx += 256) {
+            const int t = idx / H, hh = idx % H;
+            dout[(size_t)t * H + hh] = hist[hh * TS + t];
+        }
+        signal_set(dready, c + 1);
+    }
+    if (live && hv) {
+        th[a.off_b1 + h] = b1;
+#pragma unroll
+        for (int o = 0; o < OC; ++o)
+            if (o < O) th[a.off_w2 + (size_t)o * H + h] = w2[o];
+    }
+    if (tid < O) th[a.off_b2 + tid] = b2v;
+}
+
+template <int T>
+__device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs& a, int k, int rb, float* smem) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int H = a.H, In = a.In, K = a.k_rep;
+    const int h = rb * 16 + (lane & 15);
+    const int g = lane >> 4;
+    const int nib = (In + 15) / 16;  // input blocks of 16; wave w owns blocks w, w+4, ...
+    float* th = a.theta + (size_t)k * a.pstride;
+    float W[MAX_IB][4];
+#pragma unroll
+    for (int j = 0; j < MAX_IB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
+            W[j][q] = (ib < nib && h < H && i < In) ? th[a.off_w1 + (size_t)h * In + i] : 0.f;
+        }
+    const int64_t nz = shard_len(a.n_total, K, k), xs = shard_start(a.n_total, K, k);
+    const int nchk = (int)((nz + T - 1) / T);
+    int* qready = a.flags + k;
+    int* dready = a.flags + K + k;
+    int* abort = a.flags + 2 * K;
+    constexpr int NMT = T / 16;
+    float* red4 = smem;  // [4 waves][NMT][64][4]
+
+    // Q_c = W1 (current registers) x_t for the rows of chunk c, published to qbuf[c & 1]
+    auto publish_q = [&](int c) {
+        const int tc = (int)min<int64_t>(T, nz - (int64_t)c * T);
+        const int64_t xb = xs + (int64_t)c * T;
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) {
+            const int row = mt * 16 + (lane & 15);
+            float4 xv[MAX_IB];
+#pragma unroll
+            for (int j = 0; j < MAX_IB; ++j) {
+                const int ib = wave + 4 * j, i = ib * 16 + 4 * g;
+                xv[j] = (ib < nib && row < tc && i < In) ? *(const float4*)(a.X + (size_t)(xb + row) * In + i)
+                                                          : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int j = 0; j < MAX_IB; ++j) {
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].x, W[j][0], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].y, W[j][1], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].z, W[j][2], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].w, W[j][3], acc, 0, 0, 0);
+            }
+            *(f4*)(red4 + ((size_t)(wave * NMT + mt) * 64 + lane) * 4) = acc;
+        }
+        __syncthreads();
+        float* Q = a.qbuf + ((size_t)(c & 1) * K + k) * T * H;
+        for (int e = tid; e < NMT * 256; e += 256) {
+            const int mt = e >> 8, rem = e & 255, ln = rem >> 2, r = rem & 3;
+            float s = 0.f;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) s += red4[((size_t)(w * NMT + mt) * 64 + ln) * 4 + r];
+            const int t = mt * 16 + 4 * (ln >> 4) + r, hh = rb * 16 + (ln & 15);
+            if (t < tc && hh < H) Q[(size_t)t * H + hh] = s;
+        }
+        signal_add(qready, 1);
+    };
+    // W1 tile -= eta * sum_t d1_t x_t^T over the rows of chunk c
+    auto update = [&](int c) {
+        const int tc = (int)min<int64_t>(T, nz - (int64_t)c * T);
+        const int64_t xb = xs + (int64_t)c * T;
+        const float* D = a.d1 + ((size_t)(c & 1) * K + k) * T * H;
+        float bv[T / 4];
+#pragma unroll
+        for (int u = 0; u < T / 4; ++u) {
+            const int t = (u >> 2) * 16 + 4 * g + (u & 3);
+            bv[u] = (t < tc && h < H) ? D[(size_t)t * H + h] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < MAX_IB; ++j) {
+            const int ib = wave + 4 * j;
+            if (ib >= nib) continue;
+            const int icol = ib * 16 + (lane & 15);
+            float av[T / 4];
+#pragma unroll
+            for (int u = 0; u < T / 4; ++u) {
+                const int t = (u >> 2) * 16 + 4 * g + (u & 3);
+                av[u] = (t < tc && icol < In) ? a.X[(size_t)(xb + t) * In + icol] : 0.f;
+            }
+            f4 dacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int u = 0; u < T / 4; ++u) dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], dacc, 0, 0, 0);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) W[j][r] -= a.lr * dacc[r];
+        }
+    };
+
+    publish_q(0);
+    if (nchk > 1) publish_q(1);
+    bool ok = true;
+    for (int c = 1; c < nchk && ok; ++c) {
+        if (!wait_geq(dready, c, abort, a.spin_limit)) { ok = false; break; }
+        update(c - 1);
+        if (c + 1 < nchk) publish_q(c + 1);
+    }
+    if (!ok || !wait_geq(dready, nchk, abort, a.spin_limit)) return;
+    update(nchk - 1);
+#pragma unroll
+    for (int j = 0; j < MAX_IB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
+            if (ib < nib && h < H && i < In) th[a.off_w1 + (size_t)h * In + i] = W[j][q];
+        }
+}
+
+template <int T, int HW, int A1, int A2, int LS, int OC>
+__global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
+    extern __shared__ float smem[];
+    const int b = blockIdx.x, K = a.k_rep;
+    if (b < K) psgd_rec<T, HW, A1, A2, LS, OC>(a, b, smem);
+    else {
+        const int j = b - K;
+        psgd_tile<T>(a, j / a.nrb, j % a.nrb, smem);
+    }
+}
+
+__global__ void zero_ints_kernel(int* p, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
 }
 
 }  // namespace pnn

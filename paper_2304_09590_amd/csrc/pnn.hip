@@ -75,6 +75,15 @@ struct pnn_net {
     float* d1 = nullptr;     // [K][T][H]
     float* gram = nullptr;   // [K][nch][T][T]
     size_t gram_elems = 0;
+    // persistent variant: nrb tiles of 16 rows of W1 per CN
+    bool persistent = false;
+    bool pspecial = false;   // sigmoid / sigmoid / quadratic loss / 10 outputs
+    int nrb = 0;
+    int* flags = nullptr;    // qready[K], dready[K], abort
+    float* qbuf = nullptr;   // [2][K][T][H]
+    float* gramx = nullptr;  // [K][nch-1][T][T]
+    size_t gramx_elems = 0;
+    size_t psmem = 0;
 
     // profiling
     bool prof = false;
@@ -250,9 +259,9 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
     return l.done();
 }
 
-Operand opnd(const void* p, int64_t zs, int64_t ld, int xrows) {
+Operand opnd(const void* p, int64_t zs, int64_t ld, int xrows, int64_t xshift = 0) {
     Operand o;
-    o.ptr = p; o.zstride = zs; o.ld = ld; o.xrows = xrows;
+    o.ptr = p; o.zstride = zs; o.ld = ld; o.xrows = xrows; o.xshift = xshift;
     return o;
 }
 
@@ -362,7 +371,83 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
 // ---------------------------------------------------------------------------------------
 // chunked per-sample plan
 
+constexpr int PT = 64;            // chunk length of the persistent per-sample plan
+constexpr long SPIN_LIMIT = 1L << 22;
+
+// kernel instance: hidden width class (64 / 128 live threads) x activation specialisation
+const void* persistent_fn(const pnn_net* n) {
+    const bool narrow = n->sizes[1] <= 64;
+    if (n->pspecial)
+        return narrow ? (const void*)psgd_persistent_kernel<PT, 64, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>
+                      : (const void*)psgd_persistent_kernel<PT, 128, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>;
+    return narrow ? (const void*)psgd_persistent_kernel<PT, 64, -1, -1, -1, 16>
+                  : (const void*)psgd_persistent_kernel<PT, 128, -1, -1, -1, 16>;
+}
+
+pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
+    const int K = n->cfg.replicas, H = n->sizes[1], In = n->sizes[0];
+    const int64_t nmax = shard_len(N, K, 0);
+    const int nch = (int)((nmax + PT - 1) / PT);
+    auto grow = [&](float** buf, size_t* have, size_t need) -> pnn_status {
+        if (need <= *have) return PNN_OK;
+        if (*buf) (void)hipFree(*buf);
+        *buf = nullptr;
+        *have = 0;
+        TRY(dev_alloc(n, buf, need));
+        *have = need;
+        return PNN_OK;
+    };
+    TRY(grow(&n->gram, &n->gram_elems, (size_t)K * nch * PT * PT));
+    TRY(grow(&n->gramx, &n->gramx_elems, (size_t)K * std::max(nch - 1, 1) * PT * PT));
+    {
+        // G_c[t][s] = x_t . x_s within every chunk
+        GemmArgs g = gemm_base(n, PT, PT, In, N, 0, PT, 3);
+        g.a = opnd(X, 0, In, 1);
+        g.b = opnd(X, 0, In, 1);
+        g.zdiv = nch; g.r0_step = PT;
+        g.c = n->gram; g.c_z = (int64_t)PT * PT; g.c_ld = PT;
+        TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K * nch, "psgd_gram")));
+    }
+    if (nch > 1) {
+        // GX_c[t][s] = x_t . x_s, t in chunk c, s in chunk c-1 (always full), c >= 1
+        GemmArgs g = gemm_base(n, PT, PT, In, N, PT, PT, 1);
+        g.a = opnd(X, 0, In, 1);
+        g.b = opnd(X, 0, In, 1, -PT);
+        g.zdiv = nch - 1; g.r0_step = PT;
+        g.c = n->gramx; g.c_z = (int64_t)PT * PT; g.c_ld = PT;
+        TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K * (nch - 1), "psgd_gram")));
+    }
+    {
+        Launch l(n, s, "zero_flags");
+        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, 2 * K + 1);
+        TRY(l.done());
+    }
+    PsgdPArgs a;
+    memset(&a, 0, sizeof a);
+    a.theta = n->theta; a.pstride = n->pstride;
+    a.off_w1 = n->off_w[0]; a.off_b1 = n->off_b[0]; a.off_w2 = n->off_w[1]; a.off_b2 = n->off_b[1];
+    a.X = X; a.y = Y; a.n_total = N; a.k_rep = K;
+    a.gram = n->gram; a.gramx = n->gramx; a.nch = nch;
+    a.qbuf = n->qbuf; a.d1 = n->d1; a.flags = n->flags;
+    a.H = H; a.O = n->sizes[2]; a.In = In; a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
+    a.nrb = n->nrb;
+    a.lr = n->cfg.lr;
+    a.spin_limit = SPIN_LIMIT;
+    void* params[] = {&a};
+    const dim3 grid((unsigned)(K * (1 + n->nrb)));
+    Launch l(n, s, "psgd_persistent");
+    const void* fn = persistent_fn(n);
+    hipError_t e = hipLaunchCooperativeKernel(fn, grid, dim3(256), params, (unsigned)n->psmem, s);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        n->broken = true;
+        return fail(n, PNN_EHIP, "cooperative launch of the per-sample kernel failed: %s", hipGetErrorString(e));
+    }
+    return l.done();
+}
+
 pnn_status psgd_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
+    if (n->persistent) return psgd_persistent_epoch(n, X, Y, N, s);
     const int K = n->cfg.replicas, T = n->T, H = n->sizes[1], In = n->sizes[0];
     const int64_t nmax = shard_len(N, K, 0);
     const int nch = (int)((nmax + T - 1) / T);
@@ -468,9 +553,21 @@ void free_all(pnn_net* n) {
     auto f = [](void* p) { if (p) (void)hipFree(p); };
     f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
     for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
-    f(n->d_correct); f(n->ppart); f(n->d1); f(n->gram);
+    f(n->d_correct); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
     for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : n->free_events) (void)hipEventDestroy(e);
+}
+
+// a per-sample persistent launch that gave up waiting leaves its abort flag set
+pnn_status check_abort(pnn_net* n) {
+    if (!n->persistent || !n->flags) return PNN_OK;
+    int ab = 0;
+    HIP_TRY(n, hipMemcpy(&ab, n->flags + 2 * n->cfg.replicas, sizeof(int), hipMemcpyDeviceToHost));
+    if (ab) {
+        n->broken = true;
+        return fail(n, PNN_EHIP, "the per-sample training kernel timed out waiting for a peer workgroup");
+    }
+    return PNN_OK;
 }
 
 pnn_status usable(pnn_net* n) {
@@ -544,6 +641,34 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
 
     n->psgd = (B == 1 && n->L == 2 && !n->bf16 && n->sizes[1] <= 1024 && n->sizes[2] <= MAX_OUT);
     if (n->psgd) {
+        // persistent plan: every CN needs 1 + nrb co-resident workgroups
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, n->device) != hipSuccess) cus = 0;
+        const int H = n->sizes[1], In = n->sizes[0], O = n->sizes[2];
+        const int nrb = (H + 15) / 16;
+        const int HW = (H + 63) & ~63;
+        const size_t rec_smem =
+            (size_t)(PT * HW + 2 * HW * (PT + 4) + 2 * PT * PT + 512 + 6 * HW + PT) * sizeof(float);
+        const size_t tile_smem = (size_t)4 * (PT / 16) * 64 * 4 * sizeof(float);
+        n->psmem = std::max(rec_smem, tile_smem);
+        n->pspecial = n->act[0] == PNN_SIGMOID && n->act[1] == PNN_SIGMOID && cfg->loss == PNN_LOSS_MSE && O == 10;
+        const void* fn = persistent_fn(n);
+        int per_cu = 0;
+        bool fits = H <= 128 && In <= 4 * MAX_IB * 16 && (int64_t)K * (1 + nrb) <= cus;
+        if (fits && hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)n->psmem) != hipSuccess)
+            fits = false;
+        if (fits && hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, n->psmem) != hipSuccess) fits = false;
+        if (fits && (int64_t)per_cu * cus < (int64_t)K * (1 + nrb)) fits = false;
+        (void)hipGetLastError();
+        if (fits) {
+            n->persistent = true;
+            n->nrb = nrb;
+            if ((st = dev_alloc(n, &n->qbuf, (size_t)2 * K * PT * H)) != PNN_OK) return bail(st);
+            if ((st = dev_alloc(n, &n->d1, (size_t)2 * K * PT * H)) != PNN_OK) return bail(st);
+            if ((st = dev_alloc(n, &n->flags, (size_t)(2 * K + 1))) != PNN_OK) return bail(st);
+        }
+    }
+    if (n->psgd && !n->persistent) {
         const int H = n->sizes[1];
         int T = 128;
         while (T > 16 && (int64_t)T * H > 16384) T >>= 1;
@@ -562,7 +687,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         default: e = hipFuncSetAttribute((const void*)psgd_chunk_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
         }
         if (e != hipSuccess) return bail(fail(n, PNN_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e)));
-    } else {
+    } else if (!n->psgd) {
         const size_t el = n->bf16 ? 2 : 4;
         for (int l = 1; l <= n->L; ++l) {
             const size_t cnt = (size_t)K * B * n->sizes[l] * el;
@@ -697,6 +822,7 @@ pnn_status pnn_get_params(pnn_net* n, int32_t which, float* host_out) {
     if (!host_out) return fail(n, PNN_EINVAL, "host_out is NULL");
     if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
     HIP_TRY(n, hipDeviceSynchronize());
+    TRY(check_abort(n));
     std::vector<float> padded(n->pstride);
     const float* src = which < 0 ? n->merged : n->theta + (size_t)which * n->pstride;
     HIP_TRY(n, hipMemcpy(padded.data(), src, n->pstride * sizeof(float), hipMemcpyDeviceToHost));
