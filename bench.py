@@ -34,41 +34,45 @@ FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 (vector with packed FMA, and matrix
 BF16_PEAK_TFLOPS = 2500.0      # MI355X bf16 dense matrix
 
 
-def kernel_work(w, name: str, launches: int, N: int):
+def method_flops_per_sample(w) -> float:
+    """FLOPs of the method for one training sample of one CN: forward 2*sum(W), weight
+    gradient and update 2*sum(W) (one multiply-add per weight), hidden errors
+    2*sum_{l>=2} W^l, plus the bias terms."""
+    s = w.sizes
+    fw = sum(s[l] * s[l + 1] for l in range(len(s) - 1))
+    back = sum(s[l] * s[l + 1] for l in range(1, len(s) - 1))
+    bias = sum(s[1:])
+    return 4.0 * fw + 2.0 * back + 4.0 * bias
+
+
+def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
     """Algorithmic work of one launch of a library kernel: (bound, flops, bytes).
 
-    Counts follow the method's arithmetic per sample and per CN (no padding, no extra work
-    of the implementation):
-      per-sample plan, with H hidden, O outputs, In inputs, chunk T, K CNs:
-        psgd_chunk  T steps of K CNs: second-layer forward, hidden error and update
-                    (3 * 2*H*O), biases (2*O + 2*H), and the first layer's running
-                    input-sum correction of the chunked form (2*H per earlier sample of the
-                    chunk, (T-1)/2 on average);
-        psgd_p      P = W1 x_t for T samples of K CNs: 2*H*In per sample;
-        psgd_upd    W1 -= eta * sum_t d1_t x_t^T for T samples of K CNs: 2*H*In per sample;
-        psgd_gram   x_t . x_s for the T*T pairs of each chunk: 2*In per pair.
-      merge: reads K*P floats and writes P (and K*P with broadcast) -- HBM bound.
+    psgd_persistent: one launch trains every CN for one epoch (per-sample SGD) -> N samples
+      x the method's FLOPs per sample (the first-layer products run on the matrix cores).
+    fwd_gemm / upd_gemm / bwd_gemm (mini-batch plan): totals over the profiled step of
+      2 * rows * out * in for the layers these kernels handle (output layers of <= 16
+      neurons use the row kernels), divided by the launches.
+    merge: reads K*P floats and writes P (and K*P with broadcast), HBM bound.
     """
     s = w.sizes
     K = w.replicas
-    if name.startswith("psgd"):
-        H, O, In = s[1], s[2], s[0]
-        T = 128
-        while T > 16 and T * H > 16384:
-            T //= 2
-        nk = -(-N // K)
-        nch = -(-nk // T)
-        steps_per_launch = N / nch  # samples of all CNs handled per chunk launch
-        if name == "psgd_chunk":
-            per = 3 * 2 * H * O + 2 * O + 2 * H + 2 * H * (T - 1) / 2
-            return "alu", steps_per_launch * per, steps_per_launch * (H * 4 * 3)
-        if name in ("psgd_p", "psgd_upd"):
-            return "mfma", steps_per_launch * 2 * H * In, steps_per_launch * In * 4 + K * H * In * 4 * 2
-        if name == "psgd_gram":
-            return "mfma", N * T * 2 * In, N * In * 4
+    L = len(s) - 1
+    if name == "psgd_persistent":
+        return "mfma", N * method_flops_per_sample(w), N * s[0] * 4.0 + 2 * K * w.param_count() * 4.0
+    rows = N * epochs_profiled
+    if name == "fwd_gemm":
+        f = sum(2.0 * rows * s[l + 1] * s[l] for l in range(L) if s[l + 1] > 16)
+        return "mfma", f / launches, None
+    if name == "upd_gemm":
+        f = sum(2.0 * rows * s[l + 1] * s[l] for l in range(L) if s[l + 1] > 16)
+        return "mfma", f / launches, None
+    if name == "bwd_gemm":
+        f = sum(2.0 * rows * s[l + 1] * s[l] for l in range(1, L) if s[l + 1] > 16)
+        return "mfma", f / launches, None
     if name == "merge":
         P = w.param_count()
-        return "hbm", 0.0, (K * P + P) * 4.0
+        return "hbm", 0.0, (K * P + P + (K * P if w.merge_every_epoch else 0)) * 4.0
     return None
 
 
@@ -79,6 +83,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run one device-to-device copy of 1 GiB (reference dispatch for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("this build runs on one GPU only: the CNs of a PNN are independent until the merge, "
@@ -88,6 +94,14 @@ def main():
 
     import torch
     from paper_2304_09590_amd import pnn as B
+
+    if args.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print("[bench] calibration copy: 1 GiB read + 1 GiB written", file=sys.stderr, flush=True)
+        del src, dst
 
     w = I.WORKLOADS[args.workload]
     N = w.n_train
@@ -153,7 +167,7 @@ def main():
     if dom is not None:
         tot, n_l = prof[dom]
         avg_s = tot / 1e3 / n_l
-        wk = kernel_work(w, dom, n_l, N)
+        wk = kernel_work(w, dom, n_l, N, w.epochs)
         if wk is not None:
             bound, flops, byts = wk
             if bound == "hbm":
@@ -170,10 +184,11 @@ def main():
         cores = len(os.sched_getaffinity(0))
         threads = max(1, min(w.replicas, cores))
         o = O.Oracle.from_workload(w)
-        # bounded sample: the first n_s rows of every CN's slice, one epoch
+        # bounded sample: the first n_s rows of every CN's slice, one epoch, sized for about
+        # 15 s of work per thread at ~1 GFLOP/s
         per = -(-N // w.replicas)
-        n_s = per if w.batch == 1 and w.sizes[1] <= 128 else max(w.batch, min(per, 400))
-        n_s = min(n_s, per)
+        budget = 15.0 * threads * 1e9 / method_flops_per_sample(w)
+        n_s = int(min(per, max(w.batch, budget // w.replicas)))
         idx = np.concatenate([np.arange(s, s + min(n_s, ln)) for s, ln in
                               (o.shard(N, k) for k in range(w.replicas))])
         th = o.replicate(th0)
