@@ -792,7 +792,7 @@ __device__ inline bool wait_geq(int* flag, int target, int* abort, long limit) {
         ok = good;
     }
     __syncthreads();
-    const bool r = ok != 0;
+    const bool r = __builtin_amdgcn_readfirstlane(ok) != 0;  // uniform: keeps later control flow scalar
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     __syncthreads();
     return r;
@@ -851,7 +851,7 @@ struct PsgdPArgs {
     const float* gramx;  // [K][nch-1][T][T] chunk c (rows) against chunk c-1, c >= 1
     int nch;
     float* qbuf;         // [2][K][T][H]  by chunk parity
-    float* d1;           // [2][K][T][H]  by chunk parity
+    float* d1;           // [2][K][H][T]  by chunk parity (transposed: one row per hidden neuron)
     int* flags;          // qready[K], dready[K], abort
     int H, O, In, act1, act2, loss, nrb;
     float lr;
@@ -859,6 +859,32 @@ struct PsgdPArgs {
 };
 
 constexpr int MAX_IB = 13;  // input blocks of 16 per wave of a tile (4 waves x 13 x 16 >= 784)
+
+// Wave-level bounded wait (no workgroup barrier inside): every lane polls the same flag.
+__device__ inline bool wave_wait_geq(int* flag, int target, int* abort, long limit) {
+    long it = 0;
+    while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        if (__hip_atomic_load(abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+        if (++it > limit) {
+            __hip_atomic_store(abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return true;
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One wave copies `bytes` (a multiple of 1 KiB) from global memory straight into LDS, in
+// 1 KiB pieces piece0, piece0 + stride, ...; completion is tracked by the wave's vmcnt.
+__device__ inline void wave_copy_to_lds(const void* src, float* dst_lds, int bytes, int piece0, int stride, int lane) {
+    for (int pc = piece0; pc * 1024 < bytes; pc += stride)
+        __builtin_amdgcn_global_load_lds((const char*)src + pc * 1024 + lane * 16,
+                                         (lds_void*)((char*)dst_lds + pc * 1024), 16, 0, 0);
+}
+__device__ inline void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 template <int T, int HW, int A1, int A2, int LS, int OC>
 __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& a, int k, float* smem) {
@@ -869,18 +895,22 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     const int act2 = A2 >= 0 ? A2 : a.act2;
     const int loss = LS >= 0 ? LS : a.loss;
     constexpr int nlive = HW >> 6;
+    constexpr int nhelp = 4 - nlive;  // helper waves
     const bool live = tid < HW;
     const int h = live ? tid : (tid - HW) % HW;
     const int part = live ? 0 : (tid - HW) / HW;
+    const int hwave = wave - nlive;  // helper wave index (valid for helpers)
     const bool hv = h < H;
     constexpr int TS = T + 4;  // row stride of the transposed error history
-    float* Pl = smem;                    // [T][HW]
-    float* histA = Pl + T * HW;          // [2][HW][TS]
-    float* Gl = histA + 2 * HW * TS;     // [T][T]
-    float* GXl = Gl + T * T;             // [T][T]
-    float* red = GXl + T * T;            // [2][16 outputs][16 rows]
-    float* cpre = red + 2 * 256;         // [2][3][HW]
-    int* ylds = (int*)(cpre + 6 * HW);   // [T]
+    float* Pl = smem;                    // [T][HW]   input sums of the current chunk
+    float* Qn = Pl + T * HW;             // [T][H]    next chunk's Q (prefetched)
+    float* hist = Qn + T * HW;           // [HW][TS]  first-layer errors of the current chunk
+    constexpr int GS = T + 4;            // Gram row stride: rows 4 banks apart (conflict-free MFMA operand reads)
+    float* Gb = hist + HW * TS;          // [2][T][GS] Gram blocks by chunk parity
+    float* GXn = Gb + 2 * T * GS;        // [T][GS]    next chunk against the current one
+    float* red = GXn + T * GS;           // [2][16 outputs][16 rows]
+    float* cpre = red + 2 * 256;         // [2][HW]
+    int* yb = (int*)(cpre + 2 * HW);     // [2][T] labels by chunk parity
 
     const int64_t nz = shard_len(a.n_total, K, k), xs = shard_start(a.n_total, K, k);
     const int nchk = (int)((nz + T - 1) / T);
@@ -895,88 +925,66 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     int* dready = a.flags + K + k;
     int* abort = a.flags + 2 * K;
     const float lr = a.lr;
-    // padding neurons h >= H must read zero errors in the previous-chunk correction
-    for (int i = tid; i < 2 * HW * TS; i += 256) histA[i] = 0.f;
+    // padding neurons h >= H read zero errors and zero input sums
+    for (int i = tid; i < HW * TS; i += 256) hist[i] = 0.f;
+    for (int i = tid; i < T * HW; i += 256) Pl[i] = 0.f;
 
+    // chunk 0: wait for Q_0 and stage it synchronously
+    if (!wait_geq(qready, a.nrb, abort, a.spin_limit)) return;
+    {
+        const float* Q = a.qbuf + (size_t)k * T * H;
+        const float* G = a.gram + (size_t)k * a.nch * T * GS;
+        const int tc0 = (int)min<int64_t>(T, nz);
+        for (int idx = tid; idx < tc0 * H; idx += 256) Pl[(idx / H) * HW + idx % H] = Q[idx];
+        for (int idx = tid; idx < T * GS; idx += 256) Gb[idx] = G[idx];
+        for (int idx = tid; idx < tc0; idx += 256) yb[idx] = a.y[xs + idx];
+    }
+    __syncthreads();
+
+    // helper-side prefetch state for chunk c + 1
+    bool issued = false;  // this helper wave issued its copies for the next chunk
+    int qseen = 0;        // last value read from qready (a load in flight one step)
     for (int c = 0; c < nchk; ++c) {
         const int tc = __builtin_amdgcn_readfirstlane((int)min<int64_t>(T, nz - (int64_t)c * T));
-        float* hist = histA + (c & 1) * HW * TS;
-        const float* histp = histA + ((c + 1) & 1) * HW * TS;
-        if (!wait_geq(qready, a.nrb * (c + 1), abort, a.spin_limit)) return;
-        {
-            // Q rows, Gram blocks and labels into LDS (float4, loads issued before stores)
-            const float* Q = a.qbuf + ((size_t)(c & 1) * K + k) * T * H;
-            const float* G = a.gram + ((size_t)k * a.nch + c) * T * T;
-            const float* GX = a.gramx + ((size_t)k * (a.nch - 1) + (c - 1)) * T * T;
-            float4 gv[T * T / 1024], gx[T * T / 1024];
-#pragma unroll
-            for (int j = 0; j < T * T / 1024; ++j) {
-                gv[j] = *(const float4*)(G + 4 * (tid + 256 * j));
-                gx[j] = c > 0 ? *(const float4*)(GX + 4 * (tid + 256 * j)) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float* Gl = Gb + (c & 1) * T * GS;
+        const int* ylds = yb + (c & 1) * T;
+        const bool has_next = c + 1 < nchk;
+        const int tcn = has_next ? (int)min<int64_t>(T, nz - (int64_t)(c + 1) * T) : 0;
+        // copies of chunk c + 1's inputs, issued by the helper waves as soon as the tiles
+        // have published its Q (or synchronously at the chunk end)
+        auto issue_next = [&]() {
+            const float* Q = a.qbuf + ((size_t)((c + 1) & 1) * K + k) * T * H;
+            const float* G = a.gram + ((size_t)k * a.nch + c + 1) * T * GS;
+            const float* GX = a.gramx + ((size_t)k * (a.nch - 1) + c) * T * GS;
+            wave_copy_to_lds(Q, Qn, T * H * 4, hwave, nhelp, lane);
+            wave_copy_to_lds(G, Gb + ((c + 1) & 1) * T * GS, T * GS * 4, hwave, nhelp, lane);
+            wave_copy_to_lds(GX, GXn, T * GS * 4, hwave, nhelp, lane);
+            if (hwave == 0) {  // labels: one dword per lane, rows clamped into the slice
+                const int r = min(lane, tcn - 1);
+                __builtin_amdgcn_global_load_lds(a.y + xs + (int64_t)(c + 1) * T + r,
+                                                 (lds_void*)(yb + ((c + 1) & 1) * T), 4, 0, 0);
             }
-            const int hq = HW / 4, nidx = tc * hq;
-            for (int base = 0; base < nidx; base += 4 * 256) {
-                float4 v[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int idx = base + u * 256 + tid, t = idx / hq, h4 = (idx % hq) * 4;
-                    v[u] = (idx < nidx && h4 < H) ? *(const float4*)(Q + (size_t)t * H + h4) : make_float4(0.f, 0.f, 0.f, 0.f);
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int idx = base + u * 256 + tid, t = idx / hq, h4 = (idx % hq) * 4;
-                    if (idx < nidx) *(float4*)(Pl + t * HW + h4) = v[u];
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < T * T / 1024; ++j) {
-                *(float4*)(Gl + 4 * (tid + 256 * j)) = gv[j];
-                *(float4*)(GXl + 4 * (tid + 256 * j)) = gx[j];
-            }
-            for (int idx = tid; idx < tc; idx += 256) ylds[idx] = a.y[xs + (int64_t)c * T + idx];
-        }
-        __syncthreads();
-        if (c > 0) {
-            // previous-chunk correction on the matrix cores:
-            // Pl[t][h] -= eta * sum_s GX[t][s] d1prev_s[h]   (output tiles 16 t x 16 h)
-            const int ntiles = 4 * (HW / 16) * (T / 64);
-            for (int tt = wave; tt < ntiles; tt += 4) {
-                const int mt = tt % (T / 16), nt = tt / (T / 16);
-                f4 acc = {0.f, 0.f, 0.f, 0.f};
-                const int r16 = lane & 15, g = lane >> 4;
-#pragma unroll
-                for (int sl = 0; sl < T / 16; ++sl) {
-                    const float4 av = *(const float4*)(GXl + (mt * 16 + r16) * T + sl * 16 + 4 * g);
-                    const float4 bv = *(const float4*)(histp + (nt * 16 + r16) * TS + sl * 16 + 4 * g);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
-                }
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = mt * 16 + 4 * g + r, hh = nt * 16 + r16;
-                    Pl[t * HW + hh] -= lr * acc[r];
-                }
-            }
-            __syncthreads();
-        }
+        };
+        const int sig_step = min(4, tc - 1);  // step after which the previous chunk's errors are announced
 
         // Steps in blocks of 16.  At the start of block b the errors of block b-1 are folded
         // into the input sums of every later row of the chunk on the matrix cores, so a
         // step's in-chunk correction only needs the earlier steps of its own block.
         float corr = 0.f, dprev = 0.f;
         float pl_next = live ? Pl[h] : 0.f;
-        for (int t = 0; t < tc; ++t) {
+        for (int tt = 0; tt < tc; ++tt) {
+            // the step index is read through readfirstlane so that it stays a scalar (the
+            // live/helper branches below are divergent)
+            const int t = __builtin_amdgcn_readfirstlane(tt);
             const int bs = t & ~15;  // first step of this block
             if (t > 0 && t == bs) {
                 __syncthreads();  // errors of the finished block are in LDS
                 const int sb = bs - 16;
                 const int nmt = (T - bs) >> 4, ntl = nmt * (HW / 16);
                 const int r16 = lane & 15, g = lane >> 4;
-                for (int tt = wave; tt < ntl; tt += 4) {
-                    const int mt = (bs >> 4) + tt % nmt, nt = tt / nmt;
-                    const float4 av = *(const float4*)(Gl + (mt * 16 + r16) * T + sb + 4 * g);
+                for (int ti = wave; ti < ntl; ti += 4) {
+                    const int mt = (bs >> 4) + ti % nmt, nt = ti / nmt;
+                    const float4 av = *(const float4*)(Gl + (mt * 16 + r16) * GS + sb + 4 * g);
                     const float4 bv = *(const float4*)(hist + (nt * 16 + r16) * TS + sb + 4 * g);
                     f4 acc = {0.f, 0.f, 0.f, 0.f};
                     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
@@ -999,31 +1007,50 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 for (int o = 0; o < 16; ++o) p[o] = o < OC ? w2[o < OC ? o : 0] * a1 : 0.f;
                 const float v = row_reduce_scatter16(p, lane);
                 red[(t & 1) * 256 + ol * 16 + wave * 4 + (lane >> 4)] = v;
-            } else if (part == 0 && hv) {
-                // helper: in-block part of the next step's correction, sum over s in
-                // [bs1, t-2] of d1_s G[t+1][s] (at most 14 terms: four masked float4 groups)
-                const int t1 = t + 1, bs1 = t1 & ~15;
-                float sum = 0.f;
-                if (t1 < tc && t - 2 >= bs1) {
-                    const float* g = Gl + t1 * T + bs1;
-                    const float* hr = hist + h * TS + bs1;
-                    const int last = t - 2 - bs1;  // highest offset included
-                    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+            } else {
+                if (part == 0 && hv) {
+                    // in-block part of the next step's correction, sum over s in [bs1, t-2]
+                    // of d1_s G[t+1][s] (at most 14 terms: four masked float4 groups)
+                    const int t1 = t + 1, bs1 = t1 & ~15;
+                    float sum = 0.f;
+                    if (t1 < tc && t - 2 >= bs1) {
+                        const float* g = Gl + t1 * GS + bs1;
+                        const float* hr = hist + h * TS + bs1;
+                        const int last = t - 2 - bs1;  // highest offset included
+                        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        if (4 * q <= last) {
-                            const float4 hv4 = *(const float4*)(hr + 4 * q), gv4 = *(const float4*)(g + 4 * q);
-                            acc.x += hv4.x * gv4.x;
-                            acc.y += (4 * q + 1 <= last) ? hv4.y * gv4.y : 0.f;
-                            acc.z += (4 * q + 2 <= last) ? hv4.z * gv4.z : 0.f;
-                            acc.w += (4 * q + 3 <= last) ? hv4.w * gv4.w : 0.f;
+                        for (int q = 0; q < 4; ++q) {
+                            if (4 * q <= last) {
+                                const float4 hv4 = *(const float4*)(hr + 4 * q), gv4 = *(const float4*)(g + 4 * q);
+                                acc.x += hv4.x * gv4.x;
+                                acc.y += (4 * q + 1 <= last) ? hv4.y * gv4.y : 0.f;
+                                acc.z += (4 * q + 2 <= last) ? hv4.z * gv4.z : 0.f;
+                                acc.w += (4 * q + 3 <= last) ? hv4.w * gv4.w : 0.f;
+                            }
                         }
+                        sum = (acc.x + acc.y) + (acc.z + acc.w);
                     }
-                    sum = (acc.x + acc.y) + (acc.z + acc.w);
+                    cpre[((t + 1) & 1) * HW + h] = sum;
                 }
-                cpre[((t + 1) & 1) * HW + h] = sum;
+                // prefetch of the next chunk: the flag value read last step decides
+                if (has_next && !issued) {
+                    if (__builtin_amdgcn_readfirstlane(qseen) >= a.nrb * (c + 2)) {
+                        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                        issue_next();
+                        issued = true;
+                    } else {
+                        qseen = __hip_atomic_load(qready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
+                // the previous chunk's errors (stored at the chunk start) are announced once
+                // every helper wave's stores have completed
+                if (c > 0 && t == sig_step) wait_vm_all();
             }
             __syncthreads();
+            if (c > 0 && t == sig_step && tid == HW) {
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                __hip_atomic_store(dready, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
             if (live) {
                 // every operand of this phase is read up front
                 const float4* rr = (const float4*)(red + (t & 1) * 256 + ol * 16);
@@ -1034,7 +1061,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 const int bs1 = (t + 1) & ~15;
                 if (t + 1 < tc) {
                     cp = cpre[((t + 1) & 1) * HW + h];
-                    const float* g = Gl + (t + 1) * T;
+                    const float* g = Gl + (t + 1) * GS;
                     g1 = t >= bs1 ? g[t] : 0.f;
                     g0 = t - 1 >= bs1 ? g[t - 1] : 0.f;
                 }
@@ -1066,14 +1093,81 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 dprev = d1;
             }
         }
-        // publish the chunk's first-layer errors
-        __syncthreads();
+
         float* dout = a.d1 + ((size_t)(c & 1) * K + k) * T * H;
-        for (int idx = tid; idx < tc * H; idx += 256) {
-            const int t = idx / H, hh = idx % H;
-            dout[(size_t)t * H + hh] = hist[hh * TS + t];
+        if (has_next) {
+            // chunk boundary: make sure the next chunk's inputs are in LDS
+            if (!live) {
+                if (!issued) {
+                    if (wave_wait_geq(qready, a.nrb * (c + 2), abort, a.spin_limit)) issue_next();
+                }
+                wait_vm_all();
+                issued = false;
+                qseen = 0;
+            }
+            __syncthreads();
+            // previous-chunk correction on the matrix cores, written with the prefetched Q:
+            // Pl[t][h] = Q[t][h] - eta * sum_s GX[t][s] d1_s[h]; two output tiles per pass so
+            // that two independent accumulation chains share the matrix core
+            {
+                constexpr int ntiles = (T / 16) * (HW / 16);
+                const int r16 = lane & 15, g = lane >> 4;
+                for (int ti = wave; ti < ntiles; ti += 8) {
+                    const int tj = ti + 4;
+                    const bool two = tj < ntiles;
+                    const int mt0 = ti % (T / 16), nt0 = ti / (T / 16);
+                    const int mt1 = tj % (T / 16), nt1 = (two ? tj : ti) / (T / 16);
+                    f4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+                    float4 av0[T / 16], bv0[T / 16], av1[T / 16], bv1[T / 16];
+#pragma unroll
+                    for (int sl = 0; sl < T / 16; ++sl) {
+                        av0[sl] = *(const float4*)(GXn + (mt0 * 16 + r16) * GS + sl * 16 + 4 * g);
+                        bv0[sl] = *(const float4*)(hist + (nt0 * 16 + r16) * TS + sl * 16 + 4 * g);
+                        av1[sl] = *(const float4*)(GXn + ((two ? mt1 : mt0) * 16 + r16) * GS + sl * 16 + 4 * g);
+                        bv1[sl] = *(const float4*)(hist + (nt1 * 16 + r16) * TS + sl * 16 + 4 * g);
+                    }
+#pragma unroll
+                    for (int sl = 0; sl < T / 16; ++sl) {
+                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].x, bv0[sl].x, acc0, 0, 0, 0);
+                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].x, bv1[sl].x, acc1, 0, 0, 0);
+                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].y, bv0[sl].y, acc0, 0, 0, 0);
+                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].y, bv1[sl].y, acc1, 0, 0, 0);
+                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].z, bv0[sl].z, acc0, 0, 0, 0);
+                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].z, bv1[sl].z, acc1, 0, 0, 0);
+                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].w, bv0[sl].w, acc0, 0, 0, 0);
+                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].w, bv1[sl].w, acc1, 0, 0, 0);
+                    }
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int t0 = mt0 * 16 + 4 * g + r, h0 = nt0 * 16 + r16;
+                        Pl[t0 * HW + h0] = (h0 < H && t0 < tcn ? Qn[t0 * H + h0] : 0.f) - lr * acc0[r];
+                        if (two) {
+                            const int t1 = mt1 * 16 + 4 * g + r, h1 = nt1 * 16 + r16;
+                            Pl[t1 * HW + h1] = (h1 < H && t1 < tcn ? Qn[t1 * H + h1] : 0.f) - lr * acc1[r];
+                        }
+                    }
+                }
+            }
+            // the helpers store this chunk's errors for the tiles (announced a few steps into
+            // the next chunk, once the stores have completed)
+            if (!live) {
+                // errors published as [h][T] rows, the layout of the LDS history
+                constexpr int NH = 256 - HW;
+                for (int q = tid - HW; q < H * (T / 4); q += NH) {
+                    const int hh = q / (T / 4), t4 = (q % (T / 4)) * 4;
+                    *(float4*)(dout + (size_t)hh * T + t4) = *(const float4*)(hist + hh * TS + t4);
+                }
+            }
+            __syncthreads();
+        } else {
+            // last chunk: publish synchronously
+            __syncthreads();
+            for (int q = tid; q < H * (T / 4); q += 256) {
+                const int hh = q / (T / 4), t4 = (q % (T / 4)) * 4;
+                *(float4*)(dout + (size_t)hh * T + t4) = *(const float4*)(hist + hh * TS + t4);
+            }
+            signal_set(dready, c + 1);
         }
-        signal_set(dready, c + 1);
     }
     if (live && hv) {
         th[a.off_b1 + h] = b1;
@@ -1108,19 +1202,23 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
     constexpr int NMT = T / 16;
     float* red4 = smem;  // [4 waves][NMT][64][4]
 
-    // Q_c = W1 (current registers) x_t for the rows of chunk c, published to qbuf[c & 1]
+    // Q_c = W1 (current registers) x_t for the rows of chunk c, published to qbuf[c & 1].
+    // Out-of-range rows and inputs are read from a clamped (valid) address and masked.
     auto publish_q = [&](int c) {
         const int tc = (int)min<int64_t>(T, nz - (int64_t)c * T);
         const int64_t xb = xs + (int64_t)c * T;
 #pragma unroll
         for (int mt = 0; mt < NMT; ++mt) {
             const int row = mt * 16 + (lane & 15);
+            const bool rok = row < tc;
+            const float* xr = a.X + (size_t)(xb + (rok ? row : 0)) * In;
             float4 xv[MAX_IB];
 #pragma unroll
             for (int j = 0; j < MAX_IB; ++j) {
                 const int ib = wave + 4 * j, i = ib * 16 + 4 * g;
-                xv[j] = (ib < nib && row < tc && i < In) ? *(const float4*)(a.X + (size_t)(xb + row) * In + i)
-                                                          : make_float4(0.f, 0.f, 0.f, 0.f);
+                const bool ok = rok && ib < nib && i < In;
+                const float4 v = *(const float4*)(xr + (ok ? i : 0));
+                xv[j] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
             }
             f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1136,36 +1234,44 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
         float* Q = a.qbuf + ((size_t)(c & 1) * K + k) * T * H;
         for (int e = tid; e < NMT * 256; e += 256) {
             const int mt = e >> 8, rem = e & 255, ln = rem >> 2, r = rem & 3;
-            float s = 0.f;
+            float sum = 0.f;
 #pragma unroll
-            for (int w = 0; w < 4; ++w) s += red4[((size_t)(w * NMT + mt) * 64 + ln) * 4 + r];
+            for (int w = 0; w < 4; ++w) sum += red4[((size_t)(w * NMT + mt) * 64 + ln) * 4 + r];
             const int t = mt * 16 + 4 * (ln >> 4) + r, hh = rb * 16 + (ln & 15);
-            if (t < tc && hh < H) Q[(size_t)t * H + hh] = s;
+            if (t < tc && hh < H) Q[(size_t)t * H + hh] = sum;
         }
         signal_add(qready, 1);
     };
-    // W1 tile -= eta * sum_t d1_t x_t^T over the rows of chunk c
+    // W1 tile -= eta * sum_t d1_t x_t^T over the rows of chunk c (errors stored [h][T])
     auto update = [&](int c) {
         const int tc = (int)min<int64_t>(T, nz - (int64_t)c * T);
         const int64_t xb = xs + (int64_t)c * T;
-        const float* D = a.d1 + ((size_t)(c & 1) * K + k) * T * H;
+        const float* D = a.d1 + ((size_t)(c & 1) * K + k) * H * T + (size_t)(h < H ? h : 0) * T;
         float bv[T / 4];
+#pragma unroll
+        for (int sl = 0; sl < T / 16; ++sl) {
+            const float4 d = *(const float4*)(D + sl * 16 + 4 * g);
+            const int t0 = sl * 16 + 4 * g;
+            bv[4 * sl + 0] = (h < H && t0 + 0 < tc) ? d.x : 0.f;
+            bv[4 * sl + 1] = (h < H && t0 + 1 < tc) ? d.y : 0.f;
+            bv[4 * sl + 2] = (h < H && t0 + 2 < tc) ? d.z : 0.f;
+            bv[4 * sl + 3] = (h < H && t0 + 3 < tc) ? d.w : 0.f;
+        }
+        const float* xrow[T / 4];
 #pragma unroll
         for (int u = 0; u < T / 4; ++u) {
             const int t = (u >> 2) * 16 + 4 * g + (u & 3);
-            bv[u] = (t < tc && h < H) ? D[(size_t)t * H + h] : 0.f;
+            xrow[u] = a.X + (size_t)(xb + (t < tc ? t : 0)) * In;
         }
 #pragma unroll
         for (int j = 0; j < MAX_IB; ++j) {
             const int ib = wave + 4 * j;
             if (ib >= nib) continue;
             const int icol = ib * 16 + (lane & 15);
+            const int ic = icol < In ? icol : 0;
             float av[T / 4];
 #pragma unroll
-            for (int u = 0; u < T / 4; ++u) {
-                const int t = (u >> 2) * 16 + 4 * g + (u & 3);
-                av[u] = (t < tc && icol < In) ? a.X[(size_t)(xb + t) * In + icol] : 0.f;
-            }
+            for (int u = 0; u < T / 4; ++u) av[u] = xrow[u][ic];  // bv is zero where the row is out of range
             f4 dacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int u = 0; u < T / 4; ++u) dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], dacc, 0, 0, 0);
@@ -1174,16 +1280,22 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
         }
     };
 
-    publish_q(0);
-    if (nchk > 1) publish_q(1);
+    // Q_0 and Q_1 use the initial weights; afterwards chunk c's errors (c >= 0) are applied
+    // before Q_{c+2} is computed.  One call site each keeps the code compact.
     bool ok = true;
-    for (int c = 1; c < nchk && ok; ++c) {
-        if (!wait_geq(dready, c, abort, a.spin_limit)) { ok = false; break; }
-        update(c - 1);
-        if (c + 1 < nchk) publish_q(c + 1);
+    for (int step = 0; step <= nchk && ok; ++step) {
+        // step 0: publish Q_0 (and Q_1); step s >= 1: apply the errors of chunk s-1, then
+        // publish Q_{s+1}
+        if (step >= 1) {
+            if (!wait_geq(dready, step, abort, a.spin_limit)) { ok = false; break; }
+            update(step - 1);
+        }
+        const int first = step == 0 ? 0 : step + 1;
+        const int last = step == 0 ? min(1, nchk - 1) : step + 1;
+        for (int cq = first; cq <= last; ++cq)
+            if (cq < nchk) publish_q(cq);
     }
-    if (!ok || !wait_geq(dready, nchk, abort, a.spin_limit)) return;
-    update(nchk - 1);
+    if (!ok) return;
 #pragma unroll
     for (int j = 0; j < MAX_IB; ++j)
 #pragma unroll

@@ -397,15 +397,16 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
         *have = need;
         return PNN_OK;
     };
-    TRY(grow(&n->gram, &n->gram_elems, (size_t)K * nch * PT * PT));
-    TRY(grow(&n->gramx, &n->gramx_elems, (size_t)K * std::max(nch - 1, 1) * PT * PT));
+    constexpr int GS = PT + 4;  // padded Gram row stride (matches the kernel's LDS layout)
+    TRY(grow(&n->gram, &n->gram_elems, (size_t)K * nch * PT * GS));
+    TRY(grow(&n->gramx, &n->gramx_elems, (size_t)K * std::max(nch - 1, 1) * PT * GS));
     {
         // G_c[t][s] = x_t . x_s within every chunk
         GemmArgs g = gemm_base(n, PT, PT, In, N, 0, PT, 3);
         g.a = opnd(X, 0, In, 1);
         g.b = opnd(X, 0, In, 1);
         g.zdiv = nch; g.r0_step = PT;
-        g.c = n->gram; g.c_z = (int64_t)PT * PT; g.c_ld = PT;
+        g.c = n->gram; g.c_z = (int64_t)PT * GS; g.c_ld = GS;
         TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K * nch, "psgd_gram")));
     }
     if (nch > 1) {
@@ -414,7 +415,7 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
         g.a = opnd(X, 0, In, 1);
         g.b = opnd(X, 0, In, 1, -PT);
         g.zdiv = nch - 1; g.r0_step = PT;
-        g.c = n->gramx; g.c_z = (int64_t)PT * PT; g.c_ld = PT;
+        g.c = n->gramx; g.c_z = (int64_t)PT * GS; g.c_ld = GS;
         TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K * (nch - 1), "psgd_gram")));
     }
     {
@@ -648,7 +649,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         const int nrb = (H + 15) / 16;
         const int HW = (H + 63) & ~63;
         const size_t rec_smem =
-            (size_t)(PT * HW + 2 * HW * (PT + 4) + 2 * PT * PT + 512 + 6 * HW + PT) * sizeof(float);
+            (size_t)(2 * PT * HW + HW * (PT + 4) + 3 * PT * (PT + 4) + 512 + 2 * HW + 2 * PT) * sizeof(float);
         const size_t tile_smem = (size_t)4 * (PT / 16) * 64 * 4 * sizeof(float);
         n->psmem = std::max(rec_smem, tile_smem);
         n->pspecial = n->act[0] == PNN_SIGMOID && n->act[1] == PNN_SIGMOID && cfg->loss == PNN_LOSS_MSE && O == 10;
