@@ -850,7 +850,9 @@ struct PsgdPArgs {
     const float* gram;   // [K][nch][T][T]   within each chunk
     const float* gramx;  // [K][nch-1][T][T] chunk c (rows) against chunk c-1, c >= 1
     int nch;
-    float* qbuf;         // [2][K][T][H]  by chunk parity
+    float* qbuf;         // [2][K] slots of qslot floats by chunk parity: Q transposed, [neuron][row]
+    int qstride;         // row stride (per neuron) within a slot
+    int64_t qslot;
     float* d1;           // [2][K][H][T]  by chunk parity (transposed: one row per hidden neuron)
     int* flags;          // qready[K], dready[K], abort
     int H, O, In, act1, act2, loss, nrb;
@@ -886,296 +888,676 @@ __device__ inline void wave_copy_to_lds(const void* src, float* dst_lds, int byt
 }
 __device__ inline void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
-template <int T, int HW, int A1, int A2, int LS, int OC>
+// Workgroup barrier for exchanges through LDS only: waits for the wave's own LDS accesses
+// (lgkmcnt) but not for its global loads, so copies and polls in flight stay in flight.
+// (__syncthreads also waits for every outstanding global access of every wave.)
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// ------------------------------------------------------------------------------------
+// Cross-lane building blocks of the sequential per-sample steps (one wavefront).
+
+// Reduction of 10 per-lane values over the whole wavefront.  Afterwards, in every row of
+// 16 lanes, lanes 0, 1, 2, 4, 6, 8, 9, 10, 12, 14 hold the wave totals of values 0..9
+// (own10 below); the other lanes hold no total.  Rounds 1 and 2 are reduce-scatters with
+// bank-masked DPP (row mirror, half-row mirror), so each pairing costs one instruction per
+// kept value; rounds 3 and 4 pair lanes within quads; the four rows are then summed with
+// the permlane swaps.
+__device__ inline float reduce10(const float (&p)[10], int lane) {
+    float a0, a1, a2, a3, a4, b0, b1, b2;
+    asm volatile(
+        "s_nop 1\n\t"
+        // lanes 0-7 keep values 0-4, lanes 8-15 keep values 5-9 (partner: lane 15 - i)
+        "v_add_f32_dpp %0, %8, %8 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %1, %9, %9 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %2, %10, %10 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %3, %11, %11 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %4, %12, %12 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %0, %13, %13 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %1, %14, %14 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %2, %15, %15 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %3, %16, %16 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %4, %17, %17 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        // lanes of banks 0 and 2 keep their first three, banks 1 and 3 their last two
+        // (in b0 and b2) (partner: lane 7 - i within each half row)
+        "v_add_f32_dpp %5, %0, %0 row_half_mirror row_mask:0xf bank_mask:0x5\n\t"
+        "v_add_f32_dpp %6, %1, %1 row_half_mirror row_mask:0xf bank_mask:0x5\n\t"
+        "v_add_f32_dpp %7, %2, %2 row_half_mirror row_mask:0xf bank_mask:0x5\n\t"
+        "v_add_f32_dpp %5, %3, %3 row_half_mirror row_mask:0xf bank_mask:0xa\n\t"
+        "v_add_f32_dpp %7, %4, %4 row_half_mirror row_mask:0xf bank_mask:0xa"
+        : "=&v"(a0), "=&v"(a1), "=&v"(a2), "=&v"(a3), "=&v"(a4), "=&v"(b0), "=&v"(b1), "=&v"(b2)
+        : "v"(p[0]), "v"(p[1]), "v"(p[2]), "v"(p[3]), "v"(p[4]), "v"(p[5]), "v"(p[6]), "v"(p[7]), "v"(p[8]),
+          "v"(p[9]));
+    // quads: lanes with bit 1 set keep b2, the others b0 and b1; then bit 0 splits b0 / b1
+    const bool q1 = lane & 2, q0 = lane & 1;
+    const float k3 = q1 ? b2 : b0, s3 = q1 ? b0 : b2;
+    const float c0 = k3 + dpp<DPP_XOR2>(s3);
+    const float c1 = b1 + dpp<DPP_XOR2>(b1);
+    const float k4 = q0 ? c1 : c0, s4 = q0 ? c0 : c1;
+    float d = k4 + dpp<DPP_XOR1>(s4);
+    // sum of the four rows
+    auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(d), __float_as_uint(d), false, false);
+    d = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+    auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(d), __float_as_uint(d), false, false);
+    return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+// value index held by lane l (mod 16) after reduce10, -1 for none:
+// 0 1 2 - 3 - 4 - | 5 6 7 - 8 - 9 -
+__device__ inline int own10(int l16) {
+    const int base = (l16 >> 3) * 5, r = l16 & 7;
+    return r < 3 ? base + r : (r == 4 ? base + 3 : (r == 6 ? base + 4 : -1));
+}
+constexpr int SRC10[10] = {0, 1, 2, 4, 6, 8, 9, 10, 12, 14};  // lane of each total within a row
+
+// Reduction of 16 per-lane values over the wavefront; afterwards lane l holds the total of
+// value l & 15 (all rounds are reduce-scatters, bank-masked where the pairing allows).
+__device__ inline float reduce16(const float (&p)[16], int lane) {
+    float a[8], b[4];
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_add_f32_dpp %0, %12, %12 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %1, %13, %13 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %2, %14, %14 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %3, %15, %15 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %4, %16, %16 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %5, %17, %17 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %6, %18, %18 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %7, %19, %19 row_mirror row_mask:0xf bank_mask:0x3\n\t"
+        "v_add_f32_dpp %0, %20, %20 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %1, %21, %21 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %2, %22, %22 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %3, %23, %23 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %4, %24, %24 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %5, %25, %25 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %6, %26, %26 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %7, %27, %27 row_mirror row_mask:0xf bank_mask:0xc\n\t"
+        "v_add_f32_dpp %8, %0, %0 row_half_mirror row_mask:0xf bank_mask:0x5\n\t"
+        "v_add_f32_dpp %9, %1, %1 row_half_mirror row_mask:0xf bank_mask:0x5\n\t"
+        "v_add_f32_dpp %10, %2, %2 row_half_mirror row_mask:0xf bank_mask:0x5\n\t"
+        "v_add_f32_dpp %11, %3, %3 row_half_mirror row_mask:0xf bank_mask:0x5\n\t"
+        "v_add_f32_dpp %8, %4, %4 row_half_mirror row_mask:0xf bank_mask:0xa\n\t"
+        "v_add_f32_dpp %9, %5, %5 row_half_mirror row_mask:0xf bank_mask:0xa\n\t"
+        "v_add_f32_dpp %10, %6, %6 row_half_mirror row_mask:0xf bank_mask:0xa\n\t"
+        "v_add_f32_dpp %11, %7, %7 row_half_mirror row_mask:0xf bank_mask:0xa"
+        : "=&v"(a[0]), "=&v"(a[1]), "=&v"(a[2]), "=&v"(a[3]), "=&v"(a[4]), "=&v"(a[5]), "=&v"(a[6]), "=&v"(a[7]),
+          "=&v"(b[0]), "=&v"(b[1]), "=&v"(b[2]), "=&v"(b[3])
+        : "v"(p[0]), "v"(p[1]), "v"(p[2]), "v"(p[3]), "v"(p[4]), "v"(p[5]), "v"(p[6]), "v"(p[7]), "v"(p[8]),
+          "v"(p[9]), "v"(p[10]), "v"(p[11]), "v"(p[12]), "v"(p[13]), "v"(p[14]), "v"(p[15]));
+    const bool q1 = lane & 2, q0 = lane & 1;
+    float c[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const float kk = q1 ? b[j + 2] : b[j], ss = q1 ? b[j] : b[j + 2];
+        c[j] = kk + dpp<DPP_XOR2>(ss);
+    }
+    const float kk = q0 ? c[1] : c[0], ss = q0 ? c[0] : c[1];
+    float d = kk + dpp<DPP_XOR1>(ss);
+    auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(d), __float_as_uint(d), false, false);
+    d = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+    auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(d), __float_as_uint(d), false, false);
+    return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+
+// back += bcast(d2 from lane SRC of the row) * w;  w += bcast(d2) * na  (one output, one
+// neuron per lane; na = -eta * a1).  FIRST adds the two wait states a DPP read needs after a
+// VALU write of its source; they sit in the same statement as the reads of d2, so the
+// compiler cannot separate them from the write.
+#define PNN_BCAST_UPD(SRC)                                                                                   \
+    template <bool FIRST>                                                                                    \
+    __device__ inline void bcast_upd_##SRC(float& back, float& w, float d2, float na) {                     \
+        if (FIRST)                                                                                           \
+            asm volatile("s_nop 1\n\t"                                                                      \
+                         "v_fmac_f32_dpp %0, %2, %1 row_newbcast:" #SRC " row_mask:0xf bank_mask:0xf\n\t"  \
+                         "v_fmac_f32_dpp %1, %2, %3 row_newbcast:" #SRC " row_mask:0xf bank_mask:0xf"      \
+                         : "+v"(back), "+v"(w)                                                               \
+                         : "v"(d2), "v"(na));                                                                \
+        else                                                                                                 \
+            asm volatile("v_fmac_f32_dpp %0, %2, %1 row_newbcast:" #SRC " row_mask:0xf bank_mask:0xf\n\t"  \
+                         "v_fmac_f32_dpp %1, %2, %3 row_newbcast:" #SRC " row_mask:0xf bank_mask:0xf"      \
+                         : "+v"(back), "+v"(w)                                                               \
+                         : "v"(d2), "v"(na));                                                                \
+    }
+PNN_BCAST_UPD(0) PNN_BCAST_UPD(1) PNN_BCAST_UPD(2) PNN_BCAST_UPD(3) PNN_BCAST_UPD(4) PNN_BCAST_UPD(5)
+PNN_BCAST_UPD(6) PNN_BCAST_UPD(7) PNN_BCAST_UPD(8) PNN_BCAST_UPD(9) PNN_BCAST_UPD(10) PNN_BCAST_UPD(11)
+PNN_BCAST_UPD(12) PNN_BCAST_UPD(13) PNN_BCAST_UPD(14) PNN_BCAST_UPD(15)
+#undef PNN_BCAST_UPD
+
+template <int SRC, bool FIRST>
+__device__ inline void bcast_upd(float& back, float& w, float d2, float na) {
+    if constexpr (SRC == 0) bcast_upd_0<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 1) bcast_upd_1<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 2) bcast_upd_2<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 3) bcast_upd_3<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 4) bcast_upd_4<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 5) bcast_upd_5<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 6) bcast_upd_6<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 7) bcast_upd_7<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 8) bcast_upd_8<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 9) bcast_upd_9<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 10) bcast_upd_10<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 11) bcast_upd_11<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 12) bcast_upd_12<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 13) bcast_upd_13<FIRST>(back, w, d2, na);
+    else if constexpr (SRC == 14) bcast_upd_14<FIRST>(back, w, d2, na);
+    else bcast_upd_15<FIRST>(back, w, d2, na);
+}
+
+// Output error broadcast and second-layer update for every output o (compile-time loop):
+// back_j += W2[o][h_j] * d2_o (pre-update weights, eq. (11)); W2[o][h_j] -= eta d2_o a1_j.
+template <int OC, int NH, int O>
+__device__ inline void backprop_outputs(float (&back)[NH], float (&w2)[NH][OC], float d2, const float (&na)[NH]) {
+    if constexpr (O < OC) {
+        constexpr int src = OC == 10 ? SRC10[O] : O;
+#pragma unroll
+        for (int j = 0; j < NH; ++j) {
+            if (j == 0) bcast_upd<src, O == 0>(back[j], w2[j][O], d2, na[j]);
+            else bcast_upd<src, false>(back[j], w2[j][O], d2, na[j]);
+        }
+        backprop_outputs<OC, NH, O + 1>(back, w2, d2, na);
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Fold of one finished block of BS steps into stored input sums, on the matrix cores:
+//   PlT[h][t] -= eta * sum_{s in block} G[t][s] * D[h][s]      for rows t in [r0, r1)
+// (r0 a multiple of 8, at most MT tiles of 16 rows) and the NT neuron tiles starting at
+// nt0 (16 neurons each).  G rows have stride GS; D and PlT rows (one per neuron) have
+// stride TS.  v_mfma_f32_16x16x4_f32 contracts 4 steps per instruction; lane group
+// g = lane / 16 supplies the steps s0 + (BS/4) g + q of instruction q (the same permutation
+// of the steps on both operands).  A lane's accumulator holds rows 4g .. 4g+3 of one
+// neuron, contiguous in PlT: one 16-byte read-modify-write per tile.  All operand reads are
+// issued first, then the MT x NT independent accumulation chains, then the read-modify-
+// writes, so the latencies overlap.  Rows of a partial group at or past r1 are unused rows
+// of the buffer.
+template <int GS, int TS, int BS, int MT, int NT>
+__device__ __attribute__((always_inline)) inline void fold_tiles(float* PlT, const float* G, const float* D, int r0, int r1, int s0, float lr,
+                                  int nt0, int lane) {
+    constexpr int NQ = BS / 4;  // instructions per tile
+    static_assert(BS == 8 || BS == 16, "block of 8 or 16 steps");
+    typedef float vq __attribute__((ext_vector_type(NQ)));
+    const int r16 = lane & 15, g = lane >> 4;
+    vq av[MT], bv[NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int row = min(r0 + mt * 16 + r16, r1 - 1);  // rows past r1 feed discarded outputs
+        av[mt] = *(const vq*)(G + row * GS + s0 + NQ * g);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) bv[nt] = *(const vq*)(D + ((nt0 + nt) * 16 + r16) * TS + s0 + NQ * g);
+    f4 acc[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt][0], bv[nt][0], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+#pragma unroll
+    for (int q = 1; q < NQ; ++q)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt][q], bv[nt][q], acc[mt][nt], 0, 0, 0);
+    float4 v[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            if (r0 + mt * 16 + 4 * g < r1)
+                v[mt][nt] = *(const float4*)(PlT + ((nt0 + nt) * 16 + r16) * TS + r0 + mt * 16 + 4 * g);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            if (r0 + mt * 16 + 4 * g < r1) {
+                float4 w = v[mt][nt];
+                w.x -= lr * acc[mt][nt][0]; w.y -= lr * acc[mt][nt][1];
+                w.z -= lr * acc[mt][nt][2]; w.w -= lr * acc[mt][nt][3];
+                *(float4*)(PlT + ((nt0 + nt) * 16 + r16) * TS + r0 + mt * 16 + 4 * g) = w;
+            }
+}
+// (the number of row tiles is wave-uniform: one instance per count, no predicated MFMA)
+template <int GS, int TS, int BS, int MT, int NT>
+__device__ __attribute__((always_inline)) inline void fold_block(float* PlT, const float* G, const float* D, int r0, int r1, int s0, float lr,
+                                  int nt0, int lane) {
+    const int nmt = __builtin_amdgcn_readfirstlane((r1 - r0 + 15) >> 4);
+    static_assert(MT == 4, "up to four row tiles (chunks of 64 rows)");
+    switch (nmt) {
+    case 1: fold_tiles<GS, TS, BS, 1, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
+    case 2: fold_tiles<GS, TS, BS, 2, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
+    case 3: fold_tiles<GS, TS, BS, 3, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
+    case 4: fold_tiles<GS, TS, BS, 4, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
+    default: break;
+    }
+}
+
+// Bounded wait on a counter in LDS written by another wave of the workgroup.  The LDS
+// abort flag (or the spin limit, which raises it together with the grid-wide abort flag)
+// ends every wait, so the workgroup always drains.
+__device__ inline bool lds_wait_geq(const int* f, int target, int* lab, int* gabort, long limit, bool sleep) {
+    long it = 0;
+    while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < target) {
+        if (__hip_atomic_load(lab, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) return false;
+        if (++it > limit) {
+            __hip_atomic_store(lab, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            __hip_atomic_store(gabort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+        if (sleep) __builtin_amdgcn_s_sleep(1);
+    }
+    asm volatile("" ::: "memory");  // later LDS reads stay after the counter read
+    return true;
+}
+__device__ inline int lds_read(const int* f) {
+    const int v = __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    asm volatile("" ::: "memory");
+    return __builtin_amdgcn_readfirstlane(v);
+}
+// Counter update after LDS stores: a wave's LDS accesses complete in issue order, so a
+// reader that sees the counter (and reads the data after it) sees the data.  The compiler
+// barrier keeps the stores before the counter.
+__device__ inline void lds_publish(int* f, int v) {
+    asm volatile("" ::: "memory");
+    __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// ------------------------------------------------------------------------------------
+// The sequential workgroup of one CN (per-sample SGD, one persistent launch per epoch).
+//
+// Notation: steps are numbered over the CN's slice (global step r); chunk c holds steps
+// [cT, cT + T), block B holds steps [BS B, BS B + BS) (BS = 8: eight blocks per chunk).  With W1^(c)
+// the first-layer weights before chunk c, the first-layer input sum of step r in chunk c is
+//   z1_r = Q_c[r] + b1_r - eta * sum_{s in [T(c-1), r)} d1_s (x_s . x_r)
+// where Q_c[r] = W1^(c-1) x_r is published by the tile workgroups.  The dot products come
+// from the Gram blocks G_c (within chunk c) and GX_c (chunk c against chunk c-1).
+//
+// Who adds which term d1_s (x_s . x_r) of row r (block B):
+//   s < BS(B-1):        folded into the stored input sums Pl of row r in the background, on
+//                       the matrix cores, a whole block at a time;
+//   s in [BS(B-1), r-3]: the window correction cpre[r] (at most 2 BS - 3 terms), computed by
+//                       wave 1 while the live wave runs steps r-2 and r-1;
+//   s = r-2, r-1:       the live wave, with its own fresh errors.
+//
+// Waves (256 threads), each in its own loop, coordinated through counters in LDS:
+//   wave 0, live:  the steps.  Lane l owns hidden neurons l and l + 64 (NH = 2) or l
+//                  (NH = 1): their b1 and W2 columns stay in registers.
+//   wave 1:        the window corrections, one row ahead of the live wave.
+//   waves 2, 3:    the folds, each for half of the neurons: a finished block B' goes into
+//                  the rows of blocks >= B'+2 of its chunk (a chunk's last block: into rows
+//                  [BS, T) of the next chunk) as soon as it is finished, and (the other
+//                  blocks) into all rows of the next chunk once that chunk's data is in LDS.
+//                  Wave 3 also publishes each finished block's d1 for the tile workgroups,
+//                  announces finished chunks to them, and loads the next chunk's Q, Gram
+//                  blocks and labels into LDS once the tiles have published Q.
+// Counters (LDS): d1done (steps whose d1 is in hist), cdone (rows whose cpre is ready),
+// fcur (blocks folded into the rows of the chunk that needs them), fnext (blocks folded
+// into the next chunk's rows), nready (chunks whose data is in LDS), pubd (blocks whose d1
+// has been copied out of hist), abort.
+template <int T, int NH, int A1, int A2, int LS, int OC>
 __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& a, int k, float* smem) {
+    constexpr int HW = 64 * NH;     // neurons covered by the live wave
+    constexpr int TS = T + 4;       // row stride of the error history ([neuron][step in chunk])
+    constexpr int GS = T + 4;       // row stride of the Gram blocks (conflict-free MFMA operand reads)
+    constexpr int BS = 8;           // steps per fold block
+    constexpr int NB = T / BS;      // blocks per chunk
+    static_assert(T == 64, "chunks of 64 steps");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int H = a.H, K = a.k_rep;
-    const int O = OC < 16 ? OC : a.O;
-    const int act1 = A1 >= 0 ? A1 : a.act1;
-    const int act2 = A2 >= 0 ? A2 : a.act2;
-    const int loss = LS >= 0 ? LS : a.loss;
-    constexpr int nlive = HW >> 6;
-    constexpr int nhelp = 4 - nlive;  // helper waves
-    const bool live = tid < HW;
-    const int h = live ? tid : (tid - HW) % HW;
-    const int part = live ? 0 : (tid - HW) / HW;
-    const int hwave = wave - nlive;  // helper wave index (valid for helpers)
-    const bool hv = h < H;
-    constexpr int TS = T + 4;  // row stride of the transposed error history
-    float* Pl = smem;                    // [T][HW]   input sums of the current chunk
-    float* Qn = Pl + T * HW;             // [T][H]    next chunk's Q (prefetched)
-    float* hist = Qn + T * HW;           // [HW][TS]  first-layer errors of the current chunk
-    constexpr int GS = T + 4;            // Gram row stride: rows 4 banks apart (conflict-free MFMA operand reads)
-    float* Gb = hist + HW * TS;          // [2][T][GS] Gram blocks by chunk parity
-    float* GXn = Gb + 2 * T * GS;        // [T][GS]    next chunk against the current one
-    float* red = GXn + T * GS;           // [2][16 outputs][16 rows]
-    float* cpre = red + 2 * 256;         // [2][HW]
-    int* yb = (int*)(cpre + 2 * HW);     // [2][T] labels by chunk parity
+    const float lr = a.lr;
+
+    float* Pl = smem;                   // [2][HW][TS] input sums (transposed: [neuron][row]) by chunk parity
+    float* hist = Pl + 2 * HW * TS;     // [HW][TS]   first-layer errors by step mod T
+    float* Gin = hist + HW * TS;        // [2][T][GS] Gram blocks within a chunk, by parity
+    float* GX = Gin + 2 * T * GS;       // [T][GS]    a chunk (rows) against the previous one
+    float* cpre = GX + T * GS;          // [2][HW]    window corrections by row parity
+    int* yb = (int*)(cpre + 2 * HW);    // [2][T]     labels by chunk parity
+    int* lf = yb + 2 * T;
+    int* d1done = lf;
+    int* cdone = lf + 1;
+    int* fcur = lf + 2;    // [2]: one counter per folding wave
+    int* fnext = lf + 4;   // [2]
+    int* nready = lf + 6;
+    int* lab = lf + 7;
+    int* pubd = lf + 8;
 
     const int64_t nz = shard_len(a.n_total, K, k), xs = shard_start(a.n_total, K, k);
-    const int nchk = (int)((nz + T - 1) / T);
+    const int nsteps = (int)nz;
+    const int nchk = (nsteps + T - 1) / T;
+    const int nblk = (nsteps + BS - 1) / BS;
     float* th = a.theta + (size_t)k * a.pstride;
-    float b1 = (live && hv) ? th[a.off_b1 + h] : 0.f;
-    float w2[OC];
-#pragma unroll
-    for (int o = 0; o < OC; ++o) w2[o] = (live && hv && o < O) ? th[a.off_w2 + (size_t)o * H + h] : 0.f;
-    const int ol = lane & 15;
-    float b2v = (ol < O) ? th[a.off_b2 + ol] : 0.f;
     int* qready = a.flags + k;
     int* dready = a.flags + K + k;
-    int* abort = a.flags + 2 * K;
-    const float lr = a.lr;
+    int* gabort = a.flags + 2 * K;
+
     // padding neurons h >= H read zero errors and zero input sums
     for (int i = tid; i < HW * TS; i += 256) hist[i] = 0.f;
-    for (int i = tid; i < T * HW; i += 256) Pl[i] = 0.f;
+    for (int i = tid; i < 2 * HW * TS; i += 256) Pl[i] = 0.f;
+    if (tid < 12) lf[tid] = 0;
 
-    // chunk 0: wait for Q_0 and stage it synchronously
-    if (!wait_geq(qready, a.nrb, abort, a.spin_limit)) return;
+    // chunk 0: wait for Q_0 and stage it with the Gram block and labels
+    if (!wait_geq(qready, a.nrb, gabort, a.spin_limit)) return;
     {
-        const float* Q = a.qbuf + (size_t)k * T * H;
+        const float* Q = a.qbuf + (size_t)k * HW * TS;
         const float* G = a.gram + (size_t)k * a.nch * T * GS;
-        const int tc0 = (int)min<int64_t>(T, nz);
-        for (int idx = tid; idx < tc0 * H; idx += 256) Pl[(idx / H) * HW + idx % H] = Q[idx];
-        for (int idx = tid; idx < T * GS; idx += 256) Gb[idx] = G[idx];
+        const int tc0 = min(T, nsteps);
+        for (int idx = tid; idx < HW * TS; idx += 256) Pl[idx] = Q[idx];
+        for (int idx = tid; idx < T * GS; idx += 256) Gin[idx] = G[idx];
         for (int idx = tid; idx < tc0; idx += 256) yb[idx] = a.y[xs + idx];
+        if (tid == 0) nready[0] = 1;
     }
     __syncthreads();
 
-    // helper-side prefetch state for chunk c + 1
-    bool issued = false;  // this helper wave issued its copies for the next chunk
-    int qseen = 0;        // last value read from qready (a load in flight one step)
-    for (int c = 0; c < nchk; ++c) {
-        const int tc = __builtin_amdgcn_readfirstlane((int)min<int64_t>(T, nz - (int64_t)c * T));
-        const float* Gl = Gb + (c & 1) * T * GS;
-        const int* ylds = yb + (c & 1) * T;
-        const bool has_next = c + 1 < nchk;
-        const int tcn = has_next ? (int)min<int64_t>(T, nz - (int64_t)(c + 1) * T) : 0;
-        // copies of chunk c + 1's inputs, issued by the helper waves as soon as the tiles
-        // have published its Q (or synchronously at the chunk end)
-        auto issue_next = [&]() {
-            const float* Q = a.qbuf + ((size_t)((c + 1) & 1) * K + k) * T * H;
-            const float* G = a.gram + ((size_t)k * a.nch + c + 1) * T * GS;
-            const float* GX = a.gramx + ((size_t)k * (a.nch - 1) + c) * T * GS;
-            wave_copy_to_lds(Q, Qn, T * H * 4, hwave, nhelp, lane);
-            wave_copy_to_lds(G, Gb + ((c + 1) & 1) * T * GS, T * GS * 4, hwave, nhelp, lane);
-            wave_copy_to_lds(GX, GXn, T * GS * 4, hwave, nhelp, lane);
-            if (hwave == 0) {  // labels: one dword per lane, rows clamped into the slice
-                const int r = min(lane, tcn - 1);
-                __builtin_amdgcn_global_load_lds(a.y + xs + (int64_t)(c + 1) * T + r,
-                                                 (lds_void*)(yb + ((c + 1) & 1) * T), 4, 0, 0);
-            }
-        };
-        const int sig_step = min(4, tc - 1);  // step after which the previous chunk's errors are announced
+    auto chunk_len = [&](int c) { return min(T, nsteps - c * T); };
+    // Gram block of chunk c against itself
+    auto grow_in = [&](int c) { return Gin + (c & 1) * T * GS; };
 
-        // Steps in blocks of 16.  At the start of block b the errors of block b-1 are folded
-        // into the input sums of every later row of the chunk on the matrix cores, so a
-        // step's in-chunk correction only needs the earlier steps of its own block.
-        float corr = 0.f, dprev = 0.f;
-        float pl_next = live ? Pl[h] : 0.f;
-        for (int tt = 0; tt < tc; ++tt) {
-            // the step index is read through readfirstlane so that it stays a scalar (the
-            // live/helper branches below are divergent)
-            const int t = __builtin_amdgcn_readfirstlane(tt);
-            const int bs = t & ~15;  // first step of this block
-            if (t > 0 && t == bs) {
-                __syncthreads();  // errors of the finished block are in LDS
-                const int sb = bs - 16;
-                const int nmt = (T - bs) >> 4, ntl = nmt * (HW / 16);
-                const int r16 = lane & 15, g = lane >> 4;
-                for (int ti = wave; ti < ntl; ti += 4) {
-                    const int mt = (bs >> 4) + ti % nmt, nt = ti / nmt;
-                    const float4 av = *(const float4*)(Gl + (mt * 16 + r16) * GS + sb + 4 * g);
-                    const float4 bv = *(const float4*)(hist + (nt * 16 + r16) * TS + sb + 4 * g);
-                    f4 acc = {0.f, 0.f, 0.f, 0.f};
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+    if (wave == 0) {
+        // ================= live wave
+        const int O = OC < 16 ? OC : a.O;
+        const int act1 = A1 >= 0 ? A1 : a.act1;
+        const int act2 = A2 >= 0 ? A2 : a.act2;
+        const int loss = LS >= 0 ? LS : a.loss;
+        float w2[NH][OC], b1[NH], corr[NH], dprev[NH], pln[NH];
+        const int ol = lane & 15;
+        const int own = OC == 10 ? own10(ol) : ol;  // output whose total this lane holds
+        const bool owner = own >= 0 && own < O;
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) Pl[(mt * 16 + 4 * g + r) * HW + nt * 16 + r16] -= lr * acc[r];
+        for (int j = 0; j < NH; ++j) {
+            const int h = lane + 64 * j;
+            b1[j] = h < H ? th[a.off_b1 + h] : 0.f;
+#pragma unroll
+            for (int o = 0; o < OC; ++o) w2[j][o] = (h < H && o < O) ? th[a.off_w2 + (size_t)o * H + h] : 0.f;
+            corr[j] = 0.f;
+            dprev[j] = 0.f;
+            pln[j] = Pl[h * TS];
+        }
+        float b2v = owner ? th[a.off_b2 + own] : 0.f;
+        int label = yb[0];  // label of the current row; the next row's is read a step ahead
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+
+        for (int r = 0; r < nsteps; ++r) {
+            const int c = r >> 6, t = r & (T - 1);
+            const int tc = chunk_len(c);
+            // the row after this step: same chunk, or the next chunk's first row
+            const bool more = r + 1 < nsteps;
+            const bool cross = more && t + 1 == tc;
+            if (more && ((r + 1) % BS) == 0) {
+                // the next row opens block Bn: its input sums must hold every block up to
+                // Bn - 2 (next chunk: its data loaded and blocks 0..NB-2 of this one), and
+                // the hist columns it will overwrite must have been copied out (block Bn - NB)
+                const int Bn = (r + 1) / BS;
+                if (cross) {
+                    lds_wait_geq(nready, c + 2, lab, gabort, a.spin_limit, false);
+                    lds_wait_geq(fnext, NB * c + NB - 1, lab, gabort, a.spin_limit, false);
+                    lds_wait_geq(fnext + 1, NB * c + NB - 1, lab, gabort, a.spin_limit, false);
+                } else {
+                    lds_wait_geq(fcur, Bn - 1, lab, gabort, a.spin_limit, false);
+                    lds_wait_geq(fcur + 1, Bn - 1, lab, gabort, a.spin_limit, false);
                 }
-                __syncthreads();
-                pl_next = live ? Pl[t * HW + h] : 0.f;
+                lds_wait_geq(pubd, Bn - NB + 1, lab, gabort, a.spin_limit, false);
             }
-            float a1 = 0.f;
-            if (live) {
-                const float z1 = pl_next + b1 - lr * corr;
-                pl_next = (t + 1 < tc) ? Pl[(t + 1) * HW + h] : 0.f;  // prefetch the next step's input sum
-                a1 = hv ? act_fast(act1, z1) : 0.f;
+            // operands of the step's end, read up front (unconditional loads from valid
+            // addresses, so every path leaves the same LDS reads in flight)
+            const int rn = more ? r + 1 : r;
+            const int cn = rn >> 6, tn = rn & (T - 1);
+            float cp[NH], pnx[NH];
+#pragma unroll
+            for (int j = 0; j < NH; ++j) pnx[j] = Pl[(cn & 1) * HW * TS + (lane + 64 * j) * TS + tn];
+            // Gram entries of the next row against steps r and r-1: within the next row's
+            // chunk from its G block, against the chunk before it from GX (which holds the
+            // next row's chunk against the previous one whenever the next row needs it)
+            const float* gin = grow_in(cn) + tn * GS;
+            const float* gx = GX + tn * GS;
+            const float g1v = cross ? gx[t] : gin[t];
+            const int tp = t > 0 ? t - 1 : T - 1;      // position of step r-1 in its chunk
+            const float g0v = (cross || t == 0) ? gx[tp] : gin[tp];
+            const int labn = yb[(cn & 1) * T + tn];
+
+            float a1[NH], na[NH];
+#pragma unroll
+            for (int j = 0; j < NH; ++j) {
+                const float z1 = pln[j] + b1[j] - lr * corr[j];
+                a1[j] = (lane + 64 * j < H) ? act_fast(act1, z1) : 0.f;
+                na[j] = -lr * a1[j];
+            }
+            float z2;
+            if constexpr (OC == 10) {
+                float p[10];
+#pragma unroll
+                for (int o = 0; o < 10; ++o) {
+                    p[o] = w2[0][o] * a1[0];
+#pragma unroll
+                    for (int j = 1; j < NH; ++j) p[o] = __builtin_fmaf(w2[j][o], a1[j], p[o]);
+                }
+                z2 = reduce10(p, lane) + b2v;
+            } else {
                 float p[16];
 #pragma unroll
-                for (int o = 0; o < 16; ++o) p[o] = o < OC ? w2[o < OC ? o : 0] * a1 : 0.f;
-                const float v = row_reduce_scatter16(p, lane);
-                red[(t & 1) * 256 + ol * 16 + wave * 4 + (lane >> 4)] = v;
+                for (int o = 0; o < 16; ++o) {
+                    p[o] = w2[0][o] * a1[0];
+#pragma unroll
+                    for (int j = 1; j < NH; ++j) p[o] = __builtin_fmaf(w2[j][o], a1[j], p[o]);
+                }
+                z2 = reduce16(p, lane) + b2v;
+            }
+            // the window correction of the next row (wave 1 has normally finished it)
+            const int cd = __hip_atomic_load(cdone, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 1) * HW + lane + 64 * j];
+            float x2;
+            if (act2 == ACT_SOFTMAX) {
+                const float m = row_allmax16(owner ? z2 : -INFINITY);
+                const float e = owner ? __expf(z2 - m) : 0.f;
+                x2 = e * __builtin_amdgcn_rcpf(row_allsum16(e));
             } else {
-                if (part == 0 && hv) {
-                    // in-block part of the next step's correction, sum over s in [bs1, t-2]
-                    // of d1_s G[t+1][s] (at most 14 terms: four masked float4 groups)
-                    const int t1 = t + 1, bs1 = t1 & ~15;
-                    float sum = 0.f;
-                    if (t1 < tc && t - 2 >= bs1) {
-                        const float* g = Gl + t1 * GS + bs1;
-                        const float* hr = hist + h * TS + bs1;
-                        const int last = t - 2 - bs1;  // highest offset included
-                        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                x2 = act_fast(act2, z2);
+            }
+            const float e = (own == label) ? 1.0f : 0.0f;
+            const float dv = (loss == LOSS_XENT) ? (x2 - e) : (x2 - e) * act_deriv(act2, x2);
+            const float d2 = owner ? dv : 0.f;
+            b2v -= lr * d2;
+            float back[NH];
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            if (4 * q <= last) {
-                                const float4 hv4 = *(const float4*)(hr + 4 * q), gv4 = *(const float4*)(g + 4 * q);
-                                acc.x += hv4.x * gv4.x;
-                                acc.y += (4 * q + 1 <= last) ? hv4.y * gv4.y : 0.f;
-                                acc.z += (4 * q + 2 <= last) ? hv4.z * gv4.z : 0.f;
-                                acc.w += (4 * q + 3 <= last) ? hv4.w * gv4.w : 0.f;
-                            }
-                        }
-                        sum = (acc.x + acc.y) + (acc.z + acc.w);
-                    }
-                    cpre[((t + 1) & 1) * HW + h] = sum;
+            for (int j = 0; j < NH; ++j) back[j] = 0.f;
+            backprop_outputs<OC, NH, 0>(back, w2, d2, na);
+            float d1[NH];
+#pragma unroll
+            for (int j = 0; j < NH; ++j) {
+                d1[j] = (lane + 64 * j < H) ? back[j] * act_deriv(act1, a1[j]) : 0.f;
+                b1[j] -= lr * d1[j];
+                hist[(lane + 64 * j) * TS + t] = d1[j];
+            }
+            if (more) {
+                if (__builtin_amdgcn_readfirstlane(cd) < r + 2) {
+                    lds_wait_geq(cdone, r + 2, lab, gabort, a.spin_limit, false);
+#pragma unroll
+                    for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 1) * HW + lane + 64 * j];
                 }
-                // prefetch of the next chunk: the flag value read last step decides
-                if (has_next && !issued) {
-                    if (__builtin_amdgcn_readfirstlane(qseen) >= a.nrb * (c + 2)) {
+                // terms of steps r and r-1 (r-1 only if it lies in the window of the next
+                // row's block pair, which always holds: it is at most two steps back)
+                const bool has0 = r >= 1;
+                const float g1 = g1v, g0 = has0 ? g0v : 0.f;
+#pragma unroll
+                for (int j = 0; j < NH; ++j) {
+                    corr[j] = cp[j] + dprev[j] * g0 + d1[j] * g1;
+                    dprev[j] = d1[j];
+                    pln[j] = pnx[j];
+                }
+                label = labn;
+            }
+            // d1 of this step is in hist, and this step's reads of the correction slot are
+            // done: wave 1 may refill it
+            lds_publish(d1done, r + 1);
+        }
+#pragma unroll
+        for (int j = 0; j < NH; ++j) {
+            const int h = lane + 64 * j;
+            if (h < H) {
+                th[a.off_b1 + h] = b1[j];
+#pragma unroll
+                for (int o = 0; o < OC; ++o)
+                    if (o < O) th[a.off_w2 + (size_t)o * H + h] = w2[j][o];
+            }
+        }
+        if (lane < 16 && owner) th[a.off_b2 + own] = b2v;
+    } else if (wave == 1) {
+        // ================= window corrections: for row q = r + 1 (block B = q / BS),
+        // cpre[q] = sum over s in [BS(B-1), q-3] of d1_s (x_s . x_q)
+        for (int r = 0; r + 1 < nsteps; ++r) {
+            const int q = r + 1;
+            const int cq = q >> 6, tq = q & (T - 1), B = q / BS;
+            // the live wave has finished step r-2: d1 up to q-3 is in hist and the slot
+            // (q & 1) (last holding the correction of row q-2) is free
+            lds_wait_geq(d1done, r - 1, lab, gabort, a.spin_limit, true);
+            // a chunk's first rows read its Gram blocks (and GX) before the live wave enters it
+            if (tq < BS && cq >= 1) lds_wait_geq(nready, cq + 1, lab, gabort, a.spin_limit, true);
+            float sum[NH];
+#pragma unroll
+            for (int j = 0; j < NH; ++j) sum[j] = 0.f;
+            const int lo = max(0, BS * (B - 1)), hi = q - 3;  // inclusive range
+            // two aligned groups of BS steps: the previous block and the row's own block
+#pragma unroll
+            for (int part = 0; part < 2; ++part) {
+                const int sb = BS * (B - 1 + part);  // first step of the group
+                if (sb < lo || sb > hi) continue;
+                const int cs = sb >> 6, ts = sb & (T - 1);
+                // Gram row of q against the group's steps: same chunk -> G_cq, else GX_cq
+                const float* gq = (cs == cq ? grow_in(cq) : GX) + tq * GS + ts;
+                const int last = hi - sb;  // highest offset included (>= 0)
+#pragma unroll
+                for (int u = 0; u < BS / 4; ++u) {
+                    if (4 * u > last) break;
+                    float4 gv = *(const float4*)(gq + 4 * u);
+                    gv.y = (4 * u + 1 <= last) ? gv.y : 0.f;
+                    gv.z = (4 * u + 2 <= last) ? gv.z : 0.f;
+                    gv.w = (4 * u + 3 <= last) ? gv.w : 0.f;
+#pragma unroll
+                    for (int j = 0; j < NH; ++j) {
+                        const float4 hv = *(const float4*)(hist + (lane + 64 * j) * TS + ts + 4 * u);
+                        sum[j] = __builtin_fmaf(hv.x, gv.x, sum[j]);
+                        sum[j] = __builtin_fmaf(hv.y, gv.y, sum[j]);
+                        sum[j] = __builtin_fmaf(hv.z, gv.z, sum[j]);
+                        sum[j] = __builtin_fmaf(hv.w, gv.w, sum[j]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < NH; ++j) cpre[(q & 1) * HW + lane + 64 * j] = sum[j];
+            lds_publish(cdone, q + 1);
+        }
+    } else {
+        // ================= waves 2 and 3: the folds, each wave for half of the neuron tiles;
+        // wave 3 also publishes the finished blocks' d1 and loads the next chunk's data
+        constexpr int NNT = HW / 16;
+        const int w2i = wave - 2;
+        const bool io = wave == 3;
+        const int nt0 = w2i * (NNT / 2);
+        int* fc = fcur + w2i;
+        int* fn = fnext + w2i;
+        int cur = 0;     // next block whose fold into the rows that need it is pending
+        int nxt = 0;     // next block whose fold into the next chunk's rows is pending
+        int pub = 0;     // (wave 3) next block to publish
+        int loaded = 1;  // (wave 3) chunks whose data is in LDS
+        int polls = 0;
+        long idle = 0;
+        while (cur < nblk || nxt < nblk || (io && (pub < nblk || loaded < nchk))) {
+            bool progress = false;
+            const int dd = lds_read(d1done);
+            if (io && pub < nblk && dd >= min(BS * (pub + 1), nsteps)) {
+                // ---- publish block `pub` for the tile workgroups
+                const int c = pub / NB, b = pub % NB, tc = chunk_len(c);
+                float* dout = a.d1 + ((size_t)(c & 1) * K + k) * T * H;  // [h][T] errors of chunk c
+                const int s0 = BS * b;
+                for (int q = lane; q < H * (BS / 4); q += 64) {
+                    const int hh = q / (BS / 4), s4 = s0 + (q % (BS / 4)) * 4;
+                    *(float4*)(dout + (size_t)hh * T + s4) = *(const float4*)(hist + hh * TS + s4);
+                }
+                ++pub;
+                lds_publish(pubd, pub);  // (the hist reads completed: the stores consumed them)
+                if (BS * (b + 1) >= tc) {
+                    // every error of chunk c is stored: announce it to the tiles
+                    wait_vm_all();
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                    if (lane == 0) __hip_atomic_store(dready, c + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+                progress = true;
+            } else if (cur < nblk && dd >= min(BS * (cur + 1), nsteps)) {
+                // ---- block `cur` into the later rows of its chunk
+                const int c = cur / NB, b = cur % NB, tc = chunk_len(c);
+                if (BS * (b + 2) < tc) {
+                    fold_block<GS, TS, BS, T / 16, NNT / 2>(Pl + (c & 1) * HW * TS, grow_in(c), hist, BS * (b + 2), tc,
+                                                            BS * b, lr, nt0, lane);
+                } else if (b == NB - 1 && c + 1 < nchk) {
+                    // last block of a chunk: rows [BS, T) of the next chunk (its first block
+                    // takes it through the window); the live wave has waited for that chunk
+                    lds_wait_geq(nready, c + 2, lab, gabort, a.spin_limit, true);
+                    const int tn = chunk_len(c + 1);
+                    if (tn > BS)
+                        fold_block<GS, TS, BS, T / 16, NNT / 2>(Pl + ((c + 1) & 1) * HW * TS, GX, hist, BS, tn,
+                                                                T - BS, lr, nt0, lane);
+                }
+                ++cur;
+                lds_publish(fc, cur);
+                progress = true;
+            } else if (io && loaded < nchk) {
+                // ---- load chunk `loaded` into the buffers of parity loaded & 1 once (i) the
+                // tiles have published its Q and (ii) the current chunk no longer needs its
+                // cross Gram block: the first block's window corrections are done, and the
+                // previous chunk's last block is folded into it (by both waves)
+                const int c = loaded - 1;  // chunk the live wave is in (or before)
+                const bool gx_free = (c == 0) || (lds_read(cdone) >= min(T * c + BS + 1, nsteps) &&
+                                                  lds_read(fcur) >= NB * c && lds_read(fcur + 1) >= NB * c);
+                if (gx_free && (++polls & 7) == 0) {
+                    const int q = __builtin_amdgcn_readfirstlane(
+                        __hip_atomic_load(qready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                    if (q >= a.nrb * (loaded + 1)) {
                         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                        issue_next();
-                        issued = true;
-                    } else {
-                        qseen = __hip_atomic_load(qready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    }
-                }
-                // the previous chunk's errors (stored at the chunk start) are announced once
-                // every helper wave's stores have completed
-                if (c > 0 && t == sig_step) wait_vm_all();
-            }
-            __syncthreads();
-            if (c > 0 && t == sig_step && tid == HW) {
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-                __hip_atomic_store(dready, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            if (live) {
-                // every operand of this phase is read up front
-                const float4* rr = (const float4*)(red + (t & 1) * 256 + ol * 16);
-                const float4 r0 = rr[0];
-                const float4 r1 = nlive > 1 ? rr[1] : make_float4(0.f, 0.f, 0.f, 0.f);
-                const int label = ylds[t];
-                float cp = 0.f, g0 = 0.f, g1 = 0.f;
-                const int bs1 = (t + 1) & ~15;
-                if (t + 1 < tc) {
-                    cp = cpre[((t + 1) & 1) * HW + h];
-                    const float* g = Gl + (t + 1) * GS;
-                    g1 = t >= bs1 ? g[t] : 0.f;
-                    g0 = t - 1 >= bs1 ? g[t - 1] : 0.f;
-                }
-                const float z2 = b2v + ((r0.x + r0.y) + (r0.z + r0.w)) + ((r1.x + r1.y) + (r1.z + r1.w));
-                float x2;
-                if (act2 == ACT_SOFTMAX) {
-                    const float m = row_allmax16(ol < O ? z2 : -INFINITY);
-                    const float e = ol < O ? __expf(z2 - m) : 0.f;
-                    x2 = e * __builtin_amdgcn_rcpf(row_allsum16(e));
-                } else {
-                    x2 = act_fast(act2, z2);
-                }
-                const float e = (ol == label) ? 1.0f : 0.0f;
-                float d2 = (loss == LOSS_XENT) ? (x2 - e) : (x2 - e) * act_deriv(act2, x2);
-                d2 = ol < O ? d2 : 0.f;
-                b2v -= lr * d2;
-                float bk[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int o = 0; o < OC; ++o) {
-                    const float d2o = readlane_f(d2, o);
-                    bk[o & 3] += w2[o] * d2o;
-                    w2[o] -= (lr * d2o) * a1;
-                }
-                const float back = (bk[0] + bk[1]) + (bk[2] + bk[3]);
-                const float d1 = hv ? back * act_deriv(act1, a1) : 0.f;
-                b1 -= lr * d1;
-                hist[h * TS + t] = d1;
-                corr = cp + dprev * g0 + d1 * g1;
-                dprev = d1;
-            }
-        }
-
-        float* dout = a.d1 + ((size_t)(c & 1) * K + k) * T * H;
-        if (has_next) {
-            // chunk boundary: make sure the next chunk's inputs are in LDS
-            if (!live) {
-                if (!issued) {
-                    if (wave_wait_geq(qready, a.nrb * (c + 2), abort, a.spin_limit)) issue_next();
-                }
-                wait_vm_all();
-                issued = false;
-                qseen = 0;
-            }
-            __syncthreads();
-            // previous-chunk correction on the matrix cores, written with the prefetched Q:
-            // Pl[t][h] = Q[t][h] - eta * sum_s GX[t][s] d1_s[h]; two output tiles per pass so
-            // that two independent accumulation chains share the matrix core
-            {
-                constexpr int ntiles = (T / 16) * (HW / 16);
-                const int r16 = lane & 15, g = lane >> 4;
-                for (int ti = wave; ti < ntiles; ti += 8) {
-                    const int tj = ti + 4;
-                    const bool two = tj < ntiles;
-                    const int mt0 = ti % (T / 16), nt0 = ti / (T / 16);
-                    const int mt1 = tj % (T / 16), nt1 = (two ? tj : ti) / (T / 16);
-                    f4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-                    float4 av0[T / 16], bv0[T / 16], av1[T / 16], bv1[T / 16];
-#pragma unroll
-                    for (int sl = 0; sl < T / 16; ++sl) {
-                        av0[sl] = *(const float4*)(GXn + (mt0 * 16 + r16) * GS + sl * 16 + 4 * g);
-                        bv0[sl] = *(const float4*)(hist + (nt0 * 16 + r16) * TS + sl * 16 + 4 * g);
-                        av1[sl] = *(const float4*)(GXn + ((two ? mt1 : mt0) * 16 + r16) * GS + sl * 16 + 4 * g);
-                        bv1[sl] = *(const float4*)(hist + (nt1 * 16 + r16) * TS + sl * 16 + 4 * g);
-                    }
-#pragma unroll
-                    for (int sl = 0; sl < T / 16; ++sl) {
-                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].x, bv0[sl].x, acc0, 0, 0, 0);
-                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].x, bv1[sl].x, acc1, 0, 0, 0);
-                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].y, bv0[sl].y, acc0, 0, 0, 0);
-                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].y, bv1[sl].y, acc1, 0, 0, 0);
-                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].z, bv0[sl].z, acc0, 0, 0, 0);
-                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].z, bv1[sl].z, acc1, 0, 0, 0);
-                        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av0[sl].w, bv0[sl].w, acc0, 0, 0, 0);
-                        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av1[sl].w, bv1[sl].w, acc1, 0, 0, 0);
-                    }
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int t0 = mt0 * 16 + 4 * g + r, h0 = nt0 * 16 + r16;
-                        Pl[t0 * HW + h0] = (h0 < H && t0 < tcn ? Qn[t0 * H + h0] : 0.f) - lr * acc0[r];
-                        if (two) {
-                            const int t1 = mt1 * 16 + 4 * g + r, h1 = nt1 * 16 + r16;
-                            Pl[t1 * HW + h1] = (h1 < H && t1 < tcn ? Qn[t1 * H + h1] : 0.f) - lr * acc1[r];
+                        const int cn = loaded, tcn = chunk_len(cn);
+                        const float* Q = a.qbuf + ((size_t)(cn & 1) * K + k) * HW * TS;
+                        const float* G = a.gram + ((size_t)k * a.nch + cn) * T * GS;
+                        const float* GXg = a.gramx + ((size_t)k * (a.nch - 1) + cn - 1) * T * GS;
+                        wave_copy_to_lds(Q, Pl + (cn & 1) * HW * TS, HW * TS * 4, 0, 1, lane);
+                        wave_copy_to_lds(G, Gin + (cn & 1) * T * GS, T * GS * 4, 0, 1, lane);
+                        wave_copy_to_lds(GXg, GX, T * GS * 4, 0, 1, lane);
+                        {
+                            const int rr = min(lane, tcn - 1);
+                            __builtin_amdgcn_global_load_lds(a.y + xs + (int64_t)cn * T + rr,
+                                                             (lds_void*)(yb + (cn & 1) * T), 4, 0, 0);
                         }
+                        wait_vm_all();
+                        ++loaded;
+                        lds_publish(nready, loaded);
+                        progress = true;
                     }
                 }
             }
-            // the helpers store this chunk's errors for the tiles (announced a few steps into
-            // the next chunk, once the stores have completed)
-            if (!live) {
-                // errors published as [h][T] rows, the layout of the LDS history
-                constexpr int NH = 256 - HW;
-                for (int q = tid - HW; q < H * (T / 4); q += NH) {
-                    const int hh = q / (T / 4), t4 = (q % (T / 4)) * 4;
-                    *(float4*)(dout + (size_t)hh * T + t4) = *(const float4*)(hist + hh * TS + t4);
+            if (!progress && nxt < cur) {
+                // ---- block `nxt` into every row of the next chunk, once that chunk is loaded
+                const int c = nxt / NB, b = nxt % NB;
+                if (b == NB - 1 || c + 1 >= nchk) {
+                    ++nxt;  // nothing of this block goes into the next chunk here
+                    lds_publish(fn, nxt);
+                    progress = true;
+                } else if (lds_read(nready) >= c + 2) {
+                    fold_block<GS, TS, BS, T / 16, NNT / 2>(Pl + ((c + 1) & 1) * HW * TS, GX, hist, 0,
+                                                            chunk_len(c + 1), BS * b, lr, nt0, lane);
+                    ++nxt;
+                    lds_publish(fn, nxt);
+                    progress = true;
                 }
             }
-            __syncthreads();
-        } else {
-            // last chunk: publish synchronously
-            __syncthreads();
-            for (int q = tid; q < H * (T / 4); q += 256) {
-                const int hh = q / (T / 4), t4 = (q % (T / 4)) * 4;
-                *(float4*)(dout + (size_t)hh * T + t4) = *(const float4*)(hist + hh * TS + t4);
+            if (!progress) {
+                if (lds_read(lab)) break;
+                if (++idle > a.spin_limit) {
+                    lds_publish(lab, 1);
+                    __hip_atomic_store(gabort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            } else {
+                idle = 0;
             }
-            signal_set(dready, c + 1);
         }
     }
-    if (live && hv) {
-        th[a.off_b1 + h] = b1;
-#pragma unroll
-        for (int o = 0; o < OC; ++o)
-            if (o < O) th[a.off_w2 + (size_t)o * H + h] = w2[o];
-    }
-    if (tid < O) th[a.off_b2 + tid] = b2v;
 }
 
 template <int T>
@@ -1231,14 +1613,14 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
             *(f4*)(red4 + ((size_t)(wave * NMT + mt) * 64 + lane) * 4) = acc;
         }
         __syncthreads();
-        float* Q = a.qbuf + ((size_t)(c & 1) * K + k) * T * H;
+        float* Q = a.qbuf + ((size_t)(c & 1) * K + k) * a.qslot;
         for (int e = tid; e < NMT * 256; e += 256) {
             const int mt = e >> 8, rem = e & 255, ln = rem >> 2, r = rem & 3;
             float sum = 0.f;
 #pragma unroll
             for (int w = 0; w < 4; ++w) sum += red4[((size_t)(w * NMT + mt) * 64 + ln) * 4 + r];
             const int t = mt * 16 + 4 * (ln >> 4) + r, hh = rb * 16 + (ln & 15);
-            if (t < tc && hh < H) Q[(size_t)t * H + hh] = sum;
+            if (t < tc && hh < H) Q[(size_t)hh * a.qstride + t] = sum;
         }
         signal_add(qready, 1);
     };
@@ -1305,11 +1687,11 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
         }
 }
 
-template <int T, int HW, int A1, int A2, int LS, int OC>
+template <int T, int NH, int A1, int A2, int LS, int OC>
 __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
     extern __shared__ float smem[];
     const int b = blockIdx.x, K = a.k_rep;
-    if (b < K) psgd_rec<T, HW, A1, A2, LS, OC>(a, b, smem);
+    if (b < K) psgd_rec<T, NH, A1, A2, LS, OC>(a, b, smem);
     else {
         const int j = b - K;
         psgd_tile<T>(a, j / a.nrb, j % a.nrb, smem);

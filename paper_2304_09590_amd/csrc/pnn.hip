@@ -374,15 +374,19 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
 constexpr int PT = 64;            // chunk length of the persistent per-sample plan
 constexpr long SPIN_LIMIT = 1L << 22;
 
-// kernel instance: hidden width class (64 / 128 live threads) x activation specialisation
+// kernel instance: hidden neurons per lane of the live wave (1: <= 64, 2: <= 128) x
+// activation specialisation
 const void* persistent_fn(const pnn_net* n) {
     const bool narrow = n->sizes[1] <= 64;
     if (n->pspecial)
-        return narrow ? (const void*)psgd_persistent_kernel<PT, 64, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>
-                      : (const void*)psgd_persistent_kernel<PT, 128, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>;
-    return narrow ? (const void*)psgd_persistent_kernel<PT, 64, -1, -1, -1, 16>
-                  : (const void*)psgd_persistent_kernel<PT, 128, -1, -1, -1, 16>;
+        return narrow ? (const void*)psgd_persistent_kernel<PT, 1, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>
+                      : (const void*)psgd_persistent_kernel<PT, 2, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>;
+    return narrow ? (const void*)psgd_persistent_kernel<PT, 1, -1, -1, -1, 16>
+                  : (const void*)psgd_persistent_kernel<PT, 2, -1, -1, -1, 16>;
 }
+
+// width of the live wave's neuron set (input-sum rows are padded to it)
+int live_width(int H) { return H <= 64 ? 64 : 128; }
 
 pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
     const int K = n->cfg.replicas, H = n->sizes[1], In = n->sizes[0];
@@ -429,7 +433,8 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
     a.off_w1 = n->off_w[0]; a.off_b1 = n->off_b[0]; a.off_w2 = n->off_w[1]; a.off_b2 = n->off_b[1];
     a.X = X; a.y = Y; a.n_total = N; a.k_rep = K;
     a.gram = n->gram; a.gramx = n->gramx; a.nch = nch;
-    a.qbuf = n->qbuf; a.d1 = n->d1; a.flags = n->flags;
+    a.qbuf = n->qbuf; a.qstride = PT + 4; a.qslot = (int64_t)live_width(H) * (PT + 4);
+    a.d1 = n->d1; a.flags = n->flags;
     a.H = H; a.O = n->sizes[2]; a.In = In; a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
     a.nrb = n->nrb;
     a.lr = n->cfg.lr;
@@ -647,9 +652,11 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, n->device) != hipSuccess) cus = 0;
         const int H = n->sizes[1], In = n->sizes[0], O = n->sizes[2];
         const int nrb = (H + 15) / 16;
-        const int HW = (H + 63) & ~63;
+        const int HW = live_width(H);
+        // input sums [2][HW][T+4], errors [HW][T+4], Gram blocks 3 x [T][T+4], window
+        // corrections [2][HW], labels [2][T], 12 counters
         const size_t rec_smem =
-            (size_t)(2 * PT * HW + HW * (PT + 4) + 3 * PT * (PT + 4) + 512 + 2 * HW + 2 * PT) * sizeof(float);
+            (size_t)(3 * HW * (PT + 4) + 3 * PT * (PT + 4) + 2 * HW + 2 * PT + 12) * sizeof(float);
         const size_t tile_smem = (size_t)4 * (PT / 16) * 64 * 4 * sizeof(float);
         n->psmem = std::max(rec_smem, tile_smem);
         n->pspecial = n->act[0] == PNN_SIGMOID && n->act[1] == PNN_SIGMOID && cfg->loss == PNN_LOSS_MSE && O == 10;
@@ -664,7 +671,11 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         if (fits) {
             n->persistent = true;
             n->nrb = nrb;
-            if ((st = dev_alloc(n, &n->qbuf, (size_t)2 * K * PT * H)) != PNN_OK) return bail(st);
+            const size_t qn = (size_t)2 * K * HW * (PT + 4);
+            if ((st = dev_alloc(n, &n->qbuf, qn)) != PNN_OK) return bail(st);
+            // padding neurons and rows of the input sums are never written by the kernel: zero them
+            if (hipMemset(n->qbuf, 0, sizeof(float) * qn) != hipSuccess)
+                return bail(fail(n, PNN_EHIP, "hipMemset of the input-sum buffer failed"));
             if ((st = dev_alloc(n, &n->d1, (size_t)2 * K * PT * H)) != PNN_OK) return bail(st);
             if ((st = dev_alloc(n, &n->flags, (size_t)(2 * K + 1))) != PNN_OK) return bail(st);
         }
