@@ -48,8 +48,11 @@ def method_flops_per_sample(w) -> float:
 def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
     """Algorithmic work of one launch of a library kernel: (bound, flops, bytes).
 
-    psgd_persistent: one launch trains every CN for one epoch (per-sample SGD) -> N samples
-      x the method's FLOPs per sample (the first-layer products run on the matrix cores).
+    psgd_persistent: one launch trains every CN for one epoch (per-sample SGD).  Priced in
+      effective HBM bytes: a step of plain per-sample SGD reads and writes every parameter
+      once and reads its input row, 8 P + 4 n_in bytes, times the N steps of the launch.
+      (The kernel keeps the parameters on chip, so its real traffic is far lower: this is
+      the rate at which an HBM-streaming implementation would have to run to match it.)
     fwd_gemm / upd_gemm / bwd_gemm (mini-batch plan): totals over the profiled step of
       2 * rows * out * in for the layers these kernels handle (output layers of <= 16
       neurons use the row kernels), divided by the launches.
@@ -59,7 +62,7 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
     K = w.replicas
     L = len(s) - 1
     if name == "psgd_persistent":
-        return "mfma", N * method_flops_per_sample(w), N * s[0] * 4.0 + 2 * K * w.param_count() * 4.0
+        return "hbm", N * method_flops_per_sample(w), N * (8.0 * w.param_count() + 4.0 * s[0])
     rows = N * epochs_profiled
     if name == "fwd_gemm":
         f = sum(2.0 * rows * s[l + 1] * s[l] for l in range(L) if s[l + 1] > 16)
@@ -73,6 +76,39 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
     if name == "merge":
         P = w.param_count()
         return "hbm", 0.0, (K * P + P + (K * P if w.merge_every_epoch else 0)) * 4.0
+    return None
+
+
+def source_digest() -> str:
+    """sha256 over the library sources (csrc/*.hip, csrc/*.hpp, include/*.h), in name order."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2304_09590_amd", "csrc", "*.hip")) +
+                   glob.glob(os.path.join(ROOT, "paper_2304_09590_amd", "csrc", "*.hpp")) +
+                   glob.glob(os.path.join(ROOT, "include", "*.h")))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the rocprofv3 counter summaries under
+    profiles/ (lines `traffic: kernel=K workload=W source=SHA bytes_per_launch=B`), or None
+    when no summary was taken from the current sources."""
+    import glob
+    src = source_digest()
+    for f in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(f) as fh:
+            for line in fh:
+                line = line.strip().strip("`")
+                if not line.startswith("traffic:"):
+                    continue
+                kv = dict(t.split("=", 1) for t in line[len("traffic:"):].split() if "=" in t)
+                if kv.get("kernel") == kernel and kv.get("workload") == workload and kv.get("source") == src:
+                    return float(kv["bytes_per_launch"])
     return None
 
 
@@ -175,8 +211,10 @@ def main():
             else:
                 peak = BF16_PEAK_TFLOPS if w.precision == I.BF16_MIXED and bound == "mfma" else FP32_PEAK_TFLOPS
                 ach, unit = flops / avg_s / 1e12, "TFLOP/s"
+            traffic = measured_traffic(dom, w.name)
             roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 4), "peak": peak, "unit": unit,
-                        "frac": round(ach / peak, 6), "traffic": None, "avg_us": round(avg_s * 1e6, 3)}
+                        "frac": round(ach / peak, 6), "traffic": traffic, "avg_us": round(avg_s * 1e6, 3),
+                        "work_per_launch": byts if bound == "hbm" else flops}
 
     cpu = None
     if not args.no_cpu_baseline:
