@@ -800,6 +800,20 @@ __device__ inline bool wait_geq(int* flag, int target, int* abort, long limit) {
 
 // The workgroup barrier makes every wave's stores complete; thread 0's release fence then
 // publishes them before the flag update.
+// Bounded wait of a single wave on a global counter, then an acquire fence.
+__device__ inline bool wait_geq_wave(int* flag, int target, int* abort, long limit) {
+    long it = 0;
+    while (__builtin_amdgcn_readfirstlane(__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) < target) {
+        if (__hip_atomic_load(abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+        if (++it > limit) {
+            __hip_atomic_store(abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return true;
+}
 __device__ inline void signal_add(int* flag, int v) {
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -1057,76 +1071,59 @@ __device__ inline void backprop_outputs(float (&back)[NH], float (&w2)[NH][OC], 
 }
 
 // ------------------------------------------------------------------------------------
-// Fold of one finished block of BS steps into stored input sums, on the matrix cores:
-//   PlT[h][t] -= eta * sum_{s in block} G[t][s] * D[h][s]      for rows t in [r0, r1)
-// (r0 a multiple of 8, at most MT tiles of 16 rows) and the NT neuron tiles starting at
-// nt0 (16 neurons each).  G rows have stride GS; D and PlT rows (one per neuron) have
-// stride TS.  v_mfma_f32_16x16x4_f32 contracts 4 steps per instruction; lane group
-// g = lane / 16 supplies the steps s0 + (BS/4) g + q of instruction q (the same permutation
-// of the steps on both operands).  A lane's accumulator holds rows 4g .. 4g+3 of one
-// neuron, contiguous in PlT: one 16-byte read-modify-write per tile.  All operand reads are
-// issued first, then the MT x NT independent accumulation chains, then the read-modify-
-// writes, so the latencies overlap.  Rows of a partial group at or past r1 are unused rows
-// of the buffer.
-template <int GS, int TS, int BS, int MT, int NT>
-__device__ __attribute__((always_inline)) inline void fold_tiles(float* PlT, const float* G, const float* D, int r0, int r1, int s0, float lr,
-                                  int nt0, int lane) {
-    constexpr int NQ = BS / 4;  // instructions per tile
-    static_assert(BS == 8 || BS == 16, "block of 8 or 16 steps");
-    typedef float vq __attribute__((ext_vector_type(NQ)));
+// Fold of one finished block of BS = 8 steps into a chunk's input-sum accumulator held in
+// registers, on the matrix cores:
+//   acc[t][h] += sum_{s in block} G[t][s] * D[h][s]
+// for the row tiles mt >= mt0 (16 rows each) and the NT neuron tiles starting at nt0 (16
+// neurons each).  G rows have stride GS; D rows (one per neuron) have stride TS.
+// v_mfma_f32_16x16x4_f32 contracts 4 steps per instruction; lane group g = lane / 16
+// supplies the steps s0 + 2g + q of instruction q (the same permutation of the steps on both
+// operands).  A lane's accumulator acc[mt][nt] holds rows mt*16 + 4g .. +3 of neuron
+// (nt0 + nt)*16 + lane % 16.  Rows of tile mt0 before the first row that needs the block
+// also receive it; they are final already and never written again.
+template <int GS, int TS, int MT, int NT>
+__device__ __attribute__((always_inline)) inline void fold_acc(f4 (&acc)[MT][NT], const float* G, const float* D,
+                                                               int mt0, int s0, int nt0, int lane) {
+    typedef float v2 __attribute__((ext_vector_type(2)));
     const int r16 = lane & 15, g = lane >> 4;
-    vq av[MT], bv[NT];
+    v2 av[MT], bv[NT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int row = min(r0 + mt * 16 + r16, r1 - 1);  // rows past r1 feed discarded outputs
-        av[mt] = *(const vq*)(G + row * GS + s0 + NQ * g);
-    }
+    for (int mt = 0; mt < MT; ++mt) av[mt] = *(const v2*)(G + (mt * 16 + r16) * GS + s0 + 2 * g);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) bv[nt] = *(const vq*)(D + ((nt0 + nt) * 16 + r16) * TS + s0 + NQ * g);
-    f4 acc[MT][NT];
+    for (int nt = 0; nt < NT; ++nt) bv[nt] = *(const v2*)(D + ((nt0 + nt) * 16 + r16) * TS + s0 + 2 * g);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
+        if (mt >= mt0)  // wave-uniform
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt][0], bv[nt][0], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-#pragma unroll
-    for (int q = 1; q < NQ; ++q)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt][q], bv[nt][q], acc[mt][nt], 0, 0, 0);
-    float4 v[MT][NT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-            if (r0 + mt * 16 + 4 * g < r1)
-                v[mt][nt] = *(const float4*)(PlT + ((nt0 + nt) * 16 + r16) * TS + r0 + mt * 16 + 4 * g);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-            if (r0 + mt * 16 + 4 * g < r1) {
-                float4 w = v[mt][nt];
-                w.x -= lr * acc[mt][nt][0]; w.y -= lr * acc[mt][nt][1];
-                w.z -= lr * acc[mt][nt][2]; w.w -= lr * acc[mt][nt][3];
-                *(float4*)(PlT + ((nt0 + nt) * 16 + r16) * TS + r0 + mt * 16 + 4 * g) = w;
+            for (int nt = 0; nt < NT; ++nt) {
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt][0], bv[nt][0], acc[mt][nt], 0, 0, 0);
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt][1], bv[nt][1], acc[mt][nt], 0, 0, 0);
             }
 }
-// (the number of row tiles is wave-uniform: one instance per count, no predicated MFMA)
-template <int GS, int TS, int BS, int MT, int NT>
-__device__ __attribute__((always_inline)) inline void fold_block(float* PlT, const float* G, const float* D, int r0, int r1, int s0, float lr,
-                                  int nt0, int lane) {
-    const int nmt = __builtin_amdgcn_readfirstlane((r1 - r0 + 15) >> 4);
-    static_assert(MT == 4, "up to four row tiles (chunks of 64 rows)");
-    switch (nmt) {
-    case 1: fold_tiles<GS, TS, BS, 1, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
-    case 2: fold_tiles<GS, TS, BS, 2, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
-    case 3: fold_tiles<GS, TS, BS, 3, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
-    case 4: fold_tiles<GS, TS, BS, 4, NT>(PlT, G, D, r0, r1, s0, lr, nt0, lane); break;
-    default: break;
-    }
+// The eight rows of block B of a chunk are final: PlT[h][t] = Q[h][t] - eta acc[t][h] for
+// those rows and this wave's neurons (PlT and Q both [neuron][row], row stride TS; Q in
+// global memory).  The rows are half of row tile B / 2: lane groups 2 (B & 1) and 2 (B & 1) + 1.
+template <int TS, int MT, int NT>
+__device__ __attribute__((always_inline)) inline void write_rows(const f4 (&acc)[MT][NT], float* PlT, const float* Q, int B,
+                                                                 float lr, int nt0, int lane) {
+    const int r16 = lane & 15, g = lane >> 4;
+    const int mtw = B >> 1;  // wave-uniform
+    const bool mine = (g >> 1) == (B & 1);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+        if (mt == mtw && mine) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int idx = ((nt0 + nt) * 16 + r16) * TS + mt * 16 + 4 * g;
+                const float4 q = *(const float4*)(Q + idx);
+                float4 w;
+                w.x = q.x - lr * acc[mt][nt][0];
+                w.y = q.y - lr * acc[mt][nt][1];
+                w.z = q.z - lr * acc[mt][nt][2];
+                w.w = q.w - lr * acc[mt][nt][3];
+                *(float4*)(PlT + idx) = w;
+            }
+        }
 }
 
 // Bounded wait on a counter in LDS written by another wave of the workgroup.  The LDS
@@ -1145,6 +1142,20 @@ __device__ inline bool lds_wait_geq(const int* f, int target, int* lab, int* gab
     }
     asm volatile("" ::: "memory");  // later LDS reads stay after the counter read
     return true;
+}
+// Three counters at once: a single LDS round trip when all have reached their targets.
+__device__ inline void lds_wait3(const int* f0, int t0, const int* f1, int t1, const int* f2, int t2, int* lab,
+                                 int* gabort, long limit) {
+    const int v0 = __hip_atomic_load(f0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const int v1 = __hip_atomic_load(f1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const int v2 = __hip_atomic_load(f2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (__builtin_amdgcn_readfirstlane(v0) < t0 || __builtin_amdgcn_readfirstlane(v1) < t1 ||
+        __builtin_amdgcn_readfirstlane(v2) < t2) {
+        lds_wait_geq(f0, t0, lab, gabort, limit, false);
+        lds_wait_geq(f1, t1, lab, gabort, limit, false);
+        lds_wait_geq(f2, t2, lab, gabort, limit, false);
+    }
+    asm volatile("" ::: "memory");  // later LDS reads stay after the counter reads
 }
 __device__ inline int lds_read(const int* f) {
     const int v = __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -1172,25 +1183,29 @@ __device__ inline void lds_publish(int* f, int v) {
 // Who adds which term d1_s (x_s . x_r) of row r (block B):
 //   s < BS(B-1):        folded into the stored input sums Pl of row r in the background, on
 //                       the matrix cores, a whole block at a time;
-//   s in [BS(B-1), r-3]: the window correction cpre[r] (at most 2 BS - 3 terms), computed by
-//                       wave 1 while the live wave runs steps r-2 and r-1;
-//   s = r-2, r-1:       the live wave, with its own fresh errors.
+//   s in [BS(B-1), r-4]: the window correction cpre[r] (at most 2 BS - 4 terms), computed by
+//                       wave 1 while the live wave runs steps r-3 to r-1;
+//   s = r-3, r-2, r-1:  the live wave, with its own fresh errors.
 //
 // Waves (256 threads), each in its own loop, coordinated through counters in LDS:
 //   wave 0, live:  the steps.  Lane l owns hidden neurons l and l + 64 (NH = 2) or l
 //                  (NH = 1): their b1 and W2 columns stay in registers.
 //   wave 1:        the window corrections, one row ahead of the live wave.
-//   waves 2, 3:    the folds, each for half of the neurons: a finished block B' goes into
-//                  the rows of blocks >= B'+2 of its chunk (a chunk's last block: into rows
-//                  [BS, T) of the next chunk) as soon as it is finished, and (the other
-//                  blocks) into all rows of the next chunk once that chunk's data is in LDS.
+//   waves 2, 3:    the folds, each for half of the neurons.  A wave keeps the sums
+//                  sum_s d1_s (x_s . x_t) of the current chunk's rows (accC) and of the next
+//                  chunk's rows (accN) in registers, as MFMA accumulator tiles.  A finished
+//                  block B' is added to the rows of blocks >= B'+2 of accC, after which the
+//                  rows of block B'+2 are final and are written once to the input-sum array
+//                  Pl as Q - eta acc; and, once the next chunk's Gram blocks are in LDS, to
+//                  all rows of accN (block NB-2 completes the next chunk's block 0, block
+//                  NB-1 its block 1: both are written then, and accN becomes accC).
 //                  Wave 3 also publishes each finished block's d1 for the tile workgroups,
-//                  announces finished chunks to them, and loads the next chunk's Q, Gram
-//                  blocks and labels into LDS once the tiles have published Q.
+//                  announces finished chunks to them, and early in each chunk loads the
+//                  next chunk's Gram blocks and labels into LDS.
 // Counters (LDS): d1done (steps whose d1 is in hist), cdone (rows whose cpre is ready),
-// fcur (blocks folded into the rows of the chunk that needs them), fnext (blocks folded
-// into the next chunk's rows), nready (chunks whose data is in LDS), pubd (blocks whose d1
-// has been copied out of hist), abort.
+// rdy (per folding wave: leading blocks whose rows of Pl are final), gready (chunks whose
+// Gram blocks and labels are in LDS), pubd (blocks whose d1 has been copied out of hist),
+// abort.
 template <int T, int NH, int A1, int A2, int LS, int OC>
 __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& a, int k, float* smem) {
     constexpr int HW = 64 * NH;     // neurons covered by the live wave
@@ -1203,18 +1218,17 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     const int H = a.H, K = a.k_rep;
     const float lr = a.lr;
 
-    float* Pl = smem;                   // [2][HW][TS] input sums (transposed: [neuron][row]) by chunk parity
-    float* hist = Pl + 2 * HW * TS;     // [HW][TS]   first-layer errors by step mod T
+    float* Pl = smem;                   // [HW][TS]   input sums (transposed: [neuron][row in chunk])
+    float* hist = Pl + HW * TS;         // [HW][TS]   first-layer errors by step mod T
     float* Gin = hist + HW * TS;        // [2][T][GS] Gram blocks within a chunk, by parity
     float* GX = Gin + 2 * T * GS;       // [T][GS]    a chunk (rows) against the previous one
-    float* cpre = GX + T * GS;          // [2][HW]    window corrections by row parity
-    int* yb = (int*)(cpre + 2 * HW);    // [2][T]     labels by chunk parity
+    float* cpre = GX + T * GS;          // [4][HW]    window corrections by row mod 4
+    int* yb = (int*)(cpre + 4 * HW);    // [2][T]     labels by chunk parity
     int* lf = yb + 2 * T;
     int* d1done = lf;
     int* cdone = lf + 1;
-    int* fcur = lf + 2;    // [2]: one counter per folding wave
-    int* fnext = lf + 4;   // [2]
-    int* nready = lf + 6;
+    int* rdy = lf + 2;     // [2]: one counter per folding wave
+    int* gready = lf + 6;
     int* lab = lf + 7;
     int* pubd = lf + 8;
 
@@ -1229,7 +1243,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
 
     // padding neurons h >= H read zero errors and zero input sums
     for (int i = tid; i < HW * TS; i += 256) hist[i] = 0.f;
-    for (int i = tid; i < 2 * HW * TS; i += 256) Pl[i] = 0.f;
+    for (int i = tid; i < HW * TS; i += 256) Pl[i] = 0.f;
     if (tid < 12) lf[tid] = 0;
 
     // chunk 0: wait for Q_0 and stage it with the Gram block and labels
@@ -1241,7 +1255,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         for (int idx = tid; idx < HW * TS; idx += 256) Pl[idx] = Q[idx];
         for (int idx = tid; idx < T * GS; idx += 256) Gin[idx] = G[idx];
         for (int idx = tid; idx < tc0; idx += 256) yb[idx] = a.y[xs + idx];
-        if (tid == 0) nready[0] = 1;
+        if (tid == 0) { gready[0] = 1; rdy[0] = 2; rdy[1] = 2; }
     }
     __syncthreads();
 
@@ -1255,7 +1269,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         const int act1 = A1 >= 0 ? A1 : a.act1;
         const int act2 = A2 >= 0 ? A2 : a.act2;
         const int loss = LS >= 0 ? LS : a.loss;
-        float w2[NH][OC], b1[NH], corr[NH], dprev[NH], pln[NH];
+        float w2[NH][OC], b1[NH], corr[NH], dprev[NH], dprev2[NH], pln[NH];
         const int ol = lane & 15;
         const int own = OC == 10 ? own10(ol) : ol;  // output whose total this lane holds
         const bool owner = own >= 0 && own < O;
@@ -1267,6 +1281,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             for (int o = 0; o < OC; ++o) w2[j][o] = (h < H && o < O) ? th[a.off_w2 + (size_t)o * H + h] : 0.f;
             corr[j] = 0.f;
             dprev[j] = 0.f;
+            dprev2[j] = 0.f;
             pln[j] = Pl[h * TS];
         }
         float b2v = owner ? th[a.off_b2 + own] : 0.f;
@@ -1280,19 +1295,12 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             const bool more = r + 1 < nsteps;
             const bool cross = more && t + 1 == tc;
             if (more && ((r + 1) % BS) == 0) {
-                // the next row opens block Bn: its input sums must hold every block up to
-                // Bn - 2 (next chunk: its data loaded and blocks 0..NB-2 of this one), and
-                // the hist columns it will overwrite must have been copied out (block Bn - NB)
+                // the next row opens block Bn: its input sums must be final in Pl (both
+                // folding waves; at a chunk's first row this also means the chunk's Gram
+                // blocks and labels are in LDS), and the hist columns it will overwrite must
+                // have been copied out (block Bn - NB)
                 const int Bn = (r + 1) / BS;
-                if (cross) {
-                    lds_wait_geq(nready, c + 2, lab, gabort, a.spin_limit, false);
-                    lds_wait_geq(fnext, NB * c + NB - 1, lab, gabort, a.spin_limit, false);
-                    lds_wait_geq(fnext + 1, NB * c + NB - 1, lab, gabort, a.spin_limit, false);
-                } else {
-                    lds_wait_geq(fcur, Bn - 1, lab, gabort, a.spin_limit, false);
-                    lds_wait_geq(fcur + 1, Bn - 1, lab, gabort, a.spin_limit, false);
-                }
-                lds_wait_geq(pubd, Bn - NB + 1, lab, gabort, a.spin_limit, false);
+                lds_wait3(rdy, Bn + 1, rdy + 1, Bn + 1, pubd, Bn - NB + 1, lab, gabort, a.spin_limit);
             }
             // operands of the step's end, read up front (unconditional loads from valid
             // addresses, so every path leaves the same LDS reads in flight)
@@ -1300,15 +1308,17 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             const int cn = rn >> 6, tn = rn & (T - 1);
             float cp[NH], pnx[NH];
 #pragma unroll
-            for (int j = 0; j < NH; ++j) pnx[j] = Pl[(cn & 1) * HW * TS + (lane + 64 * j) * TS + tn];
-            // Gram entries of the next row against steps r and r-1: within the next row's
-            // chunk from its G block, against the chunk before it from GX (which holds the
-            // next row's chunk against the previous one whenever the next row needs it)
+            for (int j = 0; j < NH; ++j) pnx[j] = Pl[(lane + 64 * j) * TS + tn];
+            // Gram entries of the next row against steps r, r-1 and r-2: within the next
+            // row's chunk from its G block, against the chunk before it from GX (which holds
+            // the next row's chunk against the previous one whenever the next row needs it)
             const float* gin = grow_in(cn) + tn * GS;
             const float* gx = GX + tn * GS;
             const float g1v = cross ? gx[t] : gin[t];
-            const int tp = t > 0 ? t - 1 : T - 1;      // position of step r-1 in its chunk
-            const float g0v = (cross || t == 0) ? gx[tp] : gin[tp];
+            const int tp = (t + T - 1) & (T - 1);      // position of step r-1 in its chunk
+            const float g0v = (cross || t < 1) ? gx[tp] : gin[tp];
+            const int tp2 = (t + T - 2) & (T - 1);     // position of step r-2 in its chunk
+            const float g2v = (cross || t < 2) ? gx[tp2] : gin[tp2];
             const int labn = yb[(cn & 1) * T + tn];
 
             float a1[NH], na[NH];
@@ -1342,7 +1352,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             const int cd = __hip_atomic_load(cdone, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             asm volatile("" ::: "memory");
 #pragma unroll
-            for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 1) * HW + lane + 64 * j];
+            for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 3) * HW + lane + 64 * j];
             float x2;
             if (act2 == ACT_SOFTMAX) {
                 const float m = row_allmax16(owner ? z2 : -INFINITY);
@@ -1370,15 +1380,15 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 if (__builtin_amdgcn_readfirstlane(cd) < r + 2) {
                     lds_wait_geq(cdone, r + 2, lab, gabort, a.spin_limit, false);
 #pragma unroll
-                    for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 1) * HW + lane + 64 * j];
+                    for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 3) * HW + lane + 64 * j];
                 }
-                // terms of steps r and r-1 (r-1 only if it lies in the window of the next
-                // row's block pair, which always holds: it is at most two steps back)
-                const bool has0 = r >= 1;
-                const float g1 = g1v, g0 = has0 ? g0v : 0.f;
+                // terms of steps r, r-1 and r-2 (all three lie in the next row's two-block
+                // window, not yet folded: they are at most three steps back)
+                const float g1 = g1v, g0 = r >= 1 ? g0v : 0.f, g2 = r >= 2 ? g2v : 0.f;
 #pragma unroll
                 for (int j = 0; j < NH; ++j) {
-                    corr[j] = cp[j] + dprev[j] * g0 + d1[j] * g1;
+                    corr[j] = cp[j] + dprev2[j] * g2 + dprev[j] * g0 + d1[j] * g1;
+                    dprev2[j] = dprev[j];
                     dprev[j] = d1[j];
                     pln[j] = pnx[j];
                 }
@@ -1401,19 +1411,19 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         if (lane < 16 && owner) th[a.off_b2 + own] = b2v;
     } else if (wave == 1) {
         // ================= window corrections: for row q = r + 1 (block B = q / BS),
-        // cpre[q] = sum over s in [BS(B-1), q-3] of d1_s (x_s . x_q)
+        // cpre[q] = sum over s in [BS(B-1), q-4] of d1_s (x_s . x_q)
         for (int r = 0; r + 1 < nsteps; ++r) {
             const int q = r + 1;
             const int cq = q >> 6, tq = q & (T - 1), B = q / BS;
-            // the live wave has finished step r-2: d1 up to q-3 is in hist and the slot
-            // (q & 1) (last holding the correction of row q-2) is free
-            lds_wait_geq(d1done, r - 1, lab, gabort, a.spin_limit, true);
+            // the live wave has finished step r-3: d1 up to q-4 is in hist and the slot
+            // (q & 3) (last holding the correction of row q-4) is free
+            lds_wait_geq(d1done, r - 2, lab, gabort, a.spin_limit, false);
             // a chunk's first rows read its Gram blocks (and GX) before the live wave enters it
-            if (tq < BS && cq >= 1) lds_wait_geq(nready, cq + 1, lab, gabort, a.spin_limit, true);
+            if (tq < BS && cq >= 1) lds_wait_geq(gready, cq + 1, lab, gabort, a.spin_limit, true);
             float sum[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) sum[j] = 0.f;
-            const int lo = max(0, BS * (B - 1)), hi = q - 3;  // inclusive range
+            const int lo = max(0, BS * (B - 1)), hi = q - 4;  // inclusive range
             // two aligned groups of BS steps: the previous block and the row's own block
 #pragma unroll
             for (int part = 0; part < 2; ++part) {
@@ -1441,25 +1451,35 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 }
             }
 #pragma unroll
-            for (int j = 0; j < NH; ++j) cpre[(q & 1) * HW + lane + 64 * j] = sum[j];
+            for (int j = 0; j < NH; ++j) cpre[(q & 3) * HW + lane + 64 * j] = sum[j];
             lds_publish(cdone, q + 1);
         }
     } else {
         // ================= waves 2 and 3: the folds, each wave for half of the neuron tiles;
         // wave 3 also publishes the finished blocks' d1 and loads the next chunk's data
         constexpr int NNT = HW / 16;
+        constexpr int NT = NNT / 2;  // neuron tiles of this wave
+        constexpr int MT = T / 16;   // row tiles of a chunk
         const int w2i = wave - 2;
         const bool io = wave == 3;
-        const int nt0 = w2i * (NNT / 2);
-        int* fc = fcur + w2i;
-        int* fn = fnext + w2i;
-        int cur = 0;     // next block whose fold into the rows that need it is pending
-        int nxt = 0;     // next block whose fold into the next chunk's rows is pending
+        const int nt0 = w2i * NT;
+        int* rd = rdy + w2i;
+        f4 accC[MT][NT], accN[MT][NT];  // sums of the current and of the next chunk's rows
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                accC[mt][nt] = f4{0.f, 0.f, 0.f, 0.f};
+                accN[mt][nt] = f4{0.f, 0.f, 0.f, 0.f};
+            }
+        auto qrows = [&](int c) { return a.qbuf + ((size_t)(c & 1) * K + k) * HW * TS; };  // Q_c, [HW][TS]
+        int fc = 0;      // next block to fold into its own chunk's rows
+        int fn = 0;      // next block to fold into the next chunk's rows
+        int qseen = 1;   // chunks whose Q this wave has acquired (Q_0 before the loop)
         int pub = 0;     // (wave 3) next block to publish
-        int loaded = 1;  // (wave 3) chunks whose data is in LDS
-        int polls = 0;
+        int loaded = 1;  // (wave 3) chunks whose Gram blocks and labels are in LDS
         long idle = 0;
-        while (cur < nblk || nxt < nblk || (io && (pub < nblk || loaded < nchk))) {
+        while (fc < nblk || fn < nblk || (io && (pub < nblk || loaded < nchk))) {
             bool progress = false;
             const int dd = lds_read(d1done);
             if (io && pub < nblk && dd >= min(BS * (pub + 1), nsteps)) {
@@ -1480,68 +1500,76 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                     if (lane == 0) __hip_atomic_store(dready, c + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
                 progress = true;
-            } else if (cur < nblk && dd >= min(BS * (cur + 1), nsteps)) {
-                // ---- block `cur` into the later rows of its chunk
-                const int c = cur / NB, b = cur % NB, tc = chunk_len(c);
-                if (BS * (b + 2) < tc) {
-                    fold_block<GS, TS, BS, T / 16, NNT / 2>(Pl + (c & 1) * HW * TS, grow_in(c), hist, BS * (b + 2), tc,
-                                                            BS * b, lr, nt0, lane);
-                } else if (b == NB - 1 && c + 1 < nchk) {
-                    // last block of a chunk: rows [BS, T) of the next chunk (its first block
-                    // takes it through the window); the live wave has waited for that chunk
-                    lds_wait_geq(nready, c + 2, lab, gabort, a.spin_limit, true);
-                    const int tn = chunk_len(c + 1);
-                    if (tn > BS)
-                        fold_block<GS, TS, BS, T / 16, NNT / 2>(Pl + ((c + 1) & 1) * HW * TS, GX, hist, BS, tn,
-                                                                T - BS, lr, nt0, lane);
+            } else if (fc < nblk && dd >= min(BS * (fc + 1), nsteps) && fn >= NB * (fc / NB)) {
+                // ---- block fc into the later rows of its own chunk (accC is that chunk's:
+                // every fold of the previous chunk into it is done); rows of block b+2 final
+                const int c = fc / NB, b = fc % NB;
+                if (BS * (b + 2) < chunk_len(c)) {
+                    fold_acc<GS, TS, MT, NT>(accC, grow_in(c), hist, (b + 2) >> 1, BS * b, nt0, lane);
+                    write_rows<TS, MT, NT>(accC, Pl, qrows(c), b + 2, lr, nt0, lane);
+                    lds_publish(rd, fc + 3);
+                } else if (c + 1 >= nchk) {
+                    lds_publish(rd, fc + 3);  // no rows left to complete
                 }
-                ++cur;
-                lds_publish(fc, cur);
+                ++fc;
                 progress = true;
             } else if (io && loaded < nchk) {
-                // ---- load chunk `loaded` into the buffers of parity loaded & 1 once (i) the
-                // tiles have published its Q and (ii) the current chunk no longer needs its
-                // cross Gram block: the first block's window corrections are done, and the
-                // previous chunk's last block is folded into it (by both waves)
+                // ---- load chunk `loaded`'s Gram blocks and labels into the buffers of parity
+                // loaded & 1 once the current chunk no longer needs the cross Gram block: the
+                // first block's window corrections are done and both waves have completed
+                // the chunk's rows of blocks 0 and 1 (the folds that read it).  The buffers of
+                // that parity last served the chunk before the current one.
                 const int c = loaded - 1;  // chunk the live wave is in (or before)
                 const bool gx_free = (c == 0) || (lds_read(cdone) >= min(T * c + BS + 1, nsteps) &&
-                                                  lds_read(fcur) >= NB * c && lds_read(fcur + 1) >= NB * c);
-                if (gx_free && (++polls & 7) == 0) {
-                    const int q = __builtin_amdgcn_readfirstlane(
-                        __hip_atomic_load(qready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-                    if (q >= a.nrb * (loaded + 1)) {
-                        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                        const int cn = loaded, tcn = chunk_len(cn);
-                        const float* Q = a.qbuf + ((size_t)(cn & 1) * K + k) * HW * TS;
-                        const float* G = a.gram + ((size_t)k * a.nch + cn) * T * GS;
-                        const float* GXg = a.gramx + ((size_t)k * (a.nch - 1) + cn - 1) * T * GS;
-                        wave_copy_to_lds(Q, Pl + (cn & 1) * HW * TS, HW * TS * 4, 0, 1, lane);
-                        wave_copy_to_lds(G, Gin + (cn & 1) * T * GS, T * GS * 4, 0, 1, lane);
-                        wave_copy_to_lds(GXg, GX, T * GS * 4, 0, 1, lane);
-                        {
-                            const int rr = min(lane, tcn - 1);
-                            __builtin_amdgcn_global_load_lds(a.y + xs + (int64_t)cn * T + rr,
-                                                             (lds_void*)(yb + (cn & 1) * T), 4, 0, 0);
-                        }
-                        wait_vm_all();
-                        ++loaded;
-                        lds_publish(nready, loaded);
-                        progress = true;
+                                                  lds_read(rdy) >= NB * c + 2 && lds_read(rdy + 1) >= NB * c + 2);
+                if (gx_free) {
+                    const int cn = loaded, tcn = chunk_len(cn);
+                    const float* G = a.gram + ((size_t)k * a.nch + cn) * T * GS;
+                    const float* GXg = a.gramx + ((size_t)k * (a.nch - 1) + cn - 1) * T * GS;
+                    wave_copy_to_lds(G, Gin + (cn & 1) * T * GS, T * GS * 4, 0, 1, lane);
+                    wave_copy_to_lds(GXg, GX, T * GS * 4, 0, 1, lane);
+                    {
+                        const int rr = min(lane, tcn - 1);
+                        __builtin_amdgcn_global_load_lds(a.y + xs + (int64_t)cn * T + rr,
+                                                         (lds_void*)(yb + (cn & 1) * T), 4, 0, 0);
                     }
+                    wait_vm_all();
+                    ++loaded;
+                    lds_publish(gready, loaded);
+                    progress = true;
                 }
             }
-            if (!progress && nxt < cur) {
-                // ---- block `nxt` into every row of the next chunk, once that chunk is loaded
-                const int c = nxt / NB, b = nxt % NB;
-                if (b == NB - 1 || c + 1 >= nchk) {
-                    ++nxt;  // nothing of this block goes into the next chunk here
-                    lds_publish(fn, nxt);
+            if (!progress && fn < fc) {
+                // ---- block fn into every row of the next chunk, once its Gram blocks are in
+                // LDS; blocks NB-2 and NB-1 complete the next chunk's blocks 0 and 1 (Q of
+                // the next chunk needed: the tiles publish it one chunk ahead)
+                const int c = fn / NB, b = fn % NB;
+                if (c + 1 >= nchk) {
+                    ++fn;  // nothing of this block goes into a next chunk
                     progress = true;
-                } else if (lds_read(nready) >= c + 2) {
-                    fold_block<GS, TS, BS, T / 16, NNT / 2>(Pl + ((c + 1) & 1) * HW * TS, GX, hist, 0,
-                                                            chunk_len(c + 1), BS * b, lr, nt0, lane);
-                    ++nxt;
-                    lds_publish(fn, nxt);
+                } else if (lds_read(gready) >= c + 2) {
+                    fold_acc<GS, TS, MT, NT>(accN, GX, hist, 0, BS * b, nt0, lane);
+                    if (b >= NB - 2) {
+                        if (qseen < c + 2) {
+                            if (!wait_geq_wave(qready, a.nrb * (c + 2), gabort, a.spin_limit)) {
+                                lds_publish(lab, 1);
+                                break;
+                            }
+                            qseen = c + 2;
+                        }
+                        write_rows<TS, MT, NT>(accN, Pl, qrows(c + 1), b - (NB - 2), lr, nt0, lane);
+                        lds_publish(rd, NB * (c + 1) + b - (NB - 2) + 1);
+                        if (b == NB - 1) {
+#pragma unroll
+                            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                                for (int nt = 0; nt < NT; ++nt) {
+                                    accC[mt][nt] = accN[mt][nt];
+                                    accN[mt][nt] = f4{0.f, 0.f, 0.f, 0.f};
+                                }
+                        }
+                    }
+                    ++fn;
                     progress = true;
                 }
             }
@@ -1552,7 +1580,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                     __hip_atomic_store(gabort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     break;
                 }
-                __builtin_amdgcn_s_sleep(2);
+                __builtin_amdgcn_s_sleep(1);
             } else {
                 idle = 0;
             }
