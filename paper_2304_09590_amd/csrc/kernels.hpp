@@ -1073,7 +1073,7 @@ __device__ inline void backprop_outputs(float (&back)[NH], float (&w2)[NH][OC], 
 // ------------------------------------------------------------------------------------
 // Fold of one finished block of BS = 8 steps into a chunk's input-sum accumulator held in
 // registers, on the matrix cores:
-//   acc[t][h] += sum_{s in block} G[t][s] * D[h][s]
+//   acc[t][h] += scale * sum_{s in block} G[t][s] * D[h][s]      (scale = -eta)
 // for the row tiles mt >= mt0 (16 rows each) and the NT neuron tiles starting at nt0 (16
 // neurons each).  G rows have stride GS; D rows (one per neuron) have stride TS.
 // v_mfma_f32_16x16x4_f32 contracts 4 steps per instruction; lane group g = lane / 16
@@ -1083,14 +1083,14 @@ __device__ inline void backprop_outputs(float (&back)[NH], float (&w2)[NH][OC], 
 // also receive it; they are final already and never written again.
 template <int GS, int TS, int MT, int NT>
 __device__ __attribute__((always_inline)) inline void fold_acc(f4 (&acc)[MT][NT], const float* G, const float* D,
-                                                               int mt0, int s0, int nt0, int lane) {
+                                                               int mt0, int s0, float scale, int nt0, int lane) {
     typedef float v2 __attribute__((ext_vector_type(2)));
     const int r16 = lane & 15, g = lane >> 4;
     v2 av[MT], bv[NT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) av[mt] = *(const v2*)(G + (mt * 16 + r16) * GS + s0 + 2 * g);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) bv[nt] = *(const v2*)(D + ((nt0 + nt) * 16 + r16) * TS + s0 + 2 * g);
+    for (int nt = 0; nt < NT; ++nt) bv[nt] = *(const v2*)(D + ((nt0 + nt) * 16 + r16) * TS + s0 + 2 * g) * scale;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
         if (mt >= mt0)  // wave-uniform
@@ -1100,12 +1100,32 @@ __device__ __attribute__((always_inline)) inline void fold_acc(f4 (&acc)[MT][NT]
                 acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt][1], bv[nt][1], acc[mt][nt], 0, 0, 0);
             }
 }
-// The eight rows of block B of a chunk are final: PlT[h][t] = Q[h][t] - eta acc[t][h] for
-// those rows and this wave's neurons (PlT and Q both [neuron][row], row stride TS; Q in
-// global memory).  The rows are half of row tile B / 2: lane groups 2 (B & 1) and 2 (B & 1) + 1.
+// acc[t][h] += Q[h][t] for every row of the chunk and this wave's neurons (Q in global
+// memory, [neuron][row] with row stride TS): the tiles' W1 x term of the input sums.
 template <int TS, int MT, int NT>
-__device__ __attribute__((always_inline)) inline void write_rows(const f4 (&acc)[MT][NT], float* PlT, const float* Q, int B,
-                                                                 float lr, int nt0, int lane) {
+__device__ __attribute__((always_inline)) inline void add_q(f4 (&acc)[MT][NT], const float* Q, int nt0, int lane) {
+    const int r16 = lane & 15, g = lane >> 4;
+    float4 q[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) q[mt][nt] = *(const float4*)(Q + ((nt0 + nt) * 16 + r16) * TS + mt * 16 + 4 * g);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            acc[mt][nt][0] += q[mt][nt].x;
+            acc[mt][nt][1] += q[mt][nt].y;
+            acc[mt][nt][2] += q[mt][nt].z;
+            acc[mt][nt][3] += q[mt][nt].w;
+        }
+}
+// The eight rows of block B of a chunk are final: PlT[h][t] = acc[t][h] for those rows and
+// this wave's neurons (PlT [neuron][row], row stride TS).  The rows are half of row tile
+// B / 2: lane groups 2 (B & 1) and 2 (B & 1) + 1.
+template <int TS, int MT, int NT>
+__device__ __attribute__((always_inline)) inline void write_rows(const f4 (&acc)[MT][NT], float* PlT, int B, int nt0,
+                                                                 int lane) {
     const int r16 = lane & 15, g = lane >> 4;
     const int mtw = B >> 1;  // wave-uniform
     const bool mine = (g >> 1) == (B & 1);
@@ -1115,13 +1135,7 @@ __device__ __attribute__((always_inline)) inline void write_rows(const f4 (&acc)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
                 const int idx = ((nt0 + nt) * 16 + r16) * TS + mt * 16 + 4 * g;
-                const float4 q = *(const float4*)(Q + idx);
-                float4 w;
-                w.x = q.x - lr * acc[mt][nt][0];
-                w.y = q.y - lr * acc[mt][nt][1];
-                w.z = q.z - lr * acc[mt][nt][2];
-                w.w = q.w - lr * acc[mt][nt][3];
-                *(float4*)(PlT + idx) = w;
+                *(float4*)(PlT + idx) = make_float4(acc[mt][nt][0], acc[mt][nt][1], acc[mt][nt][2], acc[mt][nt][3]);
             }
         }
 }
@@ -1136,6 +1150,9 @@ __device__ inline bool lds_wait_geq(const int* f, int target, int* lab, int* gab
         if (++it > limit) {
             __hip_atomic_store(lab, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             __hip_atomic_store(gabort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // (cold path) complete the stores here, so that the compiler need not protect
+            // their operand registers with a wait on the hot path after the call
+            __builtin_amdgcn_s_waitcnt(0x0070);
             return false;
         }
         if (sleep) __builtin_amdgcn_s_sleep(1);
@@ -1149,6 +1166,7 @@ __device__ inline void lds_wait3(const int* f0, int t0, const int* f1, int t1, c
     const int v0 = __hip_atomic_load(f0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     const int v1 = __hip_atomic_load(f1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     const int v2 = __hip_atomic_load(f2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): no path leaves one of the reads in flight
     if (__builtin_amdgcn_readfirstlane(v0) < t0 || __builtin_amdgcn_readfirstlane(v1) < t1 ||
         __builtin_amdgcn_readfirstlane(v2) < t2) {
         lds_wait_geq(f0, t0, lab, gabort, limit, false);
@@ -1193,12 +1211,13 @@ __device__ inline void lds_publish(int* f, int v) {
 //   wave 1:        the window corrections, one row ahead of the live wave.
 //   waves 2, 3:    the folds, each for half of the neurons.  A wave keeps the sums
 //                  sum_s d1_s (x_s . x_t) of the current chunk's rows (accC) and of the next
-//                  chunk's rows (accN) in registers, as MFMA accumulator tiles.  A finished
-//                  block B' is added to the rows of blocks >= B'+2 of accC, after which the
-//                  rows of block B'+2 are final and are written once to the input-sum array
-//                  Pl as Q - eta acc; and, once the next chunk's Gram blocks are in LDS, to
-//                  all rows of accN (block NB-2 completes the next chunk's block 0, block
-//                  NB-1 its block 1: both are written then, and accN becomes accC).
+//                  chunk's rows (accN) in registers, as MFMA accumulator tiles holding
+//                  Q - eta sum (Q, the tiles' W1 x, is added once it is published).  A
+//                  finished block B' is added to the rows of blocks >= B'+2 of accC, after
+//                  which the rows of block B'+2 are final and are written once to the input-
+//                  sum array Pl; and, once the next chunk's Gram blocks are in LDS, to all
+//                  rows of accN (block NB-2 completes the next chunk's block 0, block NB-1 its
+//                  block 1: both are written then, and accN becomes accC).
 //                  Wave 3 also publishes each finished block's d1 for the tile workgroups,
 //                  announces finished chunks to them, and early in each chunk loads the
 //                  next chunk's Gram blocks and labels into LDS.
@@ -1286,7 +1305,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         }
         float b2v = owner ? th[a.off_b2 + own] : 0.f;
         int label = yb[0];  // label of the current row; the next row's is read a step ahead
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0), visible to the compiler's wait placement
 
         for (int r = 0; r < nsteps; ++r) {
             const int c = r >> 6, t = r & (T - 1);
@@ -1369,6 +1388,10 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
 #pragma unroll
             for (int j = 0; j < NH; ++j) back[j] = 0.f;
             backprop_outputs<OC, NH, 0>(back, w2, d2, na);
+            // Every LDS read of this step has long returned: an explicit wait (seen by the
+            // compiler's wait placement) leaves only stores in flight at the loop head, so the
+            // next step starts without waiting for this step's stores to complete.
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
             float d1[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) {
@@ -1376,14 +1399,17 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 b1[j] -= lr * d1[j];
                 hist[(lane + 64 * j) * TS + t] = d1[j];
             }
-            if (more) {
-                if (__builtin_amdgcn_readfirstlane(cd) < r + 2) {
-                    lds_wait_geq(cdone, r + 2, lab, gabort, a.spin_limit, false);
+            if (more && __builtin_amdgcn_readfirstlane(cd) < r + 2) {
+                lds_wait_geq(cdone, r + 2, lab, gabort, a.spin_limit, false);
 #pragma unroll
-                    for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 3) * HW + lane + 64 * j];
-                }
-                // terms of steps r, r-1 and r-2 (all three lie in the next row's two-block
-                // window, not yet folded: they are at most three steps back)
+                for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 3) * HW + lane + 64 * j];
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // (slow path) lgkmcnt(0) here, not after the join
+            }
+            // terms of steps r, r-1 and r-2 (all three lie in the next row's two-block window,
+            // not yet folded: they are at most three steps back).  Also done after the last
+            // step (unused then): every path consumes the loads it issued, so none is still in
+            // flight into a register at the loop head.
+            {
                 const float g1 = g1v, g0 = r >= 1 ? g0v : 0.f, g2 = r >= 2 ? g2v : 0.f;
 #pragma unroll
                 for (int j = 0; j < NH; ++j) {
@@ -1473,9 +1499,10 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 accN[mt][nt] = f4{0.f, 0.f, 0.f, 0.f};
             }
         auto qrows = [&](int c) { return a.qbuf + ((size_t)(c & 1) * K + k) * HW * TS; };  // Q_c, [HW][TS]
+        add_q<TS, MT, NT>(accC, qrows(0), nt0, lane);  // (Q_0 was acquired before the roles split)
+        bool qn = false;  // Q of accN's chunk added
         int fc = 0;      // next block to fold into its own chunk's rows
         int fn = 0;      // next block to fold into the next chunk's rows
-        int qseen = 1;   // chunks whose Q this wave has acquired (Q_0 before the loop)
         int pub = 0;     // (wave 3) next block to publish
         int loaded = 1;  // (wave 3) chunks whose Gram blocks and labels are in LDS
         long idle = 0;
@@ -1505,8 +1532,8 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 // every fold of the previous chunk into it is done); rows of block b+2 final
                 const int c = fc / NB, b = fc % NB;
                 if (BS * (b + 2) < chunk_len(c)) {
-                    fold_acc<GS, TS, MT, NT>(accC, grow_in(c), hist, (b + 2) >> 1, BS * b, nt0, lane);
-                    write_rows<TS, MT, NT>(accC, Pl, qrows(c), b + 2, lr, nt0, lane);
+                    fold_acc<GS, TS, MT, NT>(accC, grow_in(c), hist, (b + 2) >> 1, BS * b, -lr, nt0, lane);
+                    write_rows<TS, MT, NT>(accC, Pl, b + 2, nt0, lane);
                     lds_publish(rd, fc + 3);
                 } else if (c + 1 >= nchk) {
                     lds_publish(rd, fc + 3);  // no rows left to complete
@@ -1548,16 +1575,17 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                     ++fn;  // nothing of this block goes into a next chunk
                     progress = true;
                 } else if (lds_read(gready) >= c + 2) {
-                    fold_acc<GS, TS, MT, NT>(accN, GX, hist, 0, BS * b, nt0, lane);
+                    fold_acc<GS, TS, MT, NT>(accN, GX, hist, 0, BS * b, -lr, nt0, lane);
                     if (b >= NB - 2) {
-                        if (qseen < c + 2) {
+                        if (!qn) {
                             if (!wait_geq_wave(qready, a.nrb * (c + 2), gabort, a.spin_limit)) {
                                 lds_publish(lab, 1);
                                 break;
                             }
-                            qseen = c + 2;
+                            add_q<TS, MT, NT>(accN, qrows(c + 1), nt0, lane);
+                            qn = true;
                         }
-                        write_rows<TS, MT, NT>(accN, Pl, qrows(c + 1), b - (NB - 2), lr, nt0, lane);
+                        write_rows<TS, MT, NT>(accN, Pl, b - (NB - 2), nt0, lane);
                         lds_publish(rd, NB * (c + 1) + b - (NB - 2) + 1);
                         if (b == NB - 1) {
 #pragma unroll
@@ -1567,9 +1595,22 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                                     accC[mt][nt] = accN[mt][nt];
                                     accN[mt][nt] = f4{0.f, 0.f, 0.f, 0.f};
                                 }
+                            qn = false;
                         }
                     }
                     ++fn;
+                    progress = true;
+                }
+            }
+            if (!progress && !qn && fn / NB + 1 < nchk && (idle & 7) == 0) {
+                // ---- Q of accN's chunk, as soon as the tiles have published it
+                const int cq = fn / NB + 1;
+                const int qv = __builtin_amdgcn_readfirstlane(
+                    __hip_atomic_load(qready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                if (qv >= a.nrb * (cq + 1)) {
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                    add_q<TS, MT, NT>(accN, qrows(cq), nt0, lane);
+                    qn = true;
                     progress = true;
                 }
             }
