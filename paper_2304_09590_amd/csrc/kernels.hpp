@@ -1201,9 +1201,9 @@ __device__ inline void lds_publish(int* f, int v) {
 // Who adds which term d1_s (x_s . x_r) of row r (block B):
 //   s < BS(B-1):        folded into the stored input sums Pl of row r in the background, on
 //                       the matrix cores, a whole block at a time;
-//   s in [BS(B-1), r-4]: the window correction cpre[r] (at most 2 BS - 4 terms), computed by
-//                       wave 1 while the live wave runs steps r-3 to r-1;
-//   s = r-3, r-2, r-1:  the live wave, with its own fresh errors.
+//   s in [BS(B-1), r-5]: the window correction cpre[r] (at most 2 BS - 5 terms), computed by
+//                       wave 1 while the live wave runs steps r-4 to r-1;
+//   s = r-4 .. r-1:     the live wave, with its own fresh errors.
 //
 // Waves (256 threads), each in its own loop, coordinated through counters in LDS:
 //   wave 0, live:  the steps.  Lane l owns hidden neurons l and l + 64 (NH = 2) or l
@@ -1218,9 +1218,9 @@ __device__ inline void lds_publish(int* f, int v) {
 //                  sum array Pl; and, once the next chunk's Gram blocks are in LDS, to all
 //                  rows of accN (block NB-2 completes the next chunk's block 0, block NB-1 its
 //                  block 1: both are written then, and accN becomes accC).
-//                  Wave 3 also publishes each finished block's d1 for the tile workgroups,
-//                  announces finished chunks to them, and early in each chunk loads the
-//                  next chunk's Gram blocks and labels into LDS.
+//                  Wave 2 also publishes each finished block's d1 for the tile workgroups
+//                  and announces finished chunks to them; wave 3 early in each chunk loads
+//                  the next chunk's Gram blocks and labels into LDS.
 // Counters (LDS): d1done (steps whose d1 is in hist), cdone (rows whose cpre is ready),
 // rdy (per folding wave: leading blocks whose rows of Pl are final), gready (chunks whose
 // Gram blocks and labels are in LDS), pubd (blocks whose d1 has been copied out of hist),
@@ -1288,7 +1288,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         const int act1 = A1 >= 0 ? A1 : a.act1;
         const int act2 = A2 >= 0 ? A2 : a.act2;
         const int loss = LS >= 0 ? LS : a.loss;
-        float w2[NH][OC], b1[NH], corr[NH], dprev[NH], dprev2[NH], pln[NH];
+        float w2[NH][OC], b1[NH], corr[NH], dprev[NH], dprev2[NH], dprev3[NH], pln[NH];
         const int ol = lane & 15;
         const int own = OC == 10 ? own10(ol) : ol;  // output whose total this lane holds
         const bool owner = own >= 0 && own < O;
@@ -1301,19 +1301,28 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             corr[j] = 0.f;
             dprev[j] = 0.f;
             dprev2[j] = 0.f;
+            dprev3[j] = 0.f;
             pln[j] = Pl[h * TS];
         }
         float b2v = owner ? th[a.off_b2 + own] : 0.f;
         int label = yb[0];  // label of the current row; the next row's is read a step ahead
         __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0), visible to the compiler's wait placement
 
-        for (int r = 0; r < nsteps; ++r) {
-            const int c = r >> 6, t = r & (T - 1);
+        // One block of BS steps per outer iteration, unrolled: the block-boundary logic and
+        // the in-block offsets are compile-time, and the rotation of the recent errors is a
+        // register renaming.
+        for (int r0 = 0; r0 < nsteps; r0 += BS) {
+            const int c = r0 >> 6, t0 = r0 & (T - 1);
             const int tc = chunk_len(c);
+#pragma unroll
+        for (int i = 0; i < BS; ++i) {
+            const int r = r0 + i;
+            if (r >= nsteps) break;  // (last block of a ragged slice)
+            const int t = t0 + i;
             // the row after this step: same chunk, or the next chunk's first row
             const bool more = r + 1 < nsteps;
             const bool cross = more && t + 1 == tc;
-            if (more && ((r + 1) % BS) == 0) {
+            if (more && i == BS - 1) {
                 // the next row opens block Bn: its input sums must be final in Pl (both
                 // folding waves; at a chunk's first row this also means the chunk's Gram
                 // blocks and labels are in LDS), and the hist columns it will overwrite must
@@ -1328,9 +1337,9 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             float cp[NH], pnx[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) pnx[j] = Pl[(lane + 64 * j) * TS + tn];
-            // Gram entries of the next row against steps r, r-1 and r-2: within the next
-            // row's chunk from its G block, against the chunk before it from GX (which holds
-            // the next row's chunk against the previous one whenever the next row needs it)
+            // Gram entries of the next row against steps r .. r-3: within the next row's chunk
+            // from its G block, against the chunk before it from GX (which holds the next
+            // row's chunk against the previous one whenever the next row needs it)
             const float* gin = grow_in(cn) + tn * GS;
             const float* gx = GX + tn * GS;
             const float g1v = cross ? gx[t] : gin[t];
@@ -1338,6 +1347,8 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             const float g0v = (cross || t < 1) ? gx[tp] : gin[tp];
             const int tp2 = (t + T - 2) & (T - 1);     // position of step r-2 in its chunk
             const float g2v = (cross || t < 2) ? gx[tp2] : gin[tp2];
+            const int tp3 = (t + T - 3) & (T - 1);     // position of step r-3 in its chunk
+            const float g3v = (cross || t < 3) ? gx[tp3] : gin[tp3];
             const int labn = yb[(cn & 1) * T + tn];
 
             float a1[NH], na[NH];
@@ -1405,15 +1416,16 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 3) * HW + lane + 64 * j];
                 __builtin_amdgcn_s_waitcnt(0xC07F);  // (slow path) lgkmcnt(0) here, not after the join
             }
-            // terms of steps r, r-1 and r-2 (all three lie in the next row's two-block window,
-            // not yet folded: they are at most three steps back).  Also done after the last
-            // step (unused then): every path consumes the loads it issued, so none is still in
+            // terms of steps r .. r-3 (all four lie in the next row's two-block window, not
+            // yet folded: they are at most four steps back).  Also done after the last step
+            // (unused then): every path consumes the loads it issued, so none is still in
             // flight into a register at the loop head.
             {
-                const float g1 = g1v, g0 = r >= 1 ? g0v : 0.f, g2 = r >= 2 ? g2v : 0.f;
+                const float g1 = g1v, g0 = r >= 1 ? g0v : 0.f, g2 = r >= 2 ? g2v : 0.f, g3 = r >= 3 ? g3v : 0.f;
 #pragma unroll
                 for (int j = 0; j < NH; ++j) {
-                    corr[j] = cp[j] + dprev2[j] * g2 + dprev[j] * g0 + d1[j] * g1;
+                    corr[j] = cp[j] + dprev3[j] * g3 + dprev2[j] * g2 + dprev[j] * g0 + d1[j] * g1;
+                    dprev3[j] = dprev2[j];
                     dprev2[j] = dprev[j];
                     dprev[j] = d1[j];
                     pln[j] = pnx[j];
@@ -1423,6 +1435,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             // d1 of this step is in hist, and this step's reads of the correction slot are
             // done: wave 1 may refill it
             lds_publish(d1done, r + 1);
+        }
         }
 #pragma unroll
         for (int j = 0; j < NH; ++j) {
@@ -1437,19 +1450,19 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         if (lane < 16 && owner) th[a.off_b2 + own] = b2v;
     } else if (wave == 1) {
         // ================= window corrections: for row q = r + 1 (block B = q / BS),
-        // cpre[q] = sum over s in [BS(B-1), q-4] of d1_s (x_s . x_q)
+        // cpre[q] = sum over s in [BS(B-1), q-5] of d1_s (x_s . x_q)
         for (int r = 0; r + 1 < nsteps; ++r) {
             const int q = r + 1;
             const int cq = q >> 6, tq = q & (T - 1), B = q / BS;
-            // the live wave has finished step r-3: d1 up to q-4 is in hist and the slot
-            // (q & 3) (last holding the correction of row q-4) is free
-            lds_wait_geq(d1done, r - 2, lab, gabort, a.spin_limit, false);
+            // the live wave has finished step r-4: d1 up to q-5 is in hist and the slot
+            // (q & 3) (last holding the correction of row q-4, read in step q-5) is free
+            lds_wait_geq(d1done, r - 3, lab, gabort, a.spin_limit, false);
             // a chunk's first rows read its Gram blocks (and GX) before the live wave enters it
             if (tq < BS && cq >= 1) lds_wait_geq(gready, cq + 1, lab, gabort, a.spin_limit, true);
             float sum[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) sum[j] = 0.f;
-            const int lo = max(0, BS * (B - 1)), hi = q - 4;  // inclusive range
+            const int lo = max(0, BS * (B - 1)), hi = q - 5;  // inclusive range
             // two aligned groups of BS steps: the previous block and the row's own block
 #pragma unroll
             for (int part = 0; part < 2; ++part) {
@@ -1482,12 +1495,13 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         }
     } else {
         // ================= waves 2 and 3: the folds, each wave for half of the neuron tiles;
-        // wave 3 also publishes the finished blocks' d1 and loads the next chunk's data
+        // wave 2 also publishes the finished blocks' d1, wave 3 loads the next chunk's data
         constexpr int NNT = HW / 16;
         constexpr int NT = NNT / 2;  // neuron tiles of this wave
         constexpr int MT = T / 16;   // row tiles of a chunk
         const int w2i = wave - 2;
-        const bool io = wave == 3;
+        const bool pw = wave == 2;  // publishes the errors
+        const bool lw = wave == 3;  // loads the next chunk's Gram blocks and labels
         const int nt0 = w2i * NT;
         int* rd = rdy + w2i;
         f4 accC[MT][NT], accN[MT][NT];  // sums of the current and of the next chunk's rows
@@ -1503,13 +1517,13 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         bool qn = false;  // Q of accN's chunk added
         int fc = 0;      // next block to fold into its own chunk's rows
         int fn = 0;      // next block to fold into the next chunk's rows
-        int pub = 0;     // (wave 3) next block to publish
+        int pub = 0;     // (wave 2) next block to publish
         int loaded = 1;  // (wave 3) chunks whose Gram blocks and labels are in LDS
         long idle = 0;
-        while (fc < nblk || fn < nblk || (io && (pub < nblk || loaded < nchk))) {
+        while (fc < nblk || fn < nblk || (pw && pub < nblk) || (lw && loaded < nchk)) {
             bool progress = false;
             const int dd = lds_read(d1done);
-            if (io && pub < nblk && dd >= min(BS * (pub + 1), nsteps)) {
+            if (pw && pub < nblk && dd >= min(BS * (pub + 1), nsteps)) {
                 // ---- publish block `pub` for the tile workgroups
                 const int c = pub / NB, b = pub % NB, tc = chunk_len(c);
                 float* dout = a.d1 + ((size_t)(c & 1) * K + k) * T * H;  // [h][T] errors of chunk c
@@ -1540,7 +1554,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 }
                 ++fc;
                 progress = true;
-            } else if (io && loaded < nchk) {
+            } else if (lw && loaded < nchk) {
                 // ---- load chunk `loaded`'s Gram blocks and labels into the buffers of parity
                 // loaded & 1 once the current chunk no longer needs the cross Gram block: the
                 // first block's window corrections are done and both waves have completed
