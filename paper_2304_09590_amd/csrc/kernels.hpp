@@ -324,6 +324,180 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 }
 
 // ------------------------------------------------------------------------------------
+// fp32 GEMM with 128 x 128 tiles for the large mini-batch shapes: four waves of 64 x 64
+// (4 x 4 v_mfma_f32_16x16x4_f32 tiles each), two LDS buffers, the next k-tile's global
+// loads issued before the current tile's matrix instructions and stored to the other buffer
+// after them (one barrier per k-tile).  A KC operand (rows = the tile's non-contraction
+// index) is kept as [row][k] (row stride 20 floats: a lane reads 4 consecutive k at once);
+// an NC operand (rows = the contraction index) as [k][column] (row stride 144 floats: the
+// 4 lane groups of a read hit disjoint banks), so neither is transposed on the way in.
+// Instruction q of a 16-step k-tile contracts the steps {q, 4+q, 8+q, 12+q} on both
+// operands.  Split of the contraction and epilogues as in gemm_kernel.
+
+constexpr int G128_LDK = 20, G128_LDM = 144, G128_TL = 128 * 20;  // (16 * 144 <= 128 * 20)
+
+// KC operand, 128 rows x 16 k: two float4 per thread
+__device__ inline void load_kc128(float4 (&v)[2], const Operand& o, int z, int cn, int64_t xbase, int row0,
+                                  int rows_valid, int k0, int k_valid, int tid) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int idx = tid + h * 256, r = idx >> 2, kq = (idx & 3) * 4;
+        v[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row0 + r < rows_valid && k0 + kq < k_valid)
+            v[h] = *(const float4*)(operand_row(o, 4, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 4);
+    }
+}
+__device__ inline void store_kc128(float* lds, const float4 (&v)[2], int tid) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int idx = tid + h * 256, r = idx >> 2, kq = (idx & 3) * 4;
+        *(float4*)(lds + r * G128_LDK + kq) = v[h];
+    }
+}
+// NC operand, 16 k x 128 columns: two float4 per thread
+__device__ inline void load_nc128(float4 (&v)[2], const Operand& o, int z, int cn, int64_t xbase, int col0,
+                                  int cols_valid, int k0, int k_valid, int tid) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int idx = tid + h * 256, k = idx >> 5, cq = (idx & 31) * 4;
+        v[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (k0 + k < k_valid && col0 + cq < cols_valid)
+            v[h] = *(const float4*)(operand_row(o, 4, z, cn, xbase, k0 + k) + (size_t)(col0 + cq) * 4);
+    }
+}
+__device__ inline void store_nc128(float* lds, const float4 (&v)[2], int tid) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int idx = tid + h * 256, k = idx >> 5, cq = (idx & 31) * 4;
+        *(float4*)(lds + k * G128_LDM + cq) = v[h];
+    }
+}
+// operand values of instruction q for the 16-row tile starting at row t0 of the tile
+template <bool KC>
+__device__ inline float g128_opnd(const float* lds, const f4& kcv, int t0, int q, int lane) {
+    if constexpr (KC) return kcv[q];
+    else return lds[((lane >> 4) * 4 + q) * G128_LDM + t0 + (lane & 15)];
+}
+
+template <bool A_KC, bool B_KC, int EPI>
+__global__ __launch_bounds__(256) void gemm128_kernel(GemmArgs g) {
+    constexpr int BK = 16, TL = G128_TL;
+    __shared__ __attribute__((aligned(16))) float As[2 * TL];
+    __shared__ __attribute__((aligned(16))) float Bs[2 * TL];
+    __shared__ float rowsum[128];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int zz = blockIdx.z / g.ksplit, slice = blockIdx.z % g.ksplit;
+    int cn, valid;
+    int64_t r0;
+    gemm_zinfo(g, zz, cn, r0, valid);
+    const int Mv = (g.sample_dims & 1) ? valid : g.M;
+    const int Nv = (g.sample_dims & 2) ? valid : g.N;
+    const int Kv = (g.sample_dims & 4) ? valid : g.Kd;
+    const int m0 = blockIdx.y * 128, n0 = blockIdx.x * 128;
+    if (m0 >= Mv || n0 >= Nv) return;
+    const int kbeg = slice * g.kchunk;
+    const int kend = min(Kv, kbeg + g.kchunk);
+    const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
+    const bool do_rowsum = (EPI == EPI_UPD) && g.ubias != nullptr && blockIdx.x == 0;
+    if (do_rowsum && tid < 128) rowsum[tid] = 0.f;
+
+    f4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    float4 ra[2], rb[2];
+    auto load = [&](int k0) {
+        if constexpr (A_KC) load_kc128(ra, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+        else load_nc128(ra, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+        if constexpr (B_KC) load_kc128(rb, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+        else load_nc128(rb, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+    };
+    auto store = [&](int buf) {
+        if constexpr (A_KC) store_kc128(As + buf * TL, ra, tid);
+        else store_nc128(As + buf * TL, ra, tid);
+        if constexpr (B_KC) store_kc128(Bs + buf * TL, rb, tid);
+        else store_nc128(Bs + buf * TL, rb, tid);
+    };
+    if (kbeg < kend) {
+        load(kbeg);
+        store(0);
+    }
+    __syncthreads();
+    int buf = 0;
+    const int rl = lane & 15, kg = lane >> 4;
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+        const bool more = k0 + BK < kend;
+        if (more) load(k0 + BK);
+        const float* A = As + buf * TL;
+        const float* Bt = Bs + buf * TL;
+        if (do_rowsum && tid < 128) {
+            float sr = 0.f;
+#pragma unroll
+            for (int k = 0; k < BK; ++k) sr += A_KC ? A[tid * G128_LDK + k] : A[k * G128_LDM + tid];
+            rowsum[tid] += sr;
+        }
+        f4 av[4], bv[4];
+        if constexpr (A_KC)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) av[i] = *(const f4*)(A + (wm * 64 + i * 16 + rl) * G128_LDK + kg * 4);
+        if constexpr (B_KC)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bv[j] = *(const f4*)(Bt + (wn * 64 + j * 16 + rl) * G128_LDK + kg * 4);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            float aq[4], bq[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) aq[i] = g128_opnd<A_KC>(A, av[i], wm * 64 + i * 16, q, lane);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bq[j] = g128_opnd<B_KC>(Bt, bv[j], wn * 64 + j * 16, q, lane);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[i], bq[j], acc[i][j], 0, 0, 0);
+        }
+        if (more) store(buf ^ 1);
+        __syncthreads();
+        buf ^= 1;
+    }
+
+    float scale = g.lr;
+    if (EPI == EPI_UPD && g.scale_per_batch) scale = valid > 0 ? g.lr / (float)valid : 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
+                const int n = n0 + wn * 64 + j * 16 + (lane & 15);
+                if (m >= Mv || n >= Nv) continue;
+                const float v = acc[i][j][r];
+                const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+                if constexpr (EPI == EPI_STORE) {
+                    ((float*)g.c)[ci + (size_t)slice * g.c_split] = v;
+                } else if constexpr (EPI == EPI_FWD) {
+                    const float zv = v + g.bias[(size_t)cn * g.bias_z + n];
+                    ((float*)g.c)[ci] = act_fn(g.act, zv);
+                } else if constexpr (EPI == EPI_BWD) {
+                    const float x = ((const float*)g.aux)[ci];
+                    ((float*)g.c)[ci] = v * act_deriv(g.act, x);
+                } else {  // EPI_UPD: in-place W -= scale * acc
+                    float* W = (float*)g.c;
+                    W[ci] = W[ci] - scale * v;
+                }
+            }
+    if (do_rowsum && tid < 128 && m0 + tid < Mv) {
+        float* b = g.ubias + (size_t)cn * g.bias_z;
+        b[m0 + tid] -= scale * rowsum[tid];
+    }
+}
+
+// ------------------------------------------------------------------------------------
 // Output layer, one wavefront per sample row: z = W x + b over <= 16 outputs, the output
 // activation (eq. (3), softmax eq. (5)), then either the output error (training, eq. (9)
 // or (10)) or the predicted class and the correct count (inference).

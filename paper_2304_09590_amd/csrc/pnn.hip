@@ -254,6 +254,17 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
     dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, (unsigned)(Z * g.ksplit));
     if (grid.x == 0 || grid.y == 0 || grid.z == 0 || grid.y > 65535 || grid.z > 65535)
         return fail(n, PNN_EINVAL, "%s: bad grid %u x %u x %u", name, grid.x, grid.y, grid.z);
+    if constexpr (!BF) {
+        // large fp32 shapes with both operands along k (forward, inference): 128 x 128 tiles.
+        // (The weight update, short contraction and a read-modify-write epilogue, keeps the
+        // 64 x 64 tiles: more workgroups in flight to cover its epilogue.)
+        if (A_KC && B_KC && g.M >= 128 && g.N >= 128 && g.shadow == nullptr) {
+            dim3 g128((g.N + 127) / 128, (g.M + 127) / 128, (unsigned)(Z * g.ksplit));
+            Launch l(n, s, name);
+            gemm128_kernel<A_KC, B_KC, EPI><<<g128, 256, 0, s>>>(g);
+            return l.done();
+        }
+    }
     Launch l(n, s, name);
     gemm_kernel<BF, TA, TB, A_KC, B_KC, EPI, TO><<<grid, 256, 0, s>>>(g);
     return l.done();
