@@ -692,6 +692,193 @@ __global__ __launch_bounds__(256) void upd_small_kernel(UpdSmallArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
+// The narrow last layer of a mini-batch step, fused, one workgroup per CN (eq. (3)-(5),
+// (9)-(13) for a last layer of <= 16 neurons behind a hidden layer of H neurons):
+//   phase 1: z = W x + b, the output activation and the output error delta for every row
+//            of the step (each wave sums a quarter of the H inputs for 64 rows, one row per
+//            lane; W staged in LDS once);
+//   phase 2: per column i (4 per thread), over the rows: the hidden error
+//            d[r][i] = (sum_o delta[r][o] W[o][i]) phi'(x[r][i]) with the pre-update W, and
+//            the update sums sum_r delta[r][o] x[r][i]; then W -= lr / B_t * sums and
+//            b -= lr / B_t * sum_r delta[r][o].
+// The same rounding points as the unfused kernels: the output error is rounded to the error
+// type before use, operands are the bf16 shadow in bf16-mixed mode, the update is applied
+// to the fp32 master and the shadow refreshed.
+
+struct TailArgs {
+    const void* x;      // last hidden activations [z][rows][H] (TH)
+    int64_t x_z;
+    const void* wop;    // W_L operand [O][H] (+ z * w_z): fp32 master or bf16 shadow
+    float* w;           // W_L fp32 master [O][H] (+ z * w_z)
+    bf16_t* shadow;     // bf16 shadow of W_L (+ z * w_z), nullable
+    float* bias;        // b_L [O] (+ z * bias_z)
+    int64_t w_z, bias_z;
+    void* d;            // hidden errors [z][rows][H] (TH)
+    int H, O, act_out, act_hid, loss;
+    float lr;
+    int64_t n_total;
+    int k_rep;
+    int64_t r0;
+    int step_rows;
+    const int32_t* y;   // labels (data-set rows)
+};
+
+template <typename TH>
+__device__ inline float4 load4(const TH* p) {
+    if constexpr (sizeof(TH) == 4) return *(const float4*)p;
+    else {
+        const uint2 q = *(const uint2*)p;
+        return make_float4(bf2f((bf16_t)(q.x & 0xffff)), bf2f((bf16_t)(q.x >> 16)), bf2f((bf16_t)(q.y & 0xffff)),
+                           bf2f((bf16_t)(q.y >> 16)));
+    }
+}
+template <typename TH>
+__device__ inline void store4(TH* p, float4 v) {
+    if constexpr (sizeof(TH) == 4) *(float4*)p = v;
+    else {
+        uint2 q;
+        q.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+        q.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+        *(uint2*)p = q;
+    }
+}
+
+template <typename TH>
+__global__ __launch_bounds__(256) void tail_kernel(TailArgs a) {
+    extern __shared__ __attribute__((aligned(16))) float tsm[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int z = blockIdx.x;
+    const int H = a.H, O = a.O;
+    int64_t v = shard_len(a.n_total, a.k_rep, z) - a.r0;
+    const int valid = (int)(v < 0 ? 0 : (v > a.step_rows ? a.step_rows : v));
+    if (valid == 0) return;
+    float* Ws = tsm;                           // [MAX_OUT][H] operand weights (fp32 values)
+    float* dl = Ws + MAX_OUT * H;              // [rows][MAX_OUT] output errors (rounded)
+    float* part = dl + a.step_rows * MAX_OUT;  // [4][64][MAX_OUT] partial sums
+    const TH* wop = (const TH*)a.wop + (size_t)z * a.w_z;
+    for (int e = tid; e < MAX_OUT * H; e += 256) {
+        const int o = e / H;
+        Ws[e] = o < O ? to_f<TH>(wop[e]) : 0.f;
+    }
+    __syncthreads();
+    const TH* x = (const TH*)a.x + (size_t)z * a.x_z;
+    const float* b = a.bias + (size_t)z * a.bias_z;
+    const int64_t drow0 = shard_start(a.n_total, a.k_rep, z) + a.r0;
+
+    // ---- phase 1: rows in passes of 64, one row per lane, a quarter of the inputs per wave
+    const int hq = H / 4, c0 = wave * hq;
+    for (int p0 = 0; p0 < valid; p0 += 64) {
+        const int r = p0 + lane;
+        float acc[MAX_OUT];
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) acc[o] = 0.f;
+        if (r < valid) {
+            const TH* xr = x + (size_t)r * H;
+            for (int i = c0; i < c0 + hq; i += 4) {
+                const float4 xv = load4(xr + i);
+#pragma unroll
+                for (int o = 0; o < MAX_OUT; ++o) {
+                    if (o < O) {
+                        const float4 w = *(const float4*)(Ws + o * H + i);
+                        acc[o] += w.x * xv.x + w.y * xv.y + w.z * xv.z + w.w * xv.w;
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int o = 0; o < MAX_OUT; ++o) part[(wave * 64 + lane) * MAX_OUT + o] = acc[o];
+        __syncthreads();
+        if (wave == 0 && r < valid) {
+            float zo[MAX_OUT], xo[MAX_OUT];
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) {
+                float sacc = 0.f;
+#pragma unroll
+                for (int w4 = 0; w4 < 4; ++w4) sacc += part[(w4 * 64 + lane) * MAX_OUT + o];
+                zo[o] = (o < O) ? sacc + b[o] : 0.f;
+            }
+            if (a.act_out == ACT_SOFTMAX) {
+                float m = zo[0];
+#pragma unroll
+                for (int o = 1; o < MAX_OUT; ++o) if (o < O) m = fmaxf(m, zo[o]);
+                float sm = 0.f;
+#pragma unroll
+                for (int o = 0; o < MAX_OUT; ++o) { xo[o] = (o < O) ? expf(zo[o] - m) : 0.f; sm += xo[o]; }
+                const float inv = 1.0f / sm;
+#pragma unroll
+                for (int o = 0; o < MAX_OUT; ++o) xo[o] *= inv;
+            } else {
+#pragma unroll
+                for (int o = 0; o < MAX_OUT; ++o) xo[o] = act_fn(a.act_out, zo[o]);
+            }
+            const int label = a.y[drow0 + r];
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) {
+                const float e = (o == label) ? 1.0f : 0.0f;
+                const float dv = (a.loss == LOSS_XENT) ? (xo[o] - e) : (xo[o] - e) * act_deriv(a.act_out, xo[o]);
+                dl[r * MAX_OUT + o] = (o < O) ? to_f<TH>(from_f<TH>(dv)) : 0.f;
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- phase 2: four columns per thread, over the rows
+    const float scale = a.lr / (float)valid;
+    TH* d = (TH*)a.d + (size_t)z * a.x_z;
+    float* wm = a.w + (size_t)z * a.w_z;
+    for (int cb = 0; cb < H; cb += 1024) {
+        const int i = cb + tid * 4;
+        if (i < H) {
+            float4 wf[MAX_OUT], dw[MAX_OUT];
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) {
+                wf[o] = *(const float4*)(Ws + o * H + i);
+                dw[o] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            for (int r = 0; r < valid; ++r) {
+                const float4 xv = load4(x + (size_t)r * H + i);
+                float4 sv = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                for (int o4 = 0; o4 < MAX_OUT; o4 += 4) {
+                    if (o4 < O) {
+                        const float4 dv = *(const float4*)(dl + r * MAX_OUT + o4);
+                        const float dd[4] = {dv.x, dv.y, dv.z, dv.w};
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            const int o = o4 + u;
+                            sv.x += dd[u] * wf[o].x; sv.y += dd[u] * wf[o].y;
+                            sv.z += dd[u] * wf[o].z; sv.w += dd[u] * wf[o].w;
+                            dw[o].x += dd[u] * xv.x; dw[o].y += dd[u] * xv.y;
+                            dw[o].z += dd[u] * xv.z; dw[o].w += dd[u] * xv.w;
+                        }
+                    }
+                }
+                float4 dh;
+                dh.x = sv.x * act_deriv(a.act_hid, xv.x);
+                dh.y = sv.y * act_deriv(a.act_hid, xv.y);
+                dh.z = sv.z * act_deriv(a.act_hid, xv.z);
+                dh.w = sv.w * act_deriv(a.act_hid, xv.w);
+                store4(d + (size_t)r * H + i, dh);
+            }
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) {
+                if (o < O) {
+                    float4 w = *(const float4*)(wm + (size_t)o * H + i);
+                    w.x -= scale * dw[o].x; w.y -= scale * dw[o].y; w.z -= scale * dw[o].z; w.w -= scale * dw[o].w;
+                    *(float4*)(wm + (size_t)o * H + i) = w;
+                    if (a.shadow) store4(a.shadow + (size_t)z * a.w_z + (size_t)o * H + i, w);
+                }
+            }
+        }
+    }
+    if (tid < O) {
+        float sb = 0.f;
+        for (int r = 0; r < valid; ++r) sb += dl[r * MAX_OUT + tid];
+        a.bias[(size_t)z * a.bias_z + tid] -= scale * sb;
+    }
+}
+
+// ------------------------------------------------------------------------------------
 // Combination by averaging: merged[p] = (sum_k theta_k[p]) / K with the sum in fp64 and k
 // ascending; optionally broadcast back to every CN; bf16 shadows refreshed.  Four
 // consecutive parameters per thread.

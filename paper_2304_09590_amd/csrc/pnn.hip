@@ -301,8 +301,31 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
         if (l == 1) TRY((run_gemm<BF, float, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
         else TRY((run_gemm<BF, TH, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
     }
+    // a narrow last layer behind a hidden layer: forward, output error, the hidden error
+    // behind it and its update in one kernel per CN
+    const int Hl = L >= 2 ? n->sizes[L - 1] : 0;
+    const size_t tail_smem = (size_t)(MAX_OUT * Hl + B * MAX_OUT + 4 * 64 * MAX_OUT) * sizeof(float);
+    const bool fuse_tail = L >= 2 && n->sizes[L] <= MAX_OUT && Hl % 16 == 0 && tail_smem <= 160 * 1024;
+    if (fuse_tail) {
+        TailArgs a;
+        memset(&a, 0, sizeof a);
+        a.x = n->act_ws[L - 1]; a.x_z = (int64_t)B * Hl;
+        a.wop = (const char*)Wop + n->off_w[L - 1] * (BF ? 2 : 4);
+        a.w = n->theta + n->off_w[L - 1];
+        a.shadow = BF ? n->shadow + n->off_w[L - 1] : nullptr;
+        a.bias = n->theta + n->off_b[L - 1];
+        a.w_z = ps; a.bias_z = ps;
+        a.d = n->del_ws[L - 1];
+        a.H = Hl; a.O = n->sizes[L]; a.act_out = n->act[L - 1]; a.act_hid = n->act[L - 2]; a.loss = n->cfg.loss;
+        a.lr = n->cfg.lr;
+        a.n_total = N; a.k_rep = K; a.r0 = r0; a.step_rows = B;
+        a.y = Y;
+        Launch lc(n, s, "tail");
+        tail_kernel<TH><<<dim3(K), 256, tail_smem, s>>>(a);
+        TRY(lc.done());
+    }
     // output layer and output error (eq. (3), (5), (9)-(10))
-    {
+    if (!fuse_tail) {
         RowArgs a;
         memset(&a, 0, sizeof a);
         if (L == 1) { a.x = X; a.x_xrows = 1; a.x_ld = n->sizes[0]; }
@@ -321,6 +344,7 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
     }
     // hidden errors, back to front, with the pre-update weights (eq. (11))
     for (int l = L - 1; l >= 1; --l) {
+        if (fuse_tail && l == L - 1) continue;  // (in the fused last layer)
         const int Hl = n->sizes[l], On = n->sizes[l + 1];
         if (On <= MAX_OUT) {
             BwdSmallArgs a;
@@ -346,6 +370,7 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
     }
     // updates, eq. (12)-(13) averaged over the batch
     for (int l = 1; l <= L; ++l) {
+        if (fuse_tail && l == L) continue;  // (in the fused last layer)
         const int In = n->sizes[l - 1], Out = n->sizes[l];
         if (Out <= MAX_OUT) {
             UpdSmallArgs a;
@@ -717,6 +742,12 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
             if (l < n->L && (st = dev_alloc(n, (char**)&n->act_ws[l], cnt)) != PNN_OK) return bail(st);
             if ((st = dev_alloc(n, (char**)&n->del_ws[l], cnt)) != PNN_OK) return bail(st);
         }
+        // the fused last layer may stage up to 160 KiB of LDS
+        hipError_t e = n->bf16 ? hipFuncSetAttribute((const void*)tail_kernel<bf16_t>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024)
+                               : hipFuncSetAttribute((const void*)tail_kernel<float>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return bail(fail(n, PNN_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e)));
     }
     // clone theta0 into every CN and the merged network
     std::vector<float> padded(n->pstride);
