@@ -756,9 +756,13 @@ __global__ __launch_bounds__(256) void tail_kernel(TailArgs a) {
     float* dl = Ws + MAX_OUT * H;              // [rows][MAX_OUT] output errors (rounded)
     float* part = dl + a.step_rows * MAX_OUT;  // [4][64][MAX_OUT] partial sums
     const TH* wop = (const TH*)a.wop + (size_t)z * a.w_z;
-    for (int e = tid; e < MAX_OUT * H; e += 256) {
-        const int o = e / H;
-        Ws[e] = o < O ? to_f<TH>(wop[e]) : 0.f;
+    {
+        // W_L is [O][H] contiguous: copy it 4 values at a time, several loads in flight;
+        // rows O .. MAX_OUT-1 are zero
+        const int n4 = O * H / 4, z4 = MAX_OUT * H / 4;
+#pragma unroll 4
+        for (int e = tid; e < n4; e += 256) *(float4*)(Ws + 4 * e) = load4(wop + 4 * e);
+        for (int e = n4 + tid; e < z4; e += 256) *(float4*)(Ws + 4 * e) = make_float4(0.f, 0.f, 0.f, 0.f);
     }
     __syncthreads();
     const TH* x = (const TH*)a.x + (size_t)z * a.x_z;
@@ -774,8 +778,11 @@ __global__ __launch_bounds__(256) void tail_kernel(TailArgs a) {
         for (int o = 0; o < MAX_OUT; ++o) acc[o] = 0.f;
         if (r < valid) {
             const TH* xr = x + (size_t)r * H;
+            // the row's next four values are loaded while the current ones are used
+            float4 xn = load4(xr + c0);
             for (int i = c0; i < c0 + hq; i += 4) {
-                const float4 xv = load4(xr + i);
+                const float4 xv = xn;
+                if (i + 4 < c0 + hq) xn = load4(xr + i + 4);
 #pragma unroll
                 for (int o = 0; o < MAX_OUT; ++o) {
                     if (o < O) {
@@ -835,8 +842,10 @@ __global__ __launch_bounds__(256) void tail_kernel(TailArgs a) {
                 wf[o] = *(const float4*)(Ws + o * H + i);
                 dw[o] = make_float4(0.f, 0.f, 0.f, 0.f);
             }
+            float4 xn = load4(x + i);  // (row 0; the next row's values load during each row)
             for (int r = 0; r < valid; ++r) {
-                const float4 xv = load4(x + (size_t)r * H + i);
+                const float4 xv = xn;
+                if (r + 1 < valid) xn = load4(x + (size_t)(r + 1) * H + i);
                 float4 sv = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
                 for (int o4 = 0; o4 < MAX_OUT; o4 += 4) {
