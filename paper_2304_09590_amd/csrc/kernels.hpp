@@ -692,6 +692,37 @@ __global__ __launch_bounds__(256) void upd_small_kernel(UpdSmallArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
+// Forward layer split along the contraction (few, long-contraction tiles): the partial
+// products of the ksplit slices are summed here, then the bias and the activation
+// (eq. (2)-(3)):  out[z][r][c] = phi(sum_s part[s][z][r][c] + b[c]).  Thread per (r, c).
+
+struct FwdReduceArgs {
+    const float* part;  // [ksplit][K][rows][N]
+    int64_t split;      // K * rows * N
+    int ksplit;
+    float* out;         // [K][rows][N]
+    const float* bias;  // b (+ z * bias_z)
+    int64_t bias_z;
+    int N, act;
+    int64_t n_total;
+    int k_rep;
+    int64_t r0;
+    int step_rows;
+};
+
+__global__ __launch_bounds__(256) void fwd_reduce_kernel(FwdReduceArgs a) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int r = blockIdx.y, z = blockIdx.z;
+    int64_t v = shard_len(a.n_total, a.k_rep, z) - a.r0;
+    const int valid = (int)(v < 0 ? 0 : (v > a.step_rows ? a.step_rows : v));
+    if (r >= valid || c >= a.N) return;
+    const size_t e = ((size_t)z * a.step_rows + r) * a.N + c;
+    float sum = 0.f;
+    for (int sl = 0; sl < a.ksplit; ++sl) sum += a.part[(size_t)sl * a.split + e];
+    a.out[e] = act_fn(a.act, sum + a.bias[(size_t)z * a.bias_z + c]);
+}
+
+// ------------------------------------------------------------------------------------
 // The narrow last layer of a mini-batch step, fused, one workgroup per CN (eq. (3)-(5),
 // (9)-(13) for a last layer of <= 16 neurons behind a hidden layer of H neurons):
 //   phase 1: z = W x + b, the output activation and the output error delta for every row

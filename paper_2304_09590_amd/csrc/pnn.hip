@@ -298,6 +298,23 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
         g.c = n->act_ws[l]; g.c_z = (int64_t)B * n->sizes[l]; g.c_ld = n->sizes[l];
         g.bias = n->theta + n->off_b[l - 1]; g.bias_z = ps;
         g.act = n->act[l - 1];
+        if (!BF && l == 1 && n->ksplit > 1) {
+            // few tiles with a long contraction: split it, then sum, bias and activation
+            g.c = n->ppart; g.ksplit = n->ksplit; g.kchunk = n->kchunk;
+            g.c_split = (int64_t)K * B * n->sizes[1];
+            TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K, "fwd_gemm")));
+            FwdReduceArgs ra;
+            memset(&ra, 0, sizeof ra);
+            ra.part = n->ppart; ra.split = g.c_split; ra.ksplit = n->ksplit;
+            ra.out = (float*)n->act_ws[1];
+            ra.bias = n->theta + n->off_b[0]; ra.bias_z = ps;
+            ra.N = n->sizes[1]; ra.act = n->act[0];
+            ra.n_total = N; ra.k_rep = K; ra.r0 = r0; ra.step_rows = B;
+            Launch lr(n, s, "fwd_reduce");
+            fwd_reduce_kernel<<<dim3((n->sizes[1] + 255) / 256, B, K), 256, 0, s>>>(ra);
+            TRY(lr.done());
+            continue;
+        }
         if (l == 1) TRY((run_gemm<BF, float, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
         else TRY((run_gemm<BF, TH, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
     }
@@ -741,6 +758,17 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
             const size_t cnt = (size_t)K * B * n->sizes[l] * el;
             if (l < n->L && (st = dev_alloc(n, (char**)&n->act_ws[l], cnt)) != PNN_OK) return bail(st);
             if ((st = dev_alloc(n, (char**)&n->del_ws[l], cnt)) != PNN_OK) return bail(st);
+        }
+        // fp32, first layer with few output tiles (less than one workgroup per CU) and the
+        // 784-long contraction: split the contraction into slices of 112
+        if (!n->bf16 && n->L >= 2) {
+            const int N1 = n->sizes[1], In = n->sizes[0];
+            const int64_t wgs = (int64_t)((N1 + 63) / 64) * ((B + 63) / 64) * K;
+            if (!(B >= 128 && N1 >= 128) && wgs < 256 && In >= 256) {
+                n->kchunk = (int)round_up((In + 7) / 8, 16);
+                n->ksplit = (In + n->kchunk - 1) / n->kchunk;
+                if ((st = dev_alloc(n, &n->ppart, (size_t)n->ksplit * K * B * N1)) != PNN_OK) return bail(st);
+            }
         }
         // the fused last layer may stage up to 160 KiB of LDS
         hipError_t e = n->bf16 ? hipFuncSetAttribute((const void*)tail_kernel<bf16_t>,
