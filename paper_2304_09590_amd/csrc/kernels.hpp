@@ -860,23 +860,31 @@ __global__ __launch_bounds__(256) void tail_kernel(TailArgs a) {
         __syncthreads();
     }
 
-    // ---- phase 2: four columns per thread, over the rows
+    // ---- phase 2: four columns per thread, over the rows; when the columns do not fill the
+    // workgroup, rsplit threads share a column group, each taking every rsplit-th row, and
+    // their update sums are added in a fixed order through LDS
     const float scale = a.lr / (float)valid;
     TH* d = (TH*)a.d + (size_t)z * a.x_z;
     float* wm = a.w + (size_t)z * a.w_z;
+    const int ng = H / 4;
+    const int rsplit = ng >= 256 ? 1 : 256 / ng;
+    float* red = part + 4 * 64 * MAX_OUT;  // [rsplit][MAX_OUT][H] (rsplit > 1)
     for (int cb = 0; cb < H; cb += 1024) {
-        const int i = cb + tid * 4;
-        if (i < H) {
-            float4 wf[MAX_OUT], dw[MAX_OUT];
+        const int cg = rsplit > 1 ? tid % ng : tid, rg = rsplit > 1 ? tid / ng : 0;
+        const int i = cb + cg * 4;
+        const bool on = i < H && rg < rsplit;
+        float4 dw[MAX_OUT];
 #pragma unroll
-            for (int o = 0; o < MAX_OUT; ++o) {
-                wf[o] = *(const float4*)(Ws + o * H + i);
-                dw[o] = make_float4(0.f, 0.f, 0.f, 0.f);
-            }
-            float4 xn = load4(x + i);  // (row 0; the next row's values load during each row)
-            for (int r = 0; r < valid; ++r) {
+        for (int o = 0; o < MAX_OUT; ++o) dw[o] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (on) {
+            float4 wf[MAX_OUT];
+#pragma unroll
+            for (int o = 0; o < MAX_OUT; ++o) wf[o] = *(const float4*)(Ws + o * H + i);
+            float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (rg < valid) xn = load4(x + (size_t)rg * H + i);  // (the next row loads during each row)
+            for (int r = rg; r < valid; r += rsplit) {
                 const float4 xv = xn;
-                if (r + 1 < valid) xn = load4(x + (size_t)(r + 1) * H + i);
+                if (r + rsplit < valid) xn = load4(x + (size_t)(r + rsplit) * H + i);
                 float4 sv = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
                 for (int o4 = 0; o4 < MAX_OUT; o4 += 4) {
@@ -900,6 +908,23 @@ __global__ __launch_bounds__(256) void tail_kernel(TailArgs a) {
                 dh.w = sv.w * act_deriv(a.act_hid, xv.w);
                 store4(d + (size_t)r * H + i, dh);
             }
+        }
+        if (rsplit > 1) {
+            if (on)
+#pragma unroll
+                for (int o = 0; o < MAX_OUT; ++o)
+                    if (o < O) *(float4*)(red + (size_t)(rg * MAX_OUT + o) * H + i) = dw[o];
+            __syncthreads();
+            if (on && rg == 0)
+                for (int g2 = 1; g2 < rsplit; ++g2)
+#pragma unroll
+                    for (int o = 0; o < MAX_OUT; ++o)
+                        if (o < O) {
+                            const float4 q = *(const float4*)(red + (size_t)(g2 * MAX_OUT + o) * H + i);
+                            dw[o].x += q.x; dw[o].y += q.y; dw[o].z += q.z; dw[o].w += q.w;
+                        }
+        }
+        if (on && rg == 0) {
 #pragma unroll
             for (int o = 0; o < MAX_OUT; ++o) {
                 if (o < O) {

@@ -321,7 +321,11 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
     // a narrow last layer behind a hidden layer: forward, output error, the hidden error
     // behind it and its update in one kernel per CN
     const int Hl = L >= 2 ? n->sizes[L - 1] : 0;
-    const size_t tail_smem = (size_t)(MAX_OUT * Hl + B * MAX_OUT + 4 * 64 * MAX_OUT) * sizeof(float);
+    // operand weights, output errors, partial sums, and (fewer than 1024 columns) the row-split
+    // update sums [256 / (H/4)][MAX_OUT][H]
+    const size_t tail_smem =
+        (size_t)(MAX_OUT * Hl + B * MAX_OUT + 4 * 64 * MAX_OUT + (Hl > 0 && Hl < 1024 ? (256 / (Hl / 4)) * MAX_OUT * Hl : 0)) *
+        sizeof(float);
     const bool fuse_tail = L >= 2 && n->sizes[L] <= MAX_OUT && Hl % 16 == 0 && tail_smem <= 160 * 1024;
     if (fuse_tail) {
         TailArgs a;
