@@ -723,18 +723,22 @@ __global__ __launch_bounds__(256) void fwd_reduce_kernel(FwdReduceArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
-// The narrow last layer of a mini-batch step, fused, one workgroup per CN (eq. (3)-(5),
-// (9)-(13) for a last layer of <= 16 neurons behind a hidden layer of H neurons):
-//   phase 1: z = W x + b, the output activation and the output error delta for every row
-//            of the step (each wave sums a quarter of the H inputs for 64 rows, one row per
-//            lane; W staged in LDS once);
-//   phase 2: per column i (4 per thread), over the rows: the hidden error
-//            d[r][i] = (sum_o delta[r][o] W[o][i]) phi'(x[r][i]) with the pre-update W, and
-//            the update sums sum_r delta[r][o] x[r][i]; then W -= lr / B_t * sums and
-//            b -= lr / B_t * sum_r delta[r][o].
-// The same rounding points as the unfused kernels: the output error is rounded to the error
-// type before use, operands are the bf16 shadow in bf16-mixed mode, the update is applied
-// to the fp32 master and the shadow refreshed.
+// The narrow last layer of a mini-batch step, fused, one workgroup of 16 waves per CN
+// (eq. (3)-(5), (9)-(13) for a last layer of O <= 16 neurons behind a hidden layer of H
+// neurons).  The step's rows are taken in groups of RG rows; each group is loaded once,
+// coalesced, into LDS (the next group's loads in flight while the current one is used), and
+// three contractions run on v_mfma_f32_16x16x4_f32 with the outputs padded to 16:
+//   Z  = X W^T      (rows x 16, over H; each 16-row tile is split over H among several
+//                    waves, partial tiles summed in LDS in a fixed order), then the output
+//                    activation and the output error of each row, one lane per (row, output);
+//   S  = delta W    (rows x H, over the 16 outputs), hidden error d = S * phi'(x) (eq. (11),
+//                    with the pre-update W);
+//   dW += delta^T X (16 x H, over the group's rows; accumulators stay in registers across
+//                    groups, wave w owning the 16-column tiles w, w+16, ...).
+// At the end W -= lr / B_t * dW and b -= lr / B_t * sum_r delta (rows in order).  The same
+// rounding points as the unfused kernels: the output error is rounded to the error type
+// before use, operands are the bf16 shadow in bf16-mixed mode, the update is applied to the
+// fp32 master and the shadow refreshed.
 
 struct TailArgs {
     const void* x;      // last hidden activations [z][rows][H] (TH)
@@ -746,6 +750,7 @@ struct TailArgs {
     int64_t w_z, bias_z;
     void* d;            // hidden errors [z][rows][H] (TH)
     int H, O, act_out, act_hid, loss;
+    int rg;             // rows per group: a multiple of 16, rg * H <= TAIL_GROUP, rg <= 256
     float lr;
     int64_t n_total;
     int k_rep;
@@ -753,6 +758,18 @@ struct TailArgs {
     int step_rows;
     const int32_t* y;   // labels (data-set rows)
 };
+
+constexpr int TAIL_THREADS = 1024, TAIL_WAVES = TAIL_THREADS / 64;
+constexpr int TAIL_PF = 4;                                // 4-value loads per thread per group
+constexpr int TAIL_GROUP = TAIL_THREADS * 4 * TAIL_PF;    // values of one row group (rg * H)
+constexpr int TAIL_DLS = 20;                              // LDS row stride of the output errors
+constexpr int TAIL_PART = TAIL_WAVES * 16 * 16;           // partial Z tiles, one per wave
+
+// LDS floats of the fused last layer: W [16][H+4], a row group [rg][H+4], its output errors
+// [rg][20], its labels [rg] and the per-wave partial tiles of Z
+__host__ __device__ inline int64_t tail_lds_floats(int H, int rg) {
+    return (int64_t)(16 + rg) * (H + 4) + (int64_t)rg * (TAIL_DLS + 1) + TAIL_PART;
+}
 
 template <typename TH>
 __device__ inline float4 load4(const TH* p) {
@@ -763,184 +780,186 @@ __device__ inline float4 load4(const TH* p) {
                            bf2f((bf16_t)(q.y >> 16)));
     }
 }
-template <typename TH>
-__device__ inline void store4(TH* p, float4 v) {
-    if constexpr (sizeof(TH) == 4) *(float4*)p = v;
-    else {
-        uint2 q;
-        q.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
-        q.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
-        *(uint2*)p = q;
-    }
+// four values as loaded (converted only when the load has landed)
+template <typename TH> struct Raw4 { typedef float4 T; };
+template <> struct Raw4<bf16_t> { typedef uint2 T; };
+__device__ inline float4 raw_f4(float4 v) { return v; }
+__device__ inline float4 raw_f4(uint2 q) {
+    return make_float4(bf2f((bf16_t)(q.x & 0xffff)), bf2f((bf16_t)(q.x >> 16)), bf2f((bf16_t)(q.y & 0xffff)),
+                       bf2f((bf16_t)(q.y >> 16)));
 }
 
-template <typename TH>
-__global__ __launch_bounds__(256) void tail_kernel(TailArgs a) {
+// NCW: 16-column tiles per wave (>= H / 256)
+template <typename TH, int NCW>
+__global__ __launch_bounds__(TAIL_THREADS) void tail_kernel(TailArgs a) {
     extern __shared__ __attribute__((aligned(16))) float tsm[];
+    typedef typename Raw4<TH>::T R4;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rl = lane & 15, kg = lane >> 4;
     const int z = blockIdx.x;
-    const int H = a.H, O = a.O;
+    const int H = a.H, O = a.O, RG = a.rg, LDW = H + 4;
     int64_t v = shard_len(a.n_total, a.k_rep, z) - a.r0;
     const int valid = (int)(v < 0 ? 0 : (v > a.step_rows ? a.step_rows : v));
     if (valid == 0) return;
-    float* Ws = tsm;                           // [MAX_OUT][H] operand weights (fp32 values)
-    float* dl = Ws + MAX_OUT * H;              // [rows][MAX_OUT] output errors (rounded)
-    float* part = dl + a.step_rows * MAX_OUT;  // [4][64][MAX_OUT] partial sums
-    const TH* wop = (const TH*)a.wop + (size_t)z * a.w_z;
+    float* Ws = tsm;                       // [16][LDW] operand weights (fp32 values), rows >= O zero
+    float* xs = Ws + 16 * LDW;             // [RG][LDW] the row group, rows past the data zero
+    float* dl = xs + RG * LDW;             // [RG][TAIL_DLS] output errors (rounded), zero padded
+    int* yl = (int*)(dl + RG * TAIL_DLS);  // [RG] labels of the group
+    float* part = (float*)(yl + RG);       // [k-part][rows][16] partial sums of Z
+    const int h4 = H / 4, nct = H / 16;
     {
-        // W_L is [O][H] contiguous: copy it 4 values at a time, several loads in flight;
-        // rows O .. MAX_OUT-1 are zero
-        const int n4 = O * H / 4, z4 = MAX_OUT * H / 4;
+        const TH* wop = (const TH*)a.wop + (size_t)z * a.w_z;
 #pragma unroll 4
-        for (int e = tid; e < n4; e += 256) *(float4*)(Ws + 4 * e) = load4(wop + 4 * e);
-        for (int e = n4 + tid; e < z4; e += 256) *(float4*)(Ws + 4 * e) = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int e = tid; e < 16 * h4; e += TAIL_THREADS) {
+            const int o = e / h4, c = (e - o * h4) * 4;
+            *(float4*)(Ws + o * LDW + c) = o < O ? load4(wop + (size_t)o * H + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
-    __syncthreads();
     const TH* x = (const TH*)a.x + (size_t)z * a.x_z;
-    const float* b = a.bias + (size_t)z * a.bias_z;
-    const int64_t drow0 = shard_start(a.n_total, a.k_rep, z) + a.r0;
-
-    // ---- phase 1: rows in passes of 64, one row per lane, a quarter of the inputs per wave
-    const int hq = H / 4, c0 = wave * hq;
-    for (int p0 = 0; p0 < valid; p0 += 64) {
-        const int r = p0 + lane;
-        float acc[MAX_OUT];
-#pragma unroll
-        for (int o = 0; o < MAX_OUT; ++o) acc[o] = 0.f;
-        if (r < valid) {
-            const TH* xr = x + (size_t)r * H;
-            // the row's next four values are loaded while the current ones are used
-            float4 xn = load4(xr + c0);
-            for (int i = c0; i < c0 + hq; i += 4) {
-                const float4 xv = xn;
-                if (i + 4 < c0 + hq) xn = load4(xr + i + 4);
-#pragma unroll
-                for (int o = 0; o < MAX_OUT; ++o) {
-                    if (o < O) {
-                        const float4 w = *(const float4*)(Ws + o * H + i);
-                        acc[o] += w.x * xv.x + w.y * xv.y + w.z * xv.z + w.w * xv.w;
-                    }
-                }
-            }
-        }
-#pragma unroll
-        for (int o = 0; o < MAX_OUT; ++o) part[(wave * 64 + lane) * MAX_OUT + o] = acc[o];
-        __syncthreads();
-        if (wave == 0 && r < valid) {
-            float zo[MAX_OUT], xo[MAX_OUT];
-#pragma unroll
-            for (int o = 0; o < MAX_OUT; ++o) {
-                float sacc = 0.f;
-#pragma unroll
-                for (int w4 = 0; w4 < 4; ++w4) sacc += part[(w4 * 64 + lane) * MAX_OUT + o];
-                zo[o] = (o < O) ? sacc + b[o] : 0.f;
-            }
-            if (a.act_out == ACT_SOFTMAX) {
-                float m = zo[0];
-#pragma unroll
-                for (int o = 1; o < MAX_OUT; ++o) if (o < O) m = fmaxf(m, zo[o]);
-                float sm = 0.f;
-#pragma unroll
-                for (int o = 0; o < MAX_OUT; ++o) { xo[o] = (o < O) ? expf(zo[o] - m) : 0.f; sm += xo[o]; }
-                const float inv = 1.0f / sm;
-#pragma unroll
-                for (int o = 0; o < MAX_OUT; ++o) xo[o] *= inv;
-            } else {
-#pragma unroll
-                for (int o = 0; o < MAX_OUT; ++o) xo[o] = act_fn(a.act_out, zo[o]);
-            }
-            const int label = a.y[drow0 + r];
-#pragma unroll
-            for (int o = 0; o < MAX_OUT; ++o) {
-                const float e = (o == label) ? 1.0f : 0.0f;
-                const float dv = (a.loss == LOSS_XENT) ? (xo[o] - e) : (xo[o] - e) * act_deriv(a.act_out, xo[o]);
-                dl[r * MAX_OUT + o] = (o < O) ? to_f<TH>(from_f<TH>(dv)) : 0.f;
-            }
-        }
-        __syncthreads();
-    }
-
-    // ---- phase 2: four columns per thread, over the rows; when the columns do not fill the
-    // workgroup, rsplit threads share a column group, each taking every rsplit-th row, and
-    // their update sums are added in a fixed order through LDS
-    const float scale = a.lr / (float)valid;
     TH* d = (TH*)a.d + (size_t)z * a.x_z;
-    float* wm = a.w + (size_t)z * a.w_z;
-    const int ng = H / 4;
-    const int rsplit = ng >= 256 ? 1 : 256 / ng;
-    float* red = part + 4 * 64 * MAX_OUT;  // [rsplit][MAX_OUT][H] (rsplit > 1)
-    for (int cb = 0; cb < H; cb += 1024) {
-        const int cg = rsplit > 1 ? tid % ng : tid, rg = rsplit > 1 ? tid / ng : 0;
-        const int i = cb + cg * 4;
-        const bool on = i < H && rg < rsplit;
-        float4 dw[MAX_OUT];
+    const int64_t drow0 = shard_start(a.n_total, a.k_rep, z) + a.r0;
+    const int ngrp = (valid + RG - 1) / RG;
+    const int eo = tid & 15;  // output of this lane in the per-row work
+    const float bo = eo < O ? a.bias[(size_t)z * a.bias_z + eo] : 0.f;
+
+    R4 pf[TAIL_PF];
+    int ypf = 0;
+    auto load_group = [&](int g) {  // the group's rows are contiguous: value 4e is load e
+        const int rows = min(RG, valid - g * RG), n4 = rows * h4;
+        const TH* xg = x + (size_t)g * RG * H;
 #pragma unroll
-        for (int o = 0; o < MAX_OUT; ++o) dw[o] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (on) {
-            float4 wf[MAX_OUT];
+        for (int u = 0; u < TAIL_PF; ++u) {
+            const int e = tid + TAIL_THREADS * u;
+            if (e < n4) pf[u] = *(const R4*)(xg + (size_t)e * 4);
+        }
+        if (tid < rows) ypf = a.y[drow0 + g * RG + tid];
+    };
+    auto store_group = [&](int g) {
+        const int rows = min(RG, valid - g * RG), n4 = rows * h4;
 #pragma unroll
-            for (int o = 0; o < MAX_OUT; ++o) wf[o] = *(const float4*)(Ws + o * H + i);
-            float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (rg < valid) xn = load4(x + (size_t)rg * H + i);  // (the next row loads during each row)
-            for (int r = rg; r < valid; r += rsplit) {
-                const float4 xv = xn;
-                if (r + rsplit < valid) xn = load4(x + (size_t)(r + rsplit) * H + i);
-                float4 sv = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int u = 0; u < TAIL_PF; ++u) {
+            const int e = tid + TAIL_THREADS * u;
+            if (e < RG * h4) {
+                const int r = e / h4, c = (e - r * h4) * 4;
+                *(float4*)(xs + r * LDW + c) = e < n4 ? raw_f4(pf[u]) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+        if (tid < RG) yl[tid] = ypf;
+    };
+
+    f4 dacc[NCW];
 #pragma unroll
-                for (int o4 = 0; o4 < MAX_OUT; o4 += 4) {
-                    if (o4 < O) {
-                        const float4 dv = *(const float4*)(dl + r * MAX_OUT + o4);
-                        const float dd[4] = {dv.x, dv.y, dv.z, dv.w};
+    for (int j = 0; j < NCW; ++j) dacc[j] = f4{0.f, 0.f, 0.f, 0.f};
+    float sb = 0.f;  // bias sum of output tid (tid < O)
+    load_group(0);
+    for (int g = 0; g < ngrp; ++g) {
+        const int g0 = g * RG, rows = min(RG, valid - g0);
+        const int nt = (rows + 15) >> 4;
+        __syncthreads();  // (the previous group's readers are done; W staged)
+        store_group(g);
+        if (g + 1 < ngrp) load_group(g + 1);
+        __syncthreads();
+        // Z = X W^T: row tile t is split over H into KP parts (16-column tiles kp, kp+KP, ...)
+        const int KP = TAIL_WAVES / nt;
+        if (wave < KP * nt) {
+            const int t = wave / KP, kp = wave - t * KP;
+            f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+            for (int kt = kp; kt < nct; kt += KP) {
+                const f4 xv = *(const f4*)(xs + (t * 16 + rl) * LDW + kt * 16 + kg * 4);
+                const f4 wv = *(const f4*)(Ws + rl * LDW + kt * 16 + kg * 4);
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) {
-                            const int o = o4 + u;
-                            sv.x += dd[u] * wf[o].x; sv.y += dd[u] * wf[o].y;
-                            sv.z += dd[u] * wf[o].z; sv.w += dd[u] * wf[o].w;
-                            dw[o].x += dd[u] * xv.x; dw[o].y += dd[u] * xv.y;
-                            dw[o].z += dd[u] * xv.z; dw[o].w += dd[u] * xv.w;
-                        }
+                for (int q = 0; q < 4; ++q) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[q], wv[q], acc, 0, 0, 0);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) part[(kp * nt * 16 + t * 16 + kg * 4 + r) * 16 + rl] = acc[r];
+        }
+        __syncthreads();
+        // output activation and output error: lane (row, output) = (e / 16, e % 16)
+        for (int e = tid; e < RG * 16; e += TAIL_THREADS) {
+            const int r = e >> 4;
+            const bool live = r < rows && eo < O;
+            float zv = 0.f;
+            if (r < rows) {
+                float s = part[r * 16 + eo];
+                for (int kp = 1; kp < KP; ++kp) s += part[(kp * nt * 16 + r) * 16 + eo];
+                zv = s + bo;
+            }
+            float xo;
+            if (a.act_out == ACT_SOFTMAX) {
+                float m = live ? zv : -INFINITY;
+#pragma unroll
+                for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
+                const float ex = live ? expf(zv - m) : 0.f;
+                float sm = ex;
+#pragma unroll
+                for (int sh = 1; sh < 16; sh <<= 1) sm += __shfl_xor(sm, sh, 16);
+                xo = ex * (1.0f / sm);
+            } else {
+                xo = act_fn(a.act_out, zv);
+            }
+            float dv = 0.f;
+            if (live) {
+                const float t1 = (eo == yl[r]) ? 1.0f : 0.0f;
+                const float dd = (a.loss == LOSS_XENT) ? (xo - t1) : (xo - t1) * act_deriv(a.act_out, xo);
+                dv = to_f<TH>(from_f<TH>(dd));
+            }
+            dl[r * TAIL_DLS + eo] = dv;
+        }
+        __syncthreads();
+        if (tid < O)
+            for (int r = 0; r < rows; ++r) sb += dl[r * TAIL_DLS + tid];
+#pragma unroll
+        for (int j = 0; j < NCW; ++j) {
+            const int ct = wave + TAIL_WAVES * j;
+            __builtin_amdgcn_sched_barrier(0);  // (one tile at a time: keeps the live registers down)
+            if (ct < nct) {
+                const int col = ct * 16 + rl;
+                float wq[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) wq[q] = Ws[(kg * 4 + q) * LDW + col];
+                // S = delta W for the tile's columns, then the hidden errors
+                for (int t = 0; t < nt; ++t) {
+                    const f4 dv = *(const f4*)(dl + (t * 16 + rl) * TAIL_DLS + kg * 4);
+                    f4 s = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) s = __builtin_amdgcn_mfma_f32_16x16x4f32(dv[q], wq[q], s, 0, 0, 0);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int row = t * 16 + kg * 4 + r;
+                        if (row < rows)
+                            d[(size_t)(g0 + row) * H + col] = from_f<TH>(s[r] * act_deriv(a.act_hid, xs[row * LDW + col]));
                     }
                 }
-                float4 dh;
-                dh.x = sv.x * act_deriv(a.act_hid, xv.x);
-                dh.y = sv.y * act_deriv(a.act_hid, xv.y);
-                dh.z = sv.z * act_deriv(a.act_hid, xv.z);
-                dh.w = sv.w * act_deriv(a.act_hid, xv.w);
-                store4(d + (size_t)r * H + i, dh);
-            }
-        }
-        if (rsplit > 1) {
-            if (on)
-#pragma unroll
-                for (int o = 0; o < MAX_OUT; ++o)
-                    if (o < O) *(float4*)(red + (size_t)(rg * MAX_OUT + o) * H + i) = dw[o];
-            __syncthreads();
-            if (on && rg == 0)
-                for (int g2 = 1; g2 < rsplit; ++g2)
-#pragma unroll
-                    for (int o = 0; o < MAX_OUT; ++o)
-                        if (o < O) {
-                            const float4 q = *(const float4*)(red + (size_t)(g2 * MAX_OUT + o) * H + i);
-                            dw[o].x += q.x; dw[o].y += q.y; dw[o].z += q.z; dw[o].w += q.w;
-                        }
-        }
-        if (on && rg == 0) {
-#pragma unroll
-            for (int o = 0; o < MAX_OUT; ++o) {
-                if (o < O) {
-                    float4 w = *(const float4*)(wm + (size_t)o * H + i);
-                    w.x -= scale * dw[o].x; w.y -= scale * dw[o].y; w.z -= scale * dw[o].z; w.w -= scale * dw[o].w;
-                    *(float4*)(wm + (size_t)o * H + i) = w;
-                    if (a.shadow) store4(a.shadow + (size_t)z * a.w_z + (size_t)o * H + i, w);
+                // dW += delta^T X over the group's rows, four rows per instruction
+                for (int m = 0; m < rows; m += 4) {
+                    const int row = m + kg;
+                    dacc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(dl[row * TAIL_DLS + rl], xs[row * LDW + col], dacc[j], 0, 0, 0);
                 }
             }
         }
     }
-    if (tid < O) {
-        float sb = 0.f;
-        for (int r = 0; r < valid; ++r) sb += dl[r * MAX_OUT + tid];
-        a.bias[(size_t)z * a.bias_z + tid] -= scale * sb;
+    // the update: lane holds dW[4 kg + r][16 ct + rl]; in fp32 the staged operand weights are
+    // the master values
+    const float scale = a.lr / (float)valid;
+    float* wm = a.w + (size_t)z * a.w_z;
+    const bool staged_master = (const void*)wm == (const void*)((const TH*)a.wop + (size_t)z * a.w_z);
+#pragma unroll
+    for (int j = 0; j < NCW; ++j) {
+        const int ct = wave + TAIL_WAVES * j;
+        if (ct < nct) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int o = kg * 4 + r;
+                if (o < O) {
+                    const size_t i = (size_t)o * H + ct * 16 + rl;
+                    const float w = (staged_master ? Ws[o * LDW + ct * 16 + rl] : wm[i]) - scale * dacc[j][r];
+                    wm[i] = w;
+                    if (a.shadow) a.shadow[(size_t)z * a.w_z + i] = f2bf(w);
+                }
+            }
+        }
     }
+    if (tid < O) a.bias[(size_t)z * a.bias_z + tid] -= scale * sb;
 }
 
 // ------------------------------------------------------------------------------------

@@ -117,6 +117,16 @@ pnn_status fail(pnn_net* n, pnn_status s, const char* fmt, ...) {
 
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
+// rows per group of the fused last layer behind a hidden layer of H neurons at batch B: a
+// multiple of 16 covering the batch if it can, at most TAIL_GROUP / H and 256; 0 if the
+// layer does not fit (H not a multiple of 16, or above TAIL_GROUP / 16)
+int tail_rows(int H, int B) {
+    if (H <= 0 || H % 16 != 0) return 0;
+    const int cap = (int)std::min<int64_t>(TAIL_GROUP / H / 16 * 16, 256);
+    if (cap < 16) return 0;
+    return (int)std::min<int64_t>(round_up(B, 16), cap);
+}
+
 pnn_status check_config(const pnn_config* c, std::string* why) {
     auto bad = [&](const char* m) { if (why) *why = m; return PNN_EINVAL; };
     if (!c) return bad("config is NULL");
@@ -321,12 +331,9 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
     // a narrow last layer behind a hidden layer: forward, output error, the hidden error
     // behind it and its update in one kernel per CN
     const int Hl = L >= 2 ? n->sizes[L - 1] : 0;
-    // operand weights, output errors, partial sums, and (fewer than 1024 columns) the row-split
-    // update sums [256 / (H/4)][MAX_OUT][H]
-    const size_t tail_smem =
-        (size_t)(MAX_OUT * Hl + B * MAX_OUT + 4 * 64 * MAX_OUT + (Hl > 0 && Hl < 1024 ? (256 / (Hl / 4)) * MAX_OUT * Hl : 0)) *
-        sizeof(float);
-    const bool fuse_tail = L >= 2 && n->sizes[L] <= MAX_OUT && Hl % 16 == 0 && tail_smem <= 160 * 1024;
+    const int trg = tail_rows(Hl, B);
+    const size_t tail_smem = trg > 0 ? (size_t)tail_lds_floats(Hl, trg) * sizeof(float) : 0;
+    const bool fuse_tail = L >= 2 && n->sizes[L] <= MAX_OUT && trg > 0 && tail_smem <= 160 * 1024;
     if (fuse_tail) {
         TailArgs a;
         memset(&a, 0, sizeof a);
@@ -338,11 +345,14 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
         a.w_z = ps; a.bias_z = ps;
         a.d = n->del_ws[L - 1];
         a.H = Hl; a.O = n->sizes[L]; a.act_out = n->act[L - 1]; a.act_hid = n->act[L - 2]; a.loss = n->cfg.loss;
+        a.rg = trg;
         a.lr = n->cfg.lr;
         a.n_total = N; a.k_rep = K; a.r0 = r0; a.step_rows = B;
         a.y = Y;
         Launch lc(n, s, "tail");
-        tail_kernel<TH><<<dim3(K), 256, tail_smem, s>>>(a);
+        if (Hl <= 256) tail_kernel<TH, 1><<<dim3(K), TAIL_THREADS, tail_smem, s>>>(a);
+        else if (Hl <= 512) tail_kernel<TH, 2><<<dim3(K), TAIL_THREADS, tail_smem, s>>>(a);
+        else tail_kernel<TH, 4><<<dim3(K), TAIL_THREADS, tail_smem, s>>>(a);
         TRY(lc.done());
     }
     // output layer and output error (eq. (3), (5), (9)-(10))
@@ -775,11 +785,15 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
             }
         }
         // the fused last layer may stage up to 160 KiB of LDS
-        hipError_t e = n->bf16 ? hipFuncSetAttribute((const void*)tail_kernel<bf16_t>,
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024)
-                               : hipFuncSetAttribute((const void*)tail_kernel<float>,
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        if (e != hipSuccess) return bail(fail(n, PNN_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e)));
+        const void* tk[3] = {(const void*)tail_kernel<float, 1>, (const void*)tail_kernel<float, 2>,
+                             (const void*)tail_kernel<float, 4>};
+        const void* tkb[3] = {(const void*)tail_kernel<bf16_t, 1>, (const void*)tail_kernel<bf16_t, 2>,
+                              (const void*)tail_kernel<bf16_t, 4>};
+        for (int i = 0; i < 3; ++i) {
+            hipError_t e = hipFuncSetAttribute(n->bf16 ? tkb[i] : tk[i], hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               160 * 1024);
+            if (e != hipSuccess) return bail(fail(n, PNN_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e)));
+        }
     }
     // clone theta0 into every CN and the merged network
     std::vector<float> padded(n->pstride);
