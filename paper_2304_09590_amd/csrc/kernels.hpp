@@ -151,20 +151,13 @@ __device__ inline const char* operand_row(const Operand& o, int elem, int z, int
     return p + (size_t)(z * o.zstride + r * o.ld) * elem;
 }
 
-// Stage a BR x BK tile (rows r0t.., k k0..) of an operand whose rows are the tile's
-// non-contraction index ("KC" layout) into lds[row][k].
-template <bool BF, typename TS>
-__device__ inline void stage_kc(typename GemmTile<BF>::T* lds, const Operand& o, int z, int cn, int64_t xbase,
-                                int row0, int rows_valid, int k0, int k_valid, int tid) {
-    constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
-    if constexpr (!BF) {
-        // 64 rows x 16 k fp32: one float4 per thread
-        const int r = tid >> 2, kq = (tid & 3) * 4;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (row0 + r < rows_valid && k0 + kq < k_valid)
-            v = *(const float4*)(operand_row(o, 4, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 4);
-        *(float4*)(lds + r * LDK + kq) = v;
-    } else if constexpr (sizeof(TS) == 4) {
+// bf16 tiles: stage a 64 x 32 tile (rows row0.., k k0..) of an operand whose rows are the
+// tile's non-contraction index ("KC" layout) into lds[row][k].
+template <typename TS>
+__device__ inline void stage_kc(bf16_t* lds, const Operand& o, int z, int cn, int64_t xbase, int row0, int rows_valid,
+                                int k0, int k_valid, int tid) {
+    constexpr int LDK = GemmTile<true>::LDK;
+    if constexpr (sizeof(TS) == 4) {
         // 64 rows x 32 k from fp32: two float4 per thread, converted
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -183,15 +176,19 @@ __device__ inline void stage_kc(typename GemmTile<BF>::T* lds, const Operand& o,
             v = *(const uint4*)(operand_row(o, 2, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 2);
         *(uint4*)(lds + r * LDK + kq) = v;
     }
-    (void)BK;
 }
 
-// Stage a tile from an operand whose rows are the contraction index ("NC" layout):
-// element (t, k) = row k, column t; stored transposed into lds[t][k].
-template <bool BF, typename TS>
-__device__ inline void stage_nc(typename GemmTile<BF>::T* lds, const Operand& o, int z, int cn, int64_t xbase,
-                                int col0, int cols_valid, int k0, int k_valid, int tid) {
-    constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
+// fp32 tiles of an operand whose rows are the contraction index ("NC" layout) stay as they
+// are in LDS, [k][t] with row stride GEMM_LDM: a lane then reads one value per instruction, and
+// the 4 lane groups of a read (4 k apart) fall on disjoint banks.
+constexpr int GEMM_LDM = 68;
+
+// bf16 tiles from an operand whose rows are the contraction index ("NC" layout): element
+// (t, k) = row k, column t; stored transposed into lds[t][k].
+template <typename TS>
+__device__ inline void stage_nc(bf16_t* lds, const Operand& o, int z, int cn, int64_t xbase, int col0, int cols_valid,
+                                int k0, int k_valid, int tid) {
+    constexpr int BK = GemmTile<true>::BK, LDK = GemmTile<true>::LDK;
     // BK rows (k) x 64 columns; 4 consecutive columns per access
 #pragma unroll
     for (int h = 0; h < BK / 16; ++h) {
@@ -209,19 +206,37 @@ __device__ inline void stage_nc(typename GemmTile<BF>::T* lds, const Operand& o,
             }
         }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if constexpr (BF) lds[(cq + j) * LDK + k] = f2bf(v[j]);
-            else lds[(cq + j) * LDK + k] = v[j];
-        }
+        for (int j = 0; j < 4; ++j) lds[(cq + j) * LDK + k] = f2bf(v[j]);
     }
+}
+
+// fp32 tiles, 64 rows or columns x 16 k, one float4 per thread, loaded into registers first
+// (the next k-tile's loads are in flight during the current tile's matrix instructions)
+__device__ inline float4 load_tile32(const Operand& o, bool kc, int z, int cn, int64_t xbase, int t0, int t_valid,
+                                     int k0, int k_valid, int tid) {
+    const int a = kc ? tid >> 2 : tid >> 4, b = kc ? (tid & 3) * 4 : (tid & 15) * 4;  // (row, k) or (k, column)
+    const int t = kc ? a : b, k = kc ? b : a;
+    if (t0 + t < t_valid && k0 + k < k_valid) {
+        if (kc) return *(const float4*)(operand_row(o, 4, z, cn, xbase, t0 + t) + (size_t)(k0 + k) * 4);
+        return *(const float4*)(operand_row(o, 4, z, cn, xbase, k0 + k) + (size_t)(t0 + t) * 4);
+    }
+    return make_float4(0.f, 0.f, 0.f, 0.f);
+}
+// KC: lds[row][k] (row stride 20); NC: lds[k][column] (row stride GEMM_LDM)
+__device__ inline void store_tile32(float* lds, bool kc, const float4& v, int tid) {
+    if (kc) *(float4*)(lds + (tid >> 2) * 20 + (tid & 3) * 4) = v;
+    else *(float4*)(lds + (tid >> 4) * GEMM_LDM + (tid & 15) * 4) = v;
 }
 
 template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     typedef typename GemmTile<BF>::T LT;
     constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
-    __shared__ __attribute__((aligned(16))) LT As[64 * LDK];
-    __shared__ __attribute__((aligned(16))) LT Bs[64 * LDK];
+    // fp32: two buffers per operand (one barrier per k-tile); bf16: one
+    constexpr int ASZ = (BF || A_KC) ? 64 * LDK : 16 * GEMM_LDM, BSZ = (BF || B_KC) ? 64 * LDK : 16 * GEMM_LDM;
+    constexpr int NBUF = BF ? 1 : 2;
+    __shared__ __attribute__((aligned(16))) LT As[NBUF * ASZ];
+    __shared__ __attribute__((aligned(16))) LT Bs[NBUF * BSZ];
     __shared__ float rowsum[64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -247,33 +262,75 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-    for (int k0 = kbeg; k0 < kend; k0 += BK) {
-        if constexpr (A_KC) stage_kc<BF, TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
-        else stage_nc<BF, TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
-        if constexpr (B_KC) stage_kc<BF, TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
-        else stage_nc<BF, TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
-        __syncthreads();
-        if (do_rowsum && tid < 64) {
-            float s = 0.f;
+    const int rl = lane & 15, kg = lane >> 4;
+    if constexpr (!BF) {
+        // fp32 NC operands are kept as [k][t]
+        auto compute = [&](const float* A, const float* B) {
+            if (do_rowsum && tid < 64) {
+                float s = 0.f;
 #pragma unroll
-            for (int k = 0; k < BK; ++k) s += (float)to_f<LT>(As[tid * LDK + k]);
-            rowsum[tid] += s;
-        }
-        const int rl = lane & 15, kg = lane >> 4;
-        if constexpr (!BF) {
+                for (int k = 0; k < BK; ++k) s += A_KC ? A[tid * LDK + k] : A[k * GEMM_LDM + tid];
+                rowsum[tid] += s;
+            }
             f4 av[2], bv[2];
+            if constexpr (A_KC)
 #pragma unroll
-            for (int i = 0; i < 2; ++i) av[i] = *(const f4*)(As + (wm * 32 + i * 16 + rl) * LDK + kg * 4);
+                for (int i = 0; i < 2; ++i) av[i] = *(const f4*)(A + (wm * 32 + i * 16 + rl) * LDK + kg * 4);
+            if constexpr (B_KC)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) bv[j] = *(const f4*)(Bs + (wn * 32 + j * 16 + rl) * LDK + kg * 4);
+                for (int j = 0; j < 2; ++j) bv[j] = *(const f4*)(B + (wn * 32 + j * 16 + rl) * LDK + kg * 4);
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
+            for (int q = 0; q < 4; ++q) {
+                float aq[2], bq[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+                    aq[i] = A_KC ? av[i][q] : A[(kg * 4 + q) * GEMM_LDM + wm * 32 + i * 16 + rl];
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    bq[j] = B_KC ? bv[j][q] : B[(kg * 4 + q) * GEMM_LDM + wn * 32 + j * 16 + rl];
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][q], bv[j][q], acc[i][j], 0, 0, 0);
-        } else {
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[i], bq[j], acc[i][j], 0, 0, 0);
+            }
+        };
+        float4 ra = make_float4(0.f, 0.f, 0.f, 0.f), rb = ra;
+        if (kbeg < kend) {
+            ra = load_tile32(g.a, A_KC, zz, cn, xbase, m0, Mv, kbeg, kend, tid);
+            rb = load_tile32(g.b, B_KC, zz, cn, xbase, n0, Nv, kbeg, kend, tid);
+            store_tile32((float*)As, A_KC, ra, tid);
+            store_tile32((float*)Bs, B_KC, rb, tid);
+        }
+        __syncthreads();
+        int buf = 0;
+        for (int k0 = kbeg; k0 < kend; k0 += BK) {
+            const bool more = k0 + BK < kend;
+            if (more) {
+                ra = load_tile32(g.a, A_KC, zz, cn, xbase, m0, Mv, k0 + BK, kend, tid);
+                rb = load_tile32(g.b, B_KC, zz, cn, xbase, n0, Nv, k0 + BK, kend, tid);
+            }
+            compute((const float*)As + buf * ASZ, (const float*)Bs + buf * BSZ);
+            if (more) {
+                store_tile32((float*)As + (buf ^ 1) * ASZ, A_KC, ra, tid);
+                store_tile32((float*)Bs + (buf ^ 1) * BSZ, B_KC, rb, tid);
+            }
+            __syncthreads();
+            buf ^= 1;
+        }
+    } else {
+        for (int k0 = kbeg; k0 < kend; k0 += BK) {
+            if constexpr (A_KC) stage_kc<TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+            else stage_nc<TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+            if constexpr (B_KC) stage_kc<TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+            else stage_nc<TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+            __syncthreads();
+            if (do_rowsum && tid < 64) {
+                float s = 0.f;
+#pragma unroll
+                for (int k = 0; k < BK; ++k) s += (float)to_f<LT>(As[tid * LDK + k]);
+                rowsum[tid] += s;
+            }
             bf8v av[2], bv[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i) av[i] = *(const bf8v*)(As + (wm * 32 + i * 16 + rl) * LDK + kg * 8);
@@ -284,8 +341,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+            __syncthreads();
         }
-        __syncthreads();
     }
 
     // epilogue: lane holds C rows 4*(lane/16)+r, column lane%16 of each 16x16 block
