@@ -151,64 +151,91 @@ __device__ inline const char* operand_row(const Operand& o, int elem, int z, int
     return p + (size_t)(z * o.zstride + r * o.ld) * elem;
 }
 
-// bf16 tiles: stage a 64 x 32 tile (rows row0.., k k0..) of an operand whose rows are the
-// tile's non-contraction index ("KC" layout) into lds[row][k].
+// bf16 tiles, 64 rows or columns x 32 k, stored as lds[t][k] (row stride 40 bf16), loaded into
+// registers first (up to 32 bytes per thread; fp32 sources are rounded to bf16 on the way in).
+//   KC (rows = t): fp32 two float4 of 4 k, bf16 one 16-byte load of 8 k;
+//   NC (rows = k): a 2 k x 4 t block per thread (lane bits 0-3 the k pair, so that the
+//   transposing 4-byte stores of a wave fall on distinct banks).
+struct BfRaw { uint4 r[2]; };
+
 template <typename TS>
-__device__ inline void stage_kc(bf16_t* lds, const Operand& o, int z, int cn, int64_t xbase, int row0, int rows_valid,
-                                int k0, int k_valid, int tid) {
-    constexpr int LDK = GemmTile<true>::LDK;
+__device__ inline BfRaw bf_load_kc(const Operand& o, int z, int cn, int64_t xbase, int row0, int rows_valid, int k0,
+                                   int k_valid, int tid) {
+    BfRaw v;
+    v.r[0] = v.r[1] = make_uint4(0, 0, 0, 0);
     if constexpr (sizeof(TS) == 4) {
-        // 64 rows x 32 k from fp32: two float4 per thread, converted
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int idx = tid + h * 256, r = idx >> 3, kq = (idx & 7) * 4;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
             if (row0 + r < rows_valid && k0 + kq < k_valid)
-                v = *(const float4*)(operand_row(o, 4, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 4);
-            bf16_t* d = lds + r * LDK + kq;
-            d[0] = f2bf(v.x); d[1] = f2bf(v.y); d[2] = f2bf(v.z); d[3] = f2bf(v.w);
+                v.r[h] = *(const uint4*)(operand_row(o, 4, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 4);
         }
     } else {
-        // 64 rows x 32 k from bf16: one 16-byte load per thread
         const int r = tid >> 2, kq = (tid & 3) * 8;
-        uint4 v = make_uint4(0, 0, 0, 0);
         if (row0 + r < rows_valid && k0 + kq < k_valid)
-            v = *(const uint4*)(operand_row(o, 2, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 2);
-        *(uint4*)(lds + r * LDK + kq) = v;
+            v.r[0] = *(const uint4*)(operand_row(o, 2, z, cn, xbase, row0 + r) + (size_t)(k0 + kq) * 2);
     }
+    return v;
+}
+template <typename TS>
+__device__ inline void bf_store_kc(bf16_t* lds, const BfRaw& v, int tid) {
+    constexpr int LDK = GemmTile<true>::LDK;
+    if constexpr (sizeof(TS) == 4) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int idx = tid + h * 256, r = idx >> 3, kq = (idx & 7) * 4;
+            const uint4 u = v.r[h];
+            uint2 q;
+            q.x = (uint32_t)f2bf(__uint_as_float(u.x)) | ((uint32_t)f2bf(__uint_as_float(u.y)) << 16);
+            q.y = (uint32_t)f2bf(__uint_as_float(u.z)) | ((uint32_t)f2bf(__uint_as_float(u.w)) << 16);
+            *(uint2*)(lds + r * LDK + kq) = q;
+        }
+    } else {
+        *(uint4*)(lds + (tid >> 2) * LDK + (tid & 3) * 8) = v.r[0];
+    }
+}
+template <typename TS>
+__device__ inline BfRaw bf_load_nc(const Operand& o, int z, int cn, int64_t xbase, int col0, int cols_valid, int k0,
+                                   int k_valid, int tid) {
+    BfRaw v;
+    v.r[0] = v.r[1] = make_uint4(0, 0, 0, 0);
+    const int k = (tid & 15) * 2, cq = (tid >> 4) * 4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if (k0 + k + h < k_valid && col0 + cq < cols_valid) {
+            const char* row = operand_row(o, sizeof(TS), z, cn, xbase, k0 + k + h);
+            if constexpr (sizeof(TS) == 4) v.r[h] = *(const uint4*)(row + (size_t)(col0 + cq) * 4);
+            else {
+                const uint2 q = *(const uint2*)(row + (size_t)(col0 + cq) * 2);
+                v.r[h].x = q.x; v.r[h].y = q.y;
+            }
+        }
+    }
+    return v;
+}
+template <typename TS>
+__device__ inline void bf_store_nc(bf16_t* lds, const BfRaw& v, int tid) {
+    constexpr int LDK = GemmTile<true>::LDK;
+    const int k = (tid & 15) * 2, cq = (tid >> 4) * 4;
+    uint32_t e[2][4];  // bf16 bits of (k + h, cq + j)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if constexpr (sizeof(TS) == 4) {
+            e[h][0] = f2bf(__uint_as_float(v.r[h].x)); e[h][1] = f2bf(__uint_as_float(v.r[h].y));
+            e[h][2] = f2bf(__uint_as_float(v.r[h].z)); e[h][3] = f2bf(__uint_as_float(v.r[h].w));
+        } else {
+            e[h][0] = v.r[h].x & 0xffff; e[h][1] = v.r[h].x >> 16;
+            e[h][2] = v.r[h].y & 0xffff; e[h][3] = v.r[h].y >> 16;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) *(uint32_t*)(lds + (cq + j) * LDK + k) = e[0][j] | (e[1][j] << 16);
 }
 
 // fp32 tiles of an operand whose rows are the contraction index ("NC" layout) stay as they
 // are in LDS, [k][t] with row stride GEMM_LDM: a lane then reads one value per instruction, and
 // the 4 lane groups of a read (4 k apart) fall on disjoint banks.
 constexpr int GEMM_LDM = 68;
-
-// bf16 tiles from an operand whose rows are the contraction index ("NC" layout): element
-// (t, k) = row k, column t; stored transposed into lds[t][k].
-template <typename TS>
-__device__ inline void stage_nc(bf16_t* lds, const Operand& o, int z, int cn, int64_t xbase, int col0, int cols_valid,
-                                int k0, int k_valid, int tid) {
-    constexpr int BK = GemmTile<true>::BK, LDK = GemmTile<true>::LDK;
-    // BK rows (k) x 64 columns; 4 consecutive columns per access
-#pragma unroll
-    for (int h = 0; h < BK / 16; ++h) {
-        const int idx = tid + h * 256, k = idx >> 4, cq = (idx & 15) * 4;
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-        if (k0 + k < k_valid && col0 + cq < cols_valid) {
-            const char* row = operand_row(o, sizeof(TS), z, cn, xbase, k0 + k);
-            if constexpr (sizeof(TS) == 4) {
-                float4 q = *(const float4*)(row + (size_t)(col0 + cq) * 4);
-                v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
-            } else {
-                uint2 q = *(const uint2*)(row + (size_t)(col0 + cq) * 2);
-                v[0] = bf2f((bf16_t)(q.x & 0xffff)); v[1] = bf2f((bf16_t)(q.x >> 16));
-                v[2] = bf2f((bf16_t)(q.y & 0xffff)); v[3] = bf2f((bf16_t)(q.y >> 16));
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) lds[(cq + j) * LDK + k] = f2bf(v[j]);
-    }
-}
 
 // fp32 tiles, 64 rows or columns x 16 k, one float4 per thread, loaded into registers first
 // (the next k-tile's loads are in flight during the current tile's matrix instructions)
@@ -228,13 +255,15 @@ __device__ inline void store_tile32(float* lds, bool kc, const float4& v, int ti
     else *(float4*)(lds + (tid >> 4) * GEMM_LDM + (tid & 15) * 4) = v;
 }
 
-template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO>
+// WPRE (weight update with a short contraction): the update's targets are read before the
+// contraction, their latency behind it (16 more registers per lane)
+template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO, bool WPRE = false>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     typedef typename GemmTile<BF>::T LT;
     constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
-    // fp32: two buffers per operand (one barrier per k-tile); bf16: one
+    // two buffers per operand (one barrier per k-tile)
     constexpr int ASZ = (BF || A_KC) ? 64 * LDK : 16 * GEMM_LDM, BSZ = (BF || B_KC) ? 64 * LDK : 16 * GEMM_LDM;
-    constexpr int NBUF = BF ? 1 : 2;
+    constexpr int NBUF = 2;
     __shared__ __attribute__((aligned(16))) LT As[NBUF * ASZ];
     __shared__ __attribute__((aligned(16))) LT Bs[NBUF * BSZ];
     __shared__ float rowsum[64];
@@ -261,6 +290,19 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    float wpre[2][2][4];
+    if constexpr (WPRE) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int m = m0 + wm * 32 + i * 16 + (lane >> 4) * 4 + r;
+                    const int n = n0 + wn * 32 + j * 16 + (lane & 15);
+                    wpre[i][j][r] = (m < Mv && n < Nv) ? ((const float*)g.c)[(size_t)zz * g.c_z + (size_t)m * g.c_ld + n] : 0.f;
+                }
+    }
 
     const int rl = lane & 15, kg = lane >> 4;
     if constexpr (!BF) {
@@ -319,29 +361,49 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             buf ^= 1;
         }
     } else {
+        BfRaw ra, rb;
+        auto load = [&](int k0) {
+            if constexpr (A_KC) ra = bf_load_kc<TA>(g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+            else ra = bf_load_nc<TA>(g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+            if constexpr (B_KC) rb = bf_load_kc<TB>(g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+            else rb = bf_load_nc<TB>(g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+        };
+        auto store = [&](int buf) {
+            if constexpr (A_KC) bf_store_kc<TA>(As + buf * ASZ, ra, tid);
+            else bf_store_nc<TA>(As + buf * ASZ, ra, tid);
+            if constexpr (B_KC) bf_store_kc<TB>(Bs + buf * BSZ, rb, tid);
+            else bf_store_nc<TB>(Bs + buf * BSZ, rb, tid);
+        };
+        if (kbeg < kend) {
+            load(kbeg);
+            store(0);
+        }
+        __syncthreads();
+        int buf = 0;
         for (int k0 = kbeg; k0 < kend; k0 += BK) {
-            if constexpr (A_KC) stage_kc<TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
-            else stage_nc<TA>(As, g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
-            if constexpr (B_KC) stage_kc<TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
-            else stage_nc<TB>(Bs, g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
-            __syncthreads();
+            const bool more = k0 + BK < kend;
+            if (more) load(k0 + BK);
+            const LT* A = As + buf * ASZ;
+            const LT* Bt = Bs + buf * BSZ;
             if (do_rowsum && tid < 64) {
                 float s = 0.f;
 #pragma unroll
-                for (int k = 0; k < BK; ++k) s += (float)to_f<LT>(As[tid * LDK + k]);
+                for (int k = 0; k < BK; ++k) s += (float)to_f<LT>(A[tid * LDK + k]);
                 rowsum[tid] += s;
             }
             bf8v av[2], bv[2];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) av[i] = *(const bf8v*)(As + (wm * 32 + i * 16 + rl) * LDK + kg * 8);
+            for (int i = 0; i < 2; ++i) av[i] = *(const bf8v*)(A + (wm * 32 + i * 16 + rl) * LDK + kg * 8);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) bv[j] = *(const bf8v*)(Bs + (wn * 32 + j * 16 + rl) * LDK + kg * 8);
+            for (int j = 0; j < 2; ++j) bv[j] = *(const bf8v*)(Bt + (wn * 32 + j * 16 + rl) * LDK + kg * 8);
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+            if (more) store(buf ^ 1);
             __syncthreads();
+            buf ^= 1;
         }
     }
 
@@ -369,7 +431,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
                     ((TO*)g.c)[ci] = from_f<TO>(v * act_deriv(g.act, x));
                 } else {  // EPI_UPD: in-place W -= scale * acc (master fp32)
                     float* W = (float*)g.c;
-                    const float w = W[ci] - scale * v;
+                    const float w = (WPRE ? wpre[i][j][r] : W[ci]) - scale * v;
                     W[ci] = w;
                     if (g.shadow) g.shadow[ci] = f2bf(w);
                 }

@@ -276,7 +276,8 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
         }
     }
     Launch l(n, s, name);
-    gemm_kernel<BF, TA, TB, A_KC, B_KC, EPI, TO><<<grid, 256, 0, s>>>(g);
+    if (EPI == EPI_UPD && g.Kd <= 64) gemm_kernel<BF, TA, TB, A_KC, B_KC, EPI, TO, EPI == EPI_UPD><<<grid, 256, 0, s>>>(g);
+    else gemm_kernel<BF, TA, TB, A_KC, B_KC, EPI, TO><<<grid, 256, 0, s>>>(g);
     return l.done();
 }
 
