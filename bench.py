@@ -46,37 +46,67 @@ def method_flops_per_sample(w) -> float:
 
 
 def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
-    """Algorithmic work of one launch of a library kernel: (bound, flops, bytes).
+    """Algorithmic work of one launch of a library kernel: (flops, bytes), or None.
 
     psgd_persistent: one launch trains every CN for one epoch (per-sample SGD).  Priced in
       effective HBM bytes: a step of plain per-sample SGD reads and writes every parameter
       once and reads its input row, 8 P + 4 n_in bytes, times the N steps of the launch.
       (The kernel keeps the parameters on chip, so its real traffic is far lower: this is
       the rate at which an HBM-streaming implementation would have to run to match it.)
-    fwd_gemm / upd_gemm / bwd_gemm (mini-batch plan): totals over the profiled step of
-      2 * rows * out * in for the layers these kernels handle (output layers of <= 16
-      neurons use the row kernels), divided by the launches.
-    merge: reads K*P floats and writes P (and K*P with broadcast), HBM bound.
+    Mini-batch plan, totals over the profiled step divided by the launches; a layer of `in`
+    inputs and `out` neurons, `rows` sample rows over all CNs and epochs, `bsteps` batch steps
+    per CN; weight operands are 4 bytes (fp32) or 2 (bf16 shadow), activations and errors 4
+    or 2, the fp32 master update reads and writes 8 bytes per weight (+ 2 for the bf16 shadow):
+      fwd_gemm (hidden layers):  2 rows out in flops; K bsteps out in w_op + rows (in x + out a)
+      bwd_gemm (hidden errors behind a wide layer): 2 rows out in; K bsteps out in w_op +
+                                 rows (out a + 2 in a)
+      upd_gemm (wide layers):    2 rows out in; K bsteps (out in (8 + shadow) + 8 out) +
+                                 rows (out a + in x)
+      tail (fused narrow last layer: forward, output error, hidden error, update):
+                                 6 rows O H; K bsteps (O H (w_op + 8 + shadow) + 8 O) +
+                                 rows (2 H a + 4)
+    merge: reads K*P floats and writes P (and K*P with broadcast).
     """
     s = w.sizes
     K = w.replicas
     L = len(s) - 1
     if name == "psgd_persistent":
-        return "hbm", N * method_flops_per_sample(w), N * (8.0 * w.param_count() + 4.0 * s[0])
-    rows = N * epochs_profiled
-    if name == "fwd_gemm":
-        f = sum(2.0 * rows * s[l + 1] * s[l] for l in range(L) if s[l + 1] > 16)
-        return "mfma", f / launches, None
-    if name == "upd_gemm":
-        f = sum(2.0 * rows * s[l + 1] * s[l] for l in range(L) if s[l + 1] > 16)
-        return "mfma", f / launches, None
-    if name == "bwd_gemm":
-        f = sum(2.0 * rows * s[l + 1] * s[l] for l in range(1, L) if s[l + 1] > 16)
-        return "mfma", f / launches, None
+        return N * method_flops_per_sample(w), N * (8.0 * w.param_count() + 4.0 * s[0])
     if name == "merge":
         P = w.param_count()
-        return "hbm", 0.0, (K * P + P + (K * P if w.merge_every_epoch else 0)) * 4.0
-    return None
+        return 0.0, (K * P + P + (K * P if w.merge_every_epoch else 0)) * 4.0
+    bf = w.precision == I.BF16_MIXED
+    a = 2.0 if bf else 4.0           # hidden activations and errors
+    wop = 2.0 if bf else 4.0         # operand weights
+    shadow = 2.0 if bf else 0.0
+    rows = float(N * epochs_profiled)
+    bsteps = float(-(-(-(-N // K)) // w.batch) * epochs_profiled)
+
+    def x_bytes(l):  # one input value of layer l (1-based): the fp32 data set for layer 1
+        return 4.0 if l == 1 else a
+
+    f = b = 0.0
+    if name == "fwd_gemm":
+        for l in range(1, L):
+            f += 2 * rows * s[l] * s[l - 1]
+            b += K * bsteps * s[l] * s[l - 1] * wop + rows * (s[l - 1] * x_bytes(l) + s[l] * a)
+    elif name == "bwd_gemm":
+        for l in range(1, L - 1):  # (the hidden error behind the last layer is in the tail)
+            if s[l + 1] > 16:
+                f += 2 * rows * s[l + 1] * s[l]
+                b += K * bsteps * s[l + 1] * s[l] * wop + rows * (s[l + 1] * a + 2 * s[l] * a)
+    elif name == "upd_gemm":
+        for l in range(1, L):
+            if s[l] > 16:
+                f += 2 * rows * s[l] * s[l - 1]
+                b += K * bsteps * (s[l] * s[l - 1] * (8 + shadow) + 8 * s[l]) + rows * (s[l] * a + s[l - 1] * x_bytes(l))
+    elif name == "tail":
+        O, H = s[L], s[L - 1]
+        f = 6 * rows * O * H
+        b = K * bsteps * (O * H * (wop + 8 + shadow) + 8 * O) + rows * (2 * H * a + 4)
+    else:
+        return None
+    return f / launches, b / launches
 
 
 def source_digest() -> str:
@@ -205,16 +235,20 @@ def main():
         avg_s = tot / 1e3 / n_l
         wk = kernel_work(w, dom, n_l, N, w.epochs)
         if wk is not None:
-            bound, flops, byts = wk
-            if bound == "hbm":
-                ach, peak, unit = byts / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+            flops, byts = wk
+            # the bound is the roof the kernel's arithmetic intensity reaches first: the matrix
+            # peak of its operand type against HBM (ridge 19.7 flop/B in fp32, 312 in bf16)
+            mpeak = BF16_PEAK_TFLOPS if w.precision == I.BF16_MIXED else FP32_PEAK_TFLOPS
+            ridge = mpeak * 1e12 / (HBM_PEAK_GBS * 1e9)
+            if dom == "psgd_persistent" or flops < ridge * byts:
+                bound, ach, peak, unit = "hbm", byts / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
             else:
-                peak = BF16_PEAK_TFLOPS if w.precision == I.BF16_MIXED and bound == "mfma" else FP32_PEAK_TFLOPS
-                ach, unit = flops / avg_s / 1e12, "TFLOP/s"
+                bound, ach, peak, unit = "mfma", flops / avg_s / 1e12, mpeak, "TFLOP/s"
             traffic = measured_traffic(dom, w.name)
             roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 4), "peak": peak, "unit": unit,
                         "frac": round(ach / peak, 6), "traffic": traffic, "avg_us": round(avg_s * 1e6, 3),
-                        "work_per_launch": byts if bound == "hbm" else flops}
+                        "work_per_launch": byts if bound == "hbm" else flops,
+                        "flop_per_byte": round(flops / byts, 3) if byts else None}
 
     cpu = None
     if not args.no_cpu_baseline:

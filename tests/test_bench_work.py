@@ -1,0 +1,51 @@
+"""Host-side checks of bench.py's pricing of the kernels (CPU only).
+
+The per-launch work that bench.py divides by measured kernel times must add up to the
+method's own operation count: the matrix kernels of a mini-batch step together perform the
+multiply-adds of the forward pass, the hidden errors and the weight gradients (eq. (2), (11),
+(12)) of every sample once per epoch, and the per-sample kernel is priced at one read and
+one write of every parameter plus the input row per step.
+"""
+import pytest
+
+import bench
+import pnn_inputs as I
+
+MINIBATCH = [i for i, w in enumerate(I.WORKLOADS) if w.batch > 1]
+
+
+def test_per_sample_effective_bytes():
+    w = I.WORKLOADS[1]
+    f, b = bench.kernel_work(w, "psgd_persistent", 1, w.n_train, 1)
+    assert b == w.n_train * (8.0 * w.param_count() + 4.0 * w.sizes[0])
+    assert f == w.n_train * bench.method_flops_per_sample(w)
+
+
+@pytest.mark.parametrize("idx", MINIBATCH)
+def test_minibatch_kernels_cover_the_method(idx):
+    w = I.WORKLOADS[idx]
+    s, N, E = w.sizes, w.n_train, w.epochs
+    total = 0.0
+    for name in ("fwd_gemm", "bwd_gemm", "upd_gemm", "tail"):
+        f, _ = bench.kernel_work(w, name, 1, N, E)
+        total += f
+    weights = sum(s[l] * s[l + 1] for l in range(len(s) - 1))
+    behind = sum(s[l] * s[l + 1] for l in range(1, len(s) - 1))
+    assert total == pytest.approx(N * E * (4.0 * weights + 2.0 * behind), rel=1e-12)
+
+
+@pytest.mark.parametrize("idx", MINIBATCH)
+def test_minibatch_bytes_cover_every_weight_pass(idx):
+    # each batch step of each CN reads every operand weight at least once and rewrites the
+    # fp32 master of every weight
+    w = I.WORKLOADS[idx]
+    s, K = w.sizes, w.replicas
+    bsteps = -(-(-(-w.n_train // K)) // w.batch) * w.epochs
+    total = sum(bench.kernel_work(w, n, 1, w.n_train, w.epochs)[1] for n in ("fwd_gemm", "bwd_gemm", "upd_gemm", "tail"))
+    weights = sum(s[l] * s[l + 1] for l in range(len(s) - 1))
+    assert total >= K * bsteps * weights * 8.0
+
+
+def test_unpriced_kernels():
+    w = I.WORKLOADS[2]
+    assert bench.kernel_work(w, "fwd_reduce", 1, w.n_train, 1) is None
