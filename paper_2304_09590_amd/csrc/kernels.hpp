@@ -47,6 +47,27 @@ template <typename T> __device__ inline T from_f(float v);
 template <> __device__ inline float from_f<float>(float v) { return v; }
 template <> __device__ inline bf16_t from_f<bf16_t>(float v) { return f2bf(v); }
 
+// four consecutive values of type T (16-byte aligned for fp32, 8-byte for bf16), as fp32
+template <typename T>
+__device__ inline float4 load4(const T* p) {
+    if constexpr (sizeof(T) == 4) return *(const float4*)p;
+    else {
+        const uint2 q = *(const uint2*)p;
+        return make_float4(bf2f((bf16_t)(q.x & 0xffff)), bf2f((bf16_t)(q.x >> 16)), bf2f((bf16_t)(q.y & 0xffff)),
+                           bf2f((bf16_t)(q.y >> 16)));
+    }
+}
+template <typename T>
+__device__ inline void store4(T* p, float4 v) {
+    if constexpr (sizeof(T) == 4) *(float4*)p = v;
+    else {
+        uint2 q;
+        q.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+        q.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+        *(uint2*)p = q;
+    }
+}
+
 // ------------------------------------------------------------------------------------
 // activations.  The rectifiers store z < 0 with its sign (a negative zero for ReLU), so
 // that phi'(z) can be read back from the stored activation alone, with phi'(0) = 1.
@@ -309,18 +330,39 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-    float wpre[2][2][4];
+    // SW: the operands enter the matrix instructions swapped (B as the first), so that a lane
+    // holds C row m = m0 + 32 wm + 16 i + (lane & 15), columns n .. n+3 with
+    // n = n0 + 32 wn + 16 j + 4 (lane >> 4), of each 16 x 16 block, and the epilogue reads and
+    // writes 4 consecutive values at once where the target's strides allow.  Otherwise a lane
+    // holds rows 4 (lane >> 4) + r, column lane & 15.  (The bf16 weight update, which also
+    // writes the bf16 shadow, measured faster with the second layout.)
+    constexpr bool SW = !(BF && EPI == EPI_UPD);
+    const bool vec = SW && ((g.c_ld | g.c_z | g.c_split | g.bias_z) & 3) == 0;
+    auto coord = [&](int i, int j, int r, int& m, int& n) {
+        if (SW) { m = m0 + wm * 32 + i * 16 + (lane & 15); n = n0 + wn * 32 + j * 16 + (lane >> 4) * 4 + r; }
+        else { m = m0 + wm * 32 + i * 16 + (lane >> 4) * 4 + r; n = n0 + wn * 32 + j * 16 + (lane & 15); }
+    };
+    float4 wpre[2][2];
     if constexpr (WPRE) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
+            for (int j = 0; j < 2; ++j) {
+                int m, n;
+                coord(i, j, 0, m, n);
+                const float* W = (const float*)g.c + (size_t)zz * g.c_z;
+                if (vec && m < Mv && n + 3 < Nv) {
+                    wpre[i][j] = *(const float4*)(W + (size_t)m * g.c_ld + n);
+                } else {
+                    float t[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = m0 + wm * 32 + i * 16 + (lane >> 4) * 4 + r;
-                    const int n = n0 + wn * 32 + j * 16 + (lane & 15);
-                    wpre[i][j][r] = (m < Mv && n < Nv) ? ((const float*)g.c)[(size_t)zz * g.c_z + (size_t)m * g.c_ld + n] : 0.f;
+                    for (int r = 0; r < 4; ++r) {
+                        coord(i, j, r, m, n);
+                        t[r] = (m < Mv && n < Nv) ? W[(size_t)m * g.c_ld + n] : 0.f;
+                    }
+                    wpre[i][j] = make_float4(t[0], t[1], t[2], t[3]);
                 }
+            }
     }
 
     const int rl = lane & 15, kg = lane >> 4;
@@ -353,7 +395,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
                 for (int i = 0; i < 2; ++i)
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[i], bq[j], acc[i][j], 0, 0, 0);
+                        acc[i][j] = SW ? __builtin_amdgcn_mfma_f32_16x16x4f32(bq[j], aq[i], acc[i][j], 0, 0, 0)
+                                       : __builtin_amdgcn_mfma_f32_16x16x4f32(aq[i], bq[j], acc[i][j], 0, 0, 0);
             }
         };
         float4 ra = make_float4(0.f, 0.f, 0.f, 0.f), rb = ra;
@@ -419,42 +462,68 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             for (int i = 0; i < 2; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = SW ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[j], av[i], acc[i][j], 0, 0, 0)
+                                   : __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
             if (more) store(buf ^ 1);
             __syncthreads();
             buf ^= 1;
         }
     }
 
-    // epilogue: lane holds C rows 4*(lane/16)+r, column lane%16 of each 16x16 block
+    // epilogue (layout above)
     float scale = g.lr;
     if (EPI == EPI_UPD && g.scale_per_batch) scale = valid > 0 ? g.lr / (float)valid : 0.f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = m0 + wm * 32 + i * 16 + (lane >> 4) * 4 + r;
-                const int n = n0 + wn * 32 + j * 16 + (lane & 15);
-                if (m >= Mv || n >= Nv) continue;
-                const float v = acc[i][j][r];
+        for (int j = 0; j < 2; ++j) {
+            int m, n;
+            coord(i, j, 0, m, n);
+            const f4 v = acc[i][j];
+            if (vec && m < Mv && n + 3 < Nv) {
                 const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+                const float4 c4 = make_float4(v[0], v[1], v[2], v[3]);
                 if constexpr (EPI == EPI_STORE) {
-                    ((float*)g.c)[ci + (size_t)slice * g.c_split] = v;
+                    *(float4*)((float*)g.c + ci + (size_t)slice * g.c_split) = c4;
                 } else if constexpr (EPI == EPI_FWD) {
-                    const float zv = v + g.bias[(size_t)cn * g.bias_z + n];
-                    ((TO*)g.c)[ci] = from_f<TO>(act_fn(g.act, zv));
+                    const float4 bb = *(const float4*)(g.bias + (size_t)cn * g.bias_z + n);
+                    store4<TO>((TO*)g.c + ci, make_float4(act_fn(g.act, c4.x + bb.x), act_fn(g.act, c4.y + bb.y),
+                                                          act_fn(g.act, c4.z + bb.z), act_fn(g.act, c4.w + bb.w)));
                 } else if constexpr (EPI == EPI_BWD) {
-                    const float x = to_f<TO>(((const TO*)g.aux)[ci]);
-                    ((TO*)g.c)[ci] = from_f<TO>(v * act_deriv(g.act, x));
+                    const float4 x = load4<TO>((const TO*)g.aux + ci);
+                    store4<TO>((TO*)g.c + ci, make_float4(c4.x * act_deriv(g.act, x.x), c4.y * act_deriv(g.act, x.y),
+                                                          c4.z * act_deriv(g.act, x.z), c4.w * act_deriv(g.act, x.w)));
                 } else {  // EPI_UPD: in-place W -= scale * acc (master fp32)
-                    float* W = (float*)g.c;
-                    const float w = (WPRE ? wpre[i][j][r] : W[ci]) - scale * v;
-                    W[ci] = w;
-                    if (g.shadow) g.shadow[ci] = f2bf(w);
+                    float* W = (float*)g.c + ci;
+                    float4 w = WPRE ? wpre[i][j] : *(const float4*)W;
+                    w.x -= scale * c4.x; w.y -= scale * c4.y; w.z -= scale * c4.z; w.w -= scale * c4.w;
+                    *(float4*)W = w;
+                    if (g.shadow) store4<bf16_t>(g.shadow + ci, w);
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    coord(i, j, r, m, n);
+                    if (m >= Mv || n >= Nv) continue;
+                    const size_t cr = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+                    if constexpr (EPI == EPI_STORE) {
+                        ((float*)g.c)[cr + (size_t)slice * g.c_split] = v[r];
+                    } else if constexpr (EPI == EPI_FWD) {
+                        const float zv = v[r] + g.bias[(size_t)cn * g.bias_z + n];
+                        ((TO*)g.c)[cr] = from_f<TO>(act_fn(g.act, zv));
+                    } else if constexpr (EPI == EPI_BWD) {
+                        const float x = to_f<TO>(((const TO*)g.aux)[cr]);
+                        ((TO*)g.c)[cr] = from_f<TO>(v[r] * act_deriv(g.act, x));
+                    } else {
+                        float* W = (float*)g.c;
+                        const float wp[4] = {wpre[i][j].x, wpre[i][j].y, wpre[i][j].z, wpre[i][j].w};
+                        const float w = (WPRE ? wp[r] : W[cr]) - scale * v[r];
+                        W[cr] = w;
+                        if (g.shadow) g.shadow[cr] = f2bf(w);
+                    }
                 }
             }
+        }
     if (do_rowsum && tid < 64 && m0 + tid < Mv) {
         float* b = g.ubias + (size_t)cn * g.bias_z;
         b[m0 + tid] -= scale * rowsum[tid];
@@ -911,15 +980,6 @@ __host__ __device__ inline int64_t tail_lds_floats(int H, int rg) {
     return (int64_t)(16 + rg) * (H + 4) + (int64_t)rg * (TAIL_DLS + 1) + TAIL_PART;
 }
 
-template <typename TH>
-__device__ inline float4 load4(const TH* p) {
-    if constexpr (sizeof(TH) == 4) return *(const float4*)p;
-    else {
-        const uint2 q = *(const uint2*)p;
-        return make_float4(bf2f((bf16_t)(q.x & 0xffff)), bf2f((bf16_t)(q.x >> 16)), bf2f((bf16_t)(q.y & 0xffff)),
-                           bf2f((bf16_t)(q.y >> 16)));
-    }
-}
 // four values as loaded (converted only when the load has landed)
 template <typename TH> struct Raw4 { typedef float4 T; };
 template <> struct Raw4<bf16_t> { typedef uint2 T; };
