@@ -667,39 +667,65 @@ __global__ __launch_bounds__(256) void gemm128_kernel(GemmArgs g) {
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[i], bq[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(bq[j], aq[i], acc[i][j], 0, 0, 0);
         }
         if (more) store(buf ^ 1);
         __syncthreads();
         buf ^= 1;
     }
 
+    // (operands entered swapped: lane holds row m0 + 64 wm + 16 i + (lane & 15), columns
+    // n .. n+3 with n = n0 + 64 wn + 16 j + 4 (lane >> 4))
     float scale = g.lr;
     if (EPI == EPI_UPD && g.scale_per_batch) scale = valid > 0 ? g.lr / (float)valid : 0.f;
+    const bool vec = ((g.c_ld | g.c_z | g.c_split | g.bias_z) & 3) == 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
-                const int n = n0 + wn * 64 + j * 16 + (lane & 15);
-                if (m >= Mv || n >= Nv) continue;
-                const float v = acc[i][j][r];
-                const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + wm * 64 + i * 16 + (lane & 15);
+            const int n = n0 + wn * 64 + j * 16 + (lane >> 4) * 4;
+            if (m >= Mv || n >= Nv) continue;
+            const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+            const f4 v = acc[i][j];
+            if (vec && n + 3 < Nv) {
+                const float4 c4 = make_float4(v[0], v[1], v[2], v[3]);
                 if constexpr (EPI == EPI_STORE) {
-                    ((float*)g.c)[ci + (size_t)slice * g.c_split] = v;
+                    *(float4*)((float*)g.c + ci + (size_t)slice * g.c_split) = c4;
                 } else if constexpr (EPI == EPI_FWD) {
-                    const float zv = v + g.bias[(size_t)cn * g.bias_z + n];
-                    ((float*)g.c)[ci] = act_fn(g.act, zv);
+                    const float4 bb = *(const float4*)(g.bias + (size_t)cn * g.bias_z + n);
+                    *(float4*)((float*)g.c + ci) = make_float4(act_fn(g.act, c4.x + bb.x), act_fn(g.act, c4.y + bb.y),
+                                                               act_fn(g.act, c4.z + bb.z), act_fn(g.act, c4.w + bb.w));
                 } else if constexpr (EPI == EPI_BWD) {
-                    const float x = ((const float*)g.aux)[ci];
-                    ((float*)g.c)[ci] = v * act_deriv(g.act, x);
+                    const float4 x = *(const float4*)((const float*)g.aux + ci);
+                    *(float4*)((float*)g.c + ci) = make_float4(c4.x * act_deriv(g.act, x.x), c4.y * act_deriv(g.act, x.y),
+                                                               c4.z * act_deriv(g.act, x.z), c4.w * act_deriv(g.act, x.w));
                 } else {  // EPI_UPD: in-place W -= scale * acc
-                    float* W = (float*)g.c;
-                    W[ci] = W[ci] - scale * v;
+                    float4* W = (float4*)((float*)g.c + ci);
+                    float4 w = *W;
+                    w.x -= scale * c4.x; w.y -= scale * c4.y; w.z -= scale * c4.z; w.w -= scale * c4.w;
+                    *W = w;
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if (n + r >= Nv) continue;
+                    const size_t cr = ci + r;
+                    if constexpr (EPI == EPI_STORE) {
+                        ((float*)g.c)[cr + (size_t)slice * g.c_split] = v[r];
+                    } else if constexpr (EPI == EPI_FWD) {
+                        const float zv = v[r] + g.bias[(size_t)cn * g.bias_z + n + r];
+                        ((float*)g.c)[cr] = act_fn(g.act, zv);
+                    } else if constexpr (EPI == EPI_BWD) {
+                        const float x = ((const float*)g.aux)[cr];
+                        ((float*)g.c)[cr] = v[r] * act_deriv(g.act, x);
+                    } else {  // EPI_UPD: in-place W -= scale * acc
+                        float* W = (float*)g.c;
+                        W[cr] = W[cr] - scale * v[r];
+                    }
                 }
             }
+        }
     if (do_rowsum && tid < 128 && m0 + tid < Mv) {
         float* b = g.ubias + (size_t)cn * g.bias_z;
         b[m0 + tid] -= scale * rowsum[tid];
