@@ -117,6 +117,22 @@ pnn_status pnn_merge(pnn_net* net, int32_t broadcast, void* hip_stream);
 pnn_status pnn_infer(pnn_net* net, int32_t which, const float* x_dev, int64_t n, int32_t* pred_dev, float* out_dev,
                      int64_t* correct_host, const int32_t* y_dev, void* hip_stream);
 
+/* Evaluation of one network on labelled rows: the accuracy test of the merged network
+ * (sections "Implementation Details" and "MNIST Dataset") and the per-CN comparison and cost
+ * per epoch of the experiments.  which = -1 merged, 0..K-1 one CN.  x_dev [n][sizes[0]] fp32
+ * and y_dev [n] int32 are the caller's device arrays (labels in [0, sizes[L])).  Writes
+ *   *correct_host (nullable): rows whose argmax output (lowest index on ties) equals the label;
+ *   *cost_host (nullable): the mean cost over the rows, the cost whose output error training
+ *     uses: quadratic 1/2 sum_o (x_o - e_o)^2, or with PNN_LOSS_XENT the cross-entropy
+ *     (-log x_label for a softmax output, eq. (6); -sum_o [e_o log x_o + (1 - e_o) log(1 - x_o)]
+ *     for a sigmoid output), each row's cost in fp64 from the fp32 outputs, the rows summed in
+ *     a fixed order in fp64.
+ * Waits for the device.  The library owns a per-row cost buffer of the largest n seen (grown
+ * with hipMalloc on the first call that needs more).  n = 0 gives 0 and 0.0 without device work;
+ * a NULL x_dev or y_dev is PNN_EINVAL. */
+pnn_status pnn_eval(pnn_net* net, int32_t which, const float* x_dev, const int32_t* y_dev, int64_t n,
+                    int64_t* correct_host, double* cost_host, void* hip_stream);
+
 /* Copies one network's parameters (which = -1 merged, 0..K-1 a CN) to host_out (P floats)
  * in the layout above.  Waits for the device. */
 pnn_status pnn_get_params(pnn_net* net, int32_t which, float* host_out);

@@ -756,6 +756,7 @@ struct RowArgs {
     float* out;        // inference: [rows][O] outputs (nullable)
     int32_t* pred;     // inference: [rows] argmax
     unsigned long long* correct;  // inference: count of pred == y (nullable)
+    double* cost;      // inference: [rows] cost of each data-set row (nullable; needs y)
 };
 
 template <typename TX, typename TW, typename TD, bool TRAIN>
@@ -815,8 +816,24 @@ __global__ __launch_bounds__(256) void out_layer_kernel(RowArgs a) {
 #pragma unroll
         for (int o = 1; o < MAX_OUT; ++o) if (o < a.O && xo[o] > bv) { bv = xo[o]; best = o; }
         if (lane == 0) {
-            a.pred[drow] = best;
+            if (a.pred) a.pred[drow] = best;
             if (a.correct && a.y && a.y[drow] == best) atomicAdd(a.correct, 1ull);
+            if (a.cost && a.y) {
+                // the cost whose output error training uses: quadratic 1/2 sum (x - e)^2, or
+                // cross-entropy (eq. (6) for a softmax output, the two-class form per output
+                // for a sigmoid output), in double from the fp32 outputs
+                const int label = a.y[drow];
+                double c = 0.0;
+#pragma unroll
+                for (int o = 0; o < MAX_OUT; ++o) {
+                    if (o >= a.O) continue;
+                    const double x = (double)xo[o], e = (o == label) ? 1.0 : 0.0;
+                    if (a.loss != LOSS_XENT) c += 0.5 * (x - e) * (x - e);
+                    else if (a.act == ACT_SOFTMAX) c += (o == label) ? -log(x) : 0.0;
+                    else c += -(e * log(x) + (1.0 - e) * log(1.0 - x));
+                }
+                a.cost[drow] = c;
+            }
         }
         if (a.out && lane < a.O) {
             float xv = 0.f;
@@ -2450,6 +2467,21 @@ __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
         const int j = b - K;
         psgd_tile<T>(a, j / a.nrb, j % a.nrb, smem);
     }
+}
+
+// sum of n doubles in a fixed order (thread t takes t, t + 256, ...; then a fixed tree)
+__global__ __launch_bounds__(256) void sum_f64_kernel(const double* v, int64_t n, double* out) {
+    __shared__ double part[256];
+    const int t = threadIdx.x;
+    double s = 0.0;
+    for (int64_t i = t; i < n; i += 256) s += v[i];
+    part[t] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (t < h) part[t] += part[t + h];
+        __syncthreads();
+    }
+    if (t == 0) *out = part[0];
 }
 
 __global__ void zero_ints_kernel(int* p, int n) {

@@ -67,6 +67,9 @@ struct pnn_net {
     void* inf_ws[9] = {nullptr};
     int inf_rows = 0;
     unsigned long long* d_correct = nullptr;
+    double* d_cost = nullptr;     // [cost_rows] per-row costs of an evaluation
+    int64_t cost_rows = 0;
+    double* d_cost_sum = nullptr;
 
     // chunked per-sample plan
     bool psgd = false;
@@ -627,7 +630,7 @@ void free_all(pnn_net* n) {
     auto f = [](void* p) { if (p) (void)hipFree(p); };
     f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
     for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
-    f(n->d_correct); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
+    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
     for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : n->free_events) (void)hipEventDestroy(e);
 }
@@ -712,6 +715,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         if ((st = dev_alloc(n, &n->mshadow, (size_t)n->pstride)) != PNN_OK) return bail(st);
     }
     if ((st = dev_alloc(n, &n->d_correct, 1)) != PNN_OK) return bail(st);
+    if ((st = dev_alloc(n, &n->d_cost_sum, 1)) != PNN_OK) return bail(st);
 
     n->psgd = (B == 1 && n->L == 2 && !n->bf16 && n->sizes[1] <= 1024 && n->sizes[2] <= MAX_OUT);
     if (n->psgd) {
@@ -839,19 +843,12 @@ pnn_status pnn_merge(pnn_net* n, int32_t broadcast, void* hip_stream) {
     return l.done();
 }
 
-pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrows, int32_t* pred_dev, float* out_dev,
-                     int64_t* correct_host, const int32_t* y_dev, void* hip_stream) {
-    TRY(usable(n));
-    if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
-    if (nrows < 0) return fail(n, PNN_ESHAPE, "n < 0");
-    if (nrows == 0) {  // nothing to read or write
-        if (correct_host) *correct_host = 0;
-        return PNN_OK;
-    }
-    if (!x_dev || !pred_dev) return fail(n, PNN_EINVAL, "x_dev / pred_dev is NULL");
-    hipStream_t s = (hipStream_t)hip_stream;
-    const bool count = correct_host && y_dev;
-    if (count) HIP_TRY(n, hipMemsetAsync(n->d_correct, 0, sizeof(unsigned long long), s));
+// forward pass of one network over nrows data-set rows in chunks, then the output layer:
+// predictions (pred, nullable), outputs (out, nullable), the correct count into d_correct
+// (count), per-row costs into cost (nullable; needs y)
+static pnn_status run_inference(pnn_net* n, int32_t which, const float* x_dev, int64_t nrows, int32_t* pred_dev,
+                                float* out_dev, bool count, const int32_t* y_dev, double* cost, hipStream_t s) {
+    if (count) zero_ints_kernel<<<1, 256, 0, s>>>((int*)n->d_correct, 2);
     const int L = n->L;
     const int CH = 8192;
     const int rows = (int)std::min<int64_t>(nrows, CH);
@@ -896,6 +893,7 @@ pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrow
         a.H = n->sizes[L - 1]; a.O = n->sizes[L]; a.act = n->act[L - 1]; a.loss = n->cfg.loss;
         a.n_total = nrows; a.k_rep = 1; a.r0 = r0; a.step_rows = CH;
         a.y = y_dev; a.out = out_dev; a.pred = pred_dev; a.correct = count ? n->d_correct : nullptr;
+        a.cost = cost;
         const int rws = (int)std::min<int64_t>(CH, nrows - r0);
         dim3 grid((rws + 3) / 4, 1, 1);
         Launch lc(n, s, "infer_out");
@@ -909,12 +907,65 @@ pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrow
         }
         TRY(lc.done());
     }
+    return PNN_OK;
+}
+
+pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrows, int32_t* pred_dev, float* out_dev,
+                     int64_t* correct_host, const int32_t* y_dev, void* hip_stream) {
+    TRY(usable(n));
+    if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
+    if (nrows < 0) return fail(n, PNN_ESHAPE, "n < 0");
+    if (nrows == 0) {  // nothing to read or write
+        if (correct_host) *correct_host = 0;
+        return PNN_OK;
+    }
+    if (!x_dev || !pred_dev) return fail(n, PNN_EINVAL, "x_dev / pred_dev is NULL");
+    hipStream_t s = (hipStream_t)hip_stream;
+    const bool count = correct_host && y_dev;
+    TRY(run_inference(n, which, x_dev, nrows, pred_dev, out_dev, count, y_dev, nullptr, s));
     if (count) {
         unsigned long long c = 0;
         HIP_TRY(n, hipMemcpyAsync(&c, n->d_correct, sizeof c, hipMemcpyDeviceToHost, s));
         HIP_TRY(n, hipStreamSynchronize(s));
         *correct_host = (int64_t)c;
     }
+    return PNN_OK;
+}
+
+pnn_status pnn_eval(pnn_net* n, int32_t which, const float* x_dev, const int32_t* y_dev, int64_t nrows,
+                    int64_t* correct_host, double* cost_host, void* hip_stream) {
+    TRY(usable(n));
+    if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
+    if (nrows < 0) return fail(n, PNN_ESHAPE, "n < 0");
+    if (nrows == 0) {
+        if (correct_host) *correct_host = 0;
+        if (cost_host) *cost_host = 0.0;
+        return PNN_OK;
+    }
+    if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
+    hipStream_t s = (hipStream_t)hip_stream;
+    if (cost_host && nrows > n->cost_rows) {
+        HIP_TRY(n, hipStreamSynchronize(s));
+        if (n->d_cost) (void)hipFree(n->d_cost);
+        n->d_cost = nullptr;
+        n->cost_rows = 0;
+        TRY(dev_alloc(n, &n->d_cost, (size_t)nrows));
+        n->cost_rows = nrows;
+    }
+    TRY(run_inference(n, which, x_dev, nrows, nullptr, nullptr, correct_host != nullptr, y_dev,
+                      cost_host ? n->d_cost : nullptr, s));
+    if (cost_host) {
+        Launch lc(n, s, "eval_cost_sum");
+        sum_f64_kernel<<<1, 256, 0, s>>>(n->d_cost, nrows, n->d_cost_sum);
+        TRY(lc.done());
+    }
+    unsigned long long c = 0;
+    double cs = 0.0;
+    if (correct_host) HIP_TRY(n, hipMemcpyAsync(&c, n->d_correct, sizeof c, hipMemcpyDeviceToHost, s));
+    if (cost_host) HIP_TRY(n, hipMemcpyAsync(&cs, n->d_cost_sum, sizeof cs, hipMemcpyDeviceToHost, s));
+    HIP_TRY(n, hipStreamSynchronize(s));
+    if (correct_host) *correct_host = (int64_t)c;
+    if (cost_host) *cost_host = cs / (double)nrows;
     return PNN_OK;
 }
 

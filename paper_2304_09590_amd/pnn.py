@@ -70,6 +70,8 @@ def lib() -> ctypes.CDLL:
         L.pnn_merge.restype = i32
         L.pnn_infer.argtypes = [vp, i32, vp, i64, vp, vp, P(i64), vp, vp]
         L.pnn_infer.restype = i32
+        L.pnn_eval.argtypes = [vp, i32, vp, vp, i64, P(i64), P(ctypes.c_double), vp]
+        L.pnn_eval.restype = i32
         L.pnn_get_params.argtypes = [vp, i32, P(ctypes.c_float)]
         L.pnn_get_params.restype = i32
         L.pnn_set_params.argtypes = [vp, i32, P(ctypes.c_float)]
@@ -174,6 +176,15 @@ class PNN:
                                         ctypes.byref(c) if count else None, _dev_ptr(y, "torch.int32"),
                                         _stream_handle(stream)), "pnn_infer")
         return c.value if count else None
+
+    def evaluate(self, x, y, which: int = -1, stream=None):
+        """(correct count, mean cost) of one network on labelled rows (pnn_eval)."""
+        c = ctypes.c_int64(-1)
+        cost = ctypes.c_double(float("nan"))
+        self._check(self._lib.pnn_eval(self.h, which, _dev_ptr(x, "torch.float32"), _dev_ptr(y, "torch.int32"),
+                                       x.shape[0], ctypes.byref(c), ctypes.byref(cost), _stream_handle(stream)),
+                    "pnn_eval")
+        return c.value, cost.value
 
     def get_params(self, which: int = -1) -> np.ndarray:
         out = np.empty(self.P, dtype=np.float32)

@@ -327,3 +327,42 @@ def test_zero_lr_and_determinism_and_resume(idx):
     b.train_epoch(xd, yd)
     assert np.array_equal(np.stack([b.get_params(k) for k in range(4)]), runs[0])
     b.close()
+
+
+# ------------------------------------------------------------------------------------
+# evaluation of the merged network and of single CNs: correct count and mean cost
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4])
+def test_eval_accuracy_and_cost(idx):
+    w = I.WORKLOADS[idx].scaled(replicas=min(4, I.WORKLOADS[idx].replicas))
+    K = w.replicas
+    X, y = I.train_set(w, K * 3 * w.batch + 7)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    net.train_epoch(dev(X), dev(y))
+    net.merge()
+    o = O.Oracle.from_workload(w)
+    Xt, yt = I.test_set(w, 9000 if idx == 1 else 1500)  # (9000 crosses the 8192-row inference chunk)
+    bf = w.precision == I.BF16_MIXED
+    for which in (-1, 0, K - 1):
+        th = net.get_params(which).astype(np.float64)
+        correct, cost = net.evaluate(dev(Xt), dev(yt), which=which)
+        log(f"eval {w.name} which={which}: correct {correct}, cost {cost:.6f}")
+        out = o.forward(th, Xt)
+        ref_correct = int((np.argmax(out, axis=1) == yt).sum())
+        srt = np.sort(out, axis=1)
+        ties = int((srt[:, -1] - srt[:, -2] <= (1e-4 if bf else 1e-5)).sum())
+        assert abs(correct - ref_correct) <= ties, (correct, ref_correct, ties)
+        ref_cost = o.cost(th, Xt, yt)
+        assert np.isfinite(cost)
+        assert abs(cost - ref_cost) <= (1e-3 if bf else 1e-5) * abs(ref_cost), (cost, ref_cost)
+        # the same rows through pnn_infer count the same
+        pred = torch.empty(len(yt), dtype=torch.int32, device="cuda")
+        assert net.infer(dev(Xt), pred, which=which, y=dev(yt), count=True) == correct
+    empty_x = torch.empty((0, w.sizes[0]), dtype=torch.float32, device="cuda")
+    assert net.evaluate(empty_x, dev(np.zeros(0, np.int32))) == (0, 0.0)
+    with pytest.raises(B.PnnError) as ei:
+        net.evaluate(dev(Xt), dev(yt), which=K)
+    assert ei.value.status == B.PNN_EINVAL
+    net.close()
