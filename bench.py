@@ -13,6 +13,16 @@ untimed step), and the CPU oracle timed on the host cores as a baseline.
 
 Default workload: 784-128-10 sigmoid MLP, K = 4 CNs, per-sample SGD, 60,000 samples,
 1 epoch + merge (workload index 1).  --workload selects another.
+
+Two further modes (not the default; one JSON line per measurement):
+  --sweep-k 1,2,4,...  the time to train the workload's whole training set with K CNs for each
+                       K (one epoch + merge), relative to K = 1, on the GPU and for the oracle on
+                       the host cores with one thread per CN (the paper's comparison of training
+                       time against the number of goroutines, section "Comparing the
+                       Performances");
+  --compare-cns E      E epochs of the workload; after each, the held-out accuracy and mean cost
+                       of every CN and of the network merged from them (the paper's comparison of
+                       the CNs' average accuracy with the PNN's, and its cost per epoch).
 """
 from __future__ import annotations
 
@@ -151,6 +161,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one device-to-device copy of 1 GiB (reference dispatch for HBM byte counters)")
+    ap.add_argument("--sweep-k", type=str, default=None,
+                    help="comma-separated CN counts: training time of the whole training set against K")
+    ap.add_argument("--sweep-cpu-samples", type=int, default=4096,
+                    help="samples the oracle trains in each CPU point of --sweep-k (0: GPU only)")
+    ap.add_argument("--compare-cns", type=int, default=0,
+                    help="epochs of the CN-versus-merged-network comparison")
     args = ap.parse_args()
     if args.gpus != 1:
         print("this build runs on one GPU only: the CNs of a PNN are independent until the merge, "
@@ -168,6 +184,11 @@ def main():
         torch.cuda.synchronize()
         print("[bench] calibration copy: 1 GiB read + 1 GiB written", file=sys.stderr, flush=True)
         del src, dst
+
+    if args.sweep_k:
+        return sweep_k(args, torch, B)
+    if args.compare_cns > 0:
+        return compare_cns(args, torch, B)
 
     w = I.WORKLOADS[args.workload]
     N = w.n_train
@@ -296,6 +317,100 @@ def main():
         "kernels": kernels,
     }
     print(json.dumps(out), flush=True)
+    net.close()
+
+
+def _plan_of(net, step) -> str:
+    """Name of the library kernel that takes the most device time in one step."""
+    net.profile(True)
+    step()
+    prof = net.profile_read()
+    net.profile(False)
+    return max(prof.items(), key=lambda kv: kv[1][0])[0] if prof else "?"
+
+
+def sweep_k(args, torch, B):
+    base = I.WORKLOADS[args.workload]
+    N = base.n_train
+    X, y = I.train_set(base)
+    th0 = I.init_params(base)
+    xd = torch.from_numpy(X).cuda()
+    yd = torch.from_numpy(y).cuda()
+    stream = torch.cuda.current_stream()
+    ks = [int(k) for k in args.sweep_k.split(",") if k.strip()]
+    cores = len(os.sched_getaffinity(0))
+    ref_gpu = ref_cpu = None
+    for K in ks:
+        w = base.scaled(replicas=K)
+        net = B.PNN(B.config_from_workload(w), th0)
+
+        def step():
+            for e in range(w.epochs):
+                net.train_epoch(xd, yd, stream=stream)
+                if w.merge_every_epoch:
+                    net.merge(broadcast=True, stream=stream)
+            if not w.merge_every_epoch:
+                net.merge(broadcast=False, stream=stream)
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(args.steps):
+            step()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / args.steps
+        plan = _plan_of(net, step)
+        torch.cuda.synchronize()
+        net.close()
+        ref_gpu = ref_gpu or ms
+        line = {"mode": "sweep_k", "workload": base.name, "replicas": K, "n_train": N, "epochs": w.epochs,
+                "gpu_ms_per_step": round(ms, 4), "gpu_samples_per_s": round(N * w.epochs / (ms / 1e3), 2),
+                "gpu_time_vs_k1": round(ms / ref_gpu, 4), "gpu_plan": plan}
+        if args.sweep_cpu_samples > 0:
+            # the oracle on the host: the same total of samples split over K threads, one per CN
+            from oracle import oracle as O
+            S = max(K, args.sweep_cpu_samples)
+            o = O.Oracle.from_workload(w)
+            th = o.replicate(th0)
+            threads = min(K, cores)
+            t1 = time.time()
+            o.train_epoch(th, X[:S], y[:S], threads=threads)
+            cpu_s = time.time() - t1
+            ref_cpu = ref_cpu or cpu_s
+            line.update({"cpu_samples": S, "cpu_threads": threads, "cpu_s": round(cpu_s, 3),
+                         "cpu_time_vs_k1": round(cpu_s / ref_cpu, 4)})
+        print(json.dumps(line), flush=True)
+
+
+def compare_cns(args, torch, B):
+    w = I.WORKLOADS[args.workload]
+    X, y = I.train_set(w)
+    Xt, yt = I.test_set(w)
+    th0 = I.init_params(w)
+    xd, yd = torch.from_numpy(X).cuda(), torch.from_numpy(y).cuda()
+    xtd, ytd = torch.from_numpy(Xt).cuda(), torch.from_numpy(yt).cuda()
+    net = B.PNN(B.config_from_workload(w), th0)
+    K = w.replicas
+    for e in range(1, args.compare_cns + 1):
+        net.train_epoch(xd, yd)
+        # the merged network of this epoch; the CNs go on from their own parameters unless the
+        # workload merges every epoch (then they restart from the merged network)
+        net.merge(broadcast=False)
+        cn = [net.evaluate(xtd, ytd, which=k) for k in range(K)]
+        pc, pcost = net.evaluate(xtd, ytd, which=-1)
+        acc = np.array([c for c, _ in cn], dtype=np.float64) / len(yt)
+        cost = np.array([c for _, c in cn])
+        print(json.dumps({"mode": "compare_cns", "workload": w.name, "replicas": K, "epoch": e,
+                          "pnn_accuracy": round(pc / len(yt), 5), "pnn_cost": round(pcost, 6),
+                          "cn_mean_accuracy": round(float(acc.mean()), 5),
+                          "cn_min_accuracy": round(float(acc.min()), 5), "cn_max_accuracy": round(float(acc.max()), 5),
+                          "cn_mean_cost": round(float(cost.mean()), 6)}), flush=True)
+        if w.merge_every_epoch:
+            net.merge(broadcast=True)
     net.close()
 
 
