@@ -67,6 +67,7 @@ def lib():
             L.or_train_epoch.argtypes = [cfg, P(d), P(f), P(i32), i64, i32]
             L.or_train_replicas.argtypes = [cfg, P(d), P(i32), i32, P(f), P(i32), i64]
             L.or_merge.argtypes = [cfg, P(d), P(d)]
+            L.or_merge_weighted.argtypes = [cfg, P(d), P(d), P(d)]
             L.or_forward.argtypes = [cfg, P(d), P(f), i64, P(d)]
             L.or_predict.argtypes = [cfg, P(d), P(f), i64, P(i32), P(i32)]
             L.or_predict.restype = i64
@@ -155,6 +156,17 @@ class Oracle:
         assert theta.shape == (self.c.replicas, self.P)
         out = np.empty(self.P, dtype=np.float64)
         lib().or_merge(ctypes.byref(self.c), _ptr(theta, ctypes.c_double), _ptr(out, ctypes.c_double))
+        return out
+
+    def merge_weighted(self, theta: np.ndarray, w: Sequence[float]) -> np.ndarray:
+        """sum_k w_k theta_k / sum_k w_k over the K CNs (weights >= 0, positive sum)."""
+        theta = np.ascontiguousarray(theta, dtype=np.float64)
+        wv = np.ascontiguousarray(w, dtype=np.float64)
+        assert theta.shape == (self.c.replicas, self.P) and wv.shape == (self.c.replicas,)
+        assert np.all(wv >= 0) and wv.sum() > 0
+        out = np.empty(self.P, dtype=np.float64)
+        lib().or_merge_weighted(ctypes.byref(self.c), _ptr(theta, ctypes.c_double), _ptr(wv, ctypes.c_double),
+                                _ptr(out, ctypes.c_double))
         return out
 
     def forward(self, theta: np.ndarray, X: np.ndarray) -> np.ndarray:

@@ -323,6 +323,21 @@ void or_merge(const or_config* c, const double* theta, double* merged)
     }
 }
 
+/* Weighted combination (the paper names other combination functions as open work without
+ * defining one; this is the weighted mean): merged = sum_k w_k theta_k / sum_k w_k, the sums in
+ * long double with k ascending.  w: K non-negative weights with a positive sum. */
+void or_merge_weighted(const or_config* c, const double* theta, const double* w, double* merged)
+{
+    const int64_t P = or_param_count(c);
+    long double ws = 0.0L;
+    for (int k = 0; k < c->replicas; ++k) ws += (long double)w[k];
+    for (int64_t i = 0; i < P; ++i) {
+        long double s = 0.0L;
+        for (int k = 0; k < c->replicas; ++k) s += (long double)w[k] * (long double)theta[(int64_t)k * P + i];
+        merged[i] = (double)(s / ws);
+    }
+}
+
 /* Forward pass of one network over n samples; out [n][sizes[L]] receives x^L. */
 void or_forward(const or_config* c, const double* th, const float* X, int64_t n, double* out)
 {

@@ -305,6 +305,35 @@ def test_merge_of_k_is_mean_index(K):
     assert np.all(o.merge(th) == (K - 1) / 2)
 
 
+@pytest.mark.parametrize("K", [2, 5, 64, 256])
+def test_weighted_merge_closed_form(K):
+    # theta_k = k everywhere, w_k = k + 1: sum k (k + 1) / sum (k + 1) = 2 (K - 1) / 3
+    o = O.Oracle((3, 2), (O.SIGMOID,), O.LOSS_MSE, replicas=K)
+    th = np.repeat(np.arange(K, dtype=np.float64)[:, None], o.P, axis=1)
+    got = o.merge_weighted(th, np.arange(1, K + 1, dtype=np.float64))
+    np.testing.assert_allclose(got, 2.0 * (K - 1) / 3.0, rtol=1e-15, atol=0)
+
+
+def test_weighted_merge_special_cases():
+    K = 6
+    o = O.Oracle((6, 5, 3), (O.SIGMOID, O.SIGMOID), O.LOSS_MSE, replicas=K)
+    th = np.stack([np.asarray(I.random_params((6, 5, 3), seed=300 + k), np.float64) for k in range(K)])
+    # equal weights: the plain average
+    np.testing.assert_allclose(o.merge_weighted(th, [2.5] * K), o.merge(th), rtol=1e-15, atol=1e-18)
+    # a one-hot weight selects that CN exactly
+    for j in (0, 3):
+        w = np.zeros(K)
+        w[j] = 0.7
+        assert np.array_equal(o.merge_weighted(th, w), th[j])
+    # scaling every weight changes nothing; a weight of 2 counts a CN twice
+    w = np.array([1.0, 2.0, 0.0, 3.0, 1.0, 0.5])
+    np.testing.assert_allclose(o.merge_weighted(th, 4 * w), o.merge_weighted(th, w), rtol=1e-15, atol=1e-18)
+    dup = np.concatenate([th, th[1:2]])
+    o7 = O.Oracle((6, 5, 3), (O.SIGMOID, O.SIGMOID), O.LOSS_MSE, replicas=K + 1)
+    w7 = np.array([1.0, 1.0, 0.0, 3.0, 1.0, 0.5, 1.0])
+    np.testing.assert_allclose(o.merge_weighted(th, w), o7.merge_weighted(dup, w7), rtol=1e-14, atol=1e-17)
+
+
 def test_merge_is_the_mean():
     K = 5
     o = O.Oracle((6, 5, 3), (O.SIGMOID, O.SIGMOID), O.LOSS_MSE, replicas=K)
