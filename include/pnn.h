@@ -107,6 +107,16 @@ pnn_status pnn_train_epoch(pnn_net* net, const float* x_dev, const int32_t* y_de
  * between epochs). */
 pnn_status pnn_merge(pnn_net* net, int32_t broadcast, void* hip_stream);
 
+/* Weighted combination: the paper notes that CNs can be combined in several ways and leaves
+ * better combination functions to future work (sections "Parallel Neuronal Networks" and
+ * "Findings and Conclusion") without defining one; this one is the weighted mean:
+ * merged := sum_k w_k theta_k / sum_k w_k, each product and the sum in fp64 with k ascending,
+ * rounded once to fp32.  weights_host: K host doubles, each finite and >= 0, with a positive sum
+ * (PNN_EINVAL otherwise, nothing launched).  Equal weights give pnn_merge's result bitwise.
+ * broadcast as in pnn_merge.  The weights are copied to a library-owned device array before
+ * the call returns (the call waits for the stream's earlier work). */
+pnn_status pnn_merge_weighted(pnn_net* net, const double* weights_host, int32_t broadcast, void* hip_stream);
+
 /* Classification (sections "Fundamentals" and "MNIST Dataset": one output neuron per class,
  * tested on unseen data).  which = -1 uses the merged network, 0..K-1 one CN.
  * x_dev [n][sizes[0]] fp32.  pred_dev [n] int32 receives the argmax of the outputs (lowest

@@ -323,9 +323,10 @@ void or_merge(const or_config* c, const double* theta, double* merged)
     }
 }
 
-/* Weighted combination (the paper names other combination functions as open work without
- * defining one; this is the weighted mean): merged = sum_k w_k theta_k / sum_k w_k, the sums in
- * long double with k ascending.  w: K non-negative weights with a positive sum. */
+/* Weighted combination (sections "Parallel Neuronal Networks" and "Findings and Conclusion"
+ * leave combination functions other than the average open without defining one; this is the
+ * weighted mean): merged = sum_k w_k theta_k / sum_k w_k, the sums in long double with k
+ * ascending.  w: K non-negative weights with a positive sum. */
 void or_merge_weighted(const or_config* c, const double* theta, const double* w, double* merged)
 {
     const int64_t P = or_param_count(c);

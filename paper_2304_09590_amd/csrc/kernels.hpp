@@ -1218,17 +1218,27 @@ struct MergeArgs {
     int64_t pstride;    // multiple of 4
     int K;
     int broadcast;
+    const double* w;    // nullable: weights of the CNs (weighted combination)
+    double wsum;        // sum of the weights (K without weights)
 };
 
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     const int64_t p = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
     if (p >= a.pstride) return;
     double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    for (int k = 0; k < a.K; ++k) {
-        const float4 v = *(const float4*)(a.theta + (size_t)k * a.pstride + p);
-        s0 += (double)v.x; s1 += (double)v.y; s2 += (double)v.z; s3 += (double)v.w;
+    if (a.w == nullptr) {
+        for (int k = 0; k < a.K; ++k) {
+            const float4 v = *(const float4*)(a.theta + (size_t)k * a.pstride + p);
+            s0 += (double)v.x; s1 += (double)v.y; s2 += (double)v.z; s3 += (double)v.w;
+        }
+    } else {
+        for (int k = 0; k < a.K; ++k) {
+            const float4 v = *(const float4*)(a.theta + (size_t)k * a.pstride + p);
+            const double wk = a.w[k];
+            s0 += wk * (double)v.x; s1 += wk * (double)v.y; s2 += wk * (double)v.z; s3 += wk * (double)v.w;
+        }
     }
-    const double inv = (double)a.K;
+    const double inv = a.wsum;
     const float4 m = make_float4((float)(s0 / inv), (float)(s1 / inv), (float)(s2 / inv), (float)(s3 / inv));
     *(float4*)(a.merged + p) = m;
     if (a.mshadow) {

@@ -70,6 +70,7 @@ struct pnn_net {
     double* d_cost = nullptr;     // [cost_rows] per-row costs of an evaluation
     int64_t cost_rows = 0;
     double* d_cost_sum = nullptr;
+    double* d_mw = nullptr;       // [K] weights of a weighted combination
 
     // chunked per-sample plan
     bool psgd = false;
@@ -630,7 +631,7 @@ void free_all(pnn_net* n) {
     auto f = [](void* p) { if (p) (void)hipFree(p); };
     f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
     for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
-    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
+    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
     for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : n->free_events) (void)hipEventDestroy(e);
 }
@@ -716,6 +717,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
     }
     if ((st = dev_alloc(n, &n->d_correct, 1)) != PNN_OK) return bail(st);
     if ((st = dev_alloc(n, &n->d_cost_sum, 1)) != PNN_OK) return bail(st);
+    if ((st = dev_alloc(n, &n->d_mw, (size_t)K)) != PNN_OK) return bail(st);
 
     n->psgd = (B == 1 && n->L == 2 && !n->bf16 && n->sizes[1] <= 1024 && n->sizes[2] <= MAX_OUT);
     if (n->psgd) {
@@ -829,18 +831,40 @@ pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev,
     return PNN_OK;
 }
 
-pnn_status pnn_merge(pnn_net* n, int32_t broadcast, void* hip_stream) {
-    TRY(usable(n));
-    hipStream_t s = (hipStream_t)hip_stream;
+static pnn_status launch_merge(pnn_net* n, int32_t broadcast, const double* w_dev, double wsum, hipStream_t s) {
     MergeArgs a;
     a.theta = n->theta; a.merged = n->merged;
     a.shadow = n->bf16 ? n->shadow : nullptr;
     a.mshadow = n->bf16 ? n->mshadow : nullptr;
     a.pstride = n->pstride; a.K = n->cfg.replicas; a.broadcast = broadcast ? 1 : 0;
+    a.w = w_dev; a.wsum = wsum;
     const int64_t q = n->pstride / 4;
     Launch l(n, s, "merge");
     merge_kernel<<<(unsigned)((q + 255) / 256), 256, 0, s>>>(a);
     return l.done();
+}
+
+pnn_status pnn_merge(pnn_net* n, int32_t broadcast, void* hip_stream) {
+    TRY(usable(n));
+    return launch_merge(n, broadcast, nullptr, (double)n->cfg.replicas, (hipStream_t)hip_stream);
+}
+
+pnn_status pnn_merge_weighted(pnn_net* n, const double* weights_host, int32_t broadcast, void* hip_stream) {
+    TRY(usable(n));
+    if (!weights_host) return fail(n, PNN_EINVAL, "weights_host is NULL");
+    const int K = n->cfg.replicas;
+    double ws = 0.0;
+    for (int k = 0; k < K; ++k) {
+        const double v = weights_host[k];
+        if (!(v >= 0.0) || !std::isfinite(v)) return fail(n, PNN_EINVAL, "weight %d is %g (must be finite and >= 0)", k, v);
+        ws += v;
+    }
+    if (!(ws > 0.0) || !std::isfinite(ws)) return fail(n, PNN_EINVAL, "the weights sum to %g (must be positive)", ws);
+    hipStream_t s = (hipStream_t)hip_stream;
+    // the weights travel with the launch's stream order (the copy waits for earlier work)
+    HIP_TRY(n, hipMemcpyAsync(n->d_mw, weights_host, sizeof(double) * K, hipMemcpyHostToDevice, s));
+    HIP_TRY(n, hipStreamSynchronize(s));
+    return launch_merge(n, broadcast, n->d_mw, ws, s);
 }
 
 // forward pass of one network over nrows data-set rows in chunks, then the output layer:

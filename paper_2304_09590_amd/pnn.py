@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
         L.pnn_infer.argtypes = [vp, i32, vp, i64, vp, vp, P(i64), vp, vp]
         L.pnn_infer.restype = i32
         L.pnn_eval.argtypes = [vp, i32, vp, vp, i64, P(i64), P(ctypes.c_double), vp]
+        L.pnn_merge_weighted.argtypes = [vp, P(ctypes.c_double), i32, vp]
+        L.pnn_merge_weighted.restype = i32
         L.pnn_eval.restype = i32
         L.pnn_get_params.argtypes = [vp, i32, P(ctypes.c_float)]
         L.pnn_get_params.restype = i32
@@ -146,6 +148,7 @@ class PNN:
         self._lib = lib()
         self.cfg = cfg
         self.P = param_count(cfg)
+        self.K = int(cfg.replicas)
         if self.P == 0:
             raise PnnError(PNN_EINVAL, "invalid configuration")
         th = np.ascontiguousarray(theta0, dtype=np.float32)
@@ -176,6 +179,13 @@ class PNN:
                                         ctypes.byref(c) if count else None, _dev_ptr(y, "torch.int32"),
                                         _stream_handle(stream)), "pnn_infer")
         return c.value if count else None
+
+    def merge_weighted(self, weights, broadcast: bool = False, stream=None) -> None:
+        w = np.ascontiguousarray(weights, dtype=np.float64)
+        if w.shape != (self.K,):
+            raise ValueError(f"expected {self.K} weights, got shape {w.shape}")
+        self._check(self._lib.pnn_merge_weighted(self.h, w.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                                 1 if broadcast else 0, _stream_handle(stream)), "pnn_merge_weighted")
 
     def evaluate(self, x, y, which: int = -1, stream=None):
         """(correct count, mean cost) of one network on labelled rows (pnn_eval)."""

@@ -401,3 +401,44 @@ def test_per_sample_stepwise_tanh_xent():
         prev = got.astype(np.float64)
     net.close()
 
+
+
+# ------------------------------------------------------------------------------------
+# weighted combination
+
+
+@pytest.mark.parametrize("idx", [2, 3])
+def test_weighted_merge(idx):
+    w = I.WORKLOADS[idx].scaled(replicas=4)
+    K = w.replicas
+    X, y = I.train_set(w, K * 2 * w.batch + 3)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    net.train_epoch(dev(X), dev(y))
+    cns = np.stack([net.get_params(k) for k in range(K)]).astype(np.float64)
+    o = O.Oracle.from_workload(w)
+    wts = np.array([0.5, 1.0, 2.0, 0.25])
+    net.merge_weighted(wts)
+    got = net.get_params(-1)
+    ref = o.merge_weighted(cns, wts).astype(np.float32)
+    np.testing.assert_allclose(got, ref, rtol=1.2e-7, atol=0)
+    # the merged network's bf16 copy follows: its evaluation matches the oracle's on those weights
+    Xt, yt = I.test_set(w, 1000)
+    _, cost = net.evaluate(dev(Xt), dev(yt))
+    ref_cost = o.cost(got.astype(np.float64), Xt, yt)
+    assert abs(cost - ref_cost) <= (1e-3 if w.precision == I.BF16_MIXED else 1e-5) * abs(ref_cost)
+    # equal weights: the plain average, bitwise
+    net.merge()
+    plain = net.get_params(-1)
+    net.merge_weighted(np.full(K, 3.0))
+    assert np.array_equal(net.get_params(-1), plain)
+    # broadcast: every CN continues from the weighted mean
+    net.merge_weighted(wts, broadcast=True)
+    m = net.get_params(-1)
+    for k in range(K):
+        assert np.array_equal(net.get_params(k), m)
+    for bad in ([-1.0, 1.0, 1.0, 1.0], [0.0, 0.0, 0.0, 0.0], [1.0, float("nan"), 1.0, 1.0]):
+        with pytest.raises(B.PnnError) as ei:
+            net.merge_weighted(np.array(bad))
+        assert ei.value.status == B.PNN_EINVAL
+    net.close()
