@@ -101,6 +101,17 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
  * (but memory-safe) update. */
 pnn_status pnn_train_epoch(pnn_net* net, const float* x_dev, const int32_t* y_dev, int64_t N, void* hip_stream);
 
+/* One epoch over the rows in a given order (the per-epoch shuffling that the paper leaves
+ * open: it trains on the slices in their stored order).  Equivalent to pnn_train_epoch on
+ * x[order[0..N)], y[order[0..N)]: epoch row r is data-set row order_dev[r], and the K slices
+ * are the contiguous ranges of that sequence.  order_dev [N] int32 on the device, normally a
+ * permutation drawn by the caller from a seeded generator (within each slice's range for a
+ * per-CN shuffle); entries outside [0, N) select row 0.  The rows are gathered into a
+ * library-owned staging copy (N x sizes[0] floats, grown with hipMalloc when a larger N
+ * arrives) on the caller's stream.  Errors as pnn_train_epoch; N must fit int32. */
+pnn_status pnn_train_epoch_order(pnn_net* net, const float* x_dev, const int32_t* y_dev, int64_t N,
+                                 const int32_t* order_dev, void* hip_stream);
+
 /* Combination by averaging (section "Implementation Details"): merged := (1/K) sum_k theta_k
  * for every weight and bias, accumulated in fp64 with k ascending, rounded once to fp32.
  * broadcast != 0 also copies the merged network back into every CN (model averaging

@@ -2479,6 +2479,23 @@ __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
     }
 }
 
+// Rows of an epoch in a given order: row r of (xo, yo) is data-set row order[r] (entries
+// outside [0, N) select row 0).  One workgroup per row.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const float* x, const int32_t* y, const int32_t* order,
+                                                          int64_t N, int D, float* xo, int32_t* yo) {
+    const int64_t r = blockIdx.x;
+    int64_t src = order[r];
+    if (src < 0 || src >= N) src = 0;
+    const float* xs = x + (size_t)src * D;
+    float* xd = xo + (size_t)r * D;
+    if ((D & 3) == 0) {
+        for (int c = threadIdx.x; c < D / 4; c += 256) ((float4*)xd)[c] = ((const float4*)xs)[c];
+    } else {
+        for (int c = threadIdx.x; c < D; c += 256) xd[c] = xs[c];
+    }
+    if (threadIdx.x == 0) yo[r] = y[src];
+}
+
 // sum of n doubles in a fixed order (thread t takes t, t + 256, ...; then a fixed tree)
 __global__ __launch_bounds__(256) void sum_f64_kernel(const double* v, int64_t n, double* out) {
     __shared__ double part[256];

@@ -71,6 +71,9 @@ struct pnn_net {
     int64_t cost_rows = 0;
     double* d_cost_sum = nullptr;
     double* d_mw = nullptr;       // [K] weights of a weighted combination
+    float* ord_x = nullptr;       // [ord_rows][sizes[0]] rows of an epoch in a given order
+    int32_t* ord_y = nullptr;
+    int64_t ord_rows = 0;
 
     // chunked per-sample plan
     bool psgd = false;
@@ -631,7 +634,7 @@ void free_all(pnn_net* n) {
     auto f = [](void* p) { if (p) (void)hipFree(p); };
     f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
     for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
-    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
+    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ord_x); f(n->ord_y); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
     for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : n->free_events) (void)hipEventDestroy(e);
 }
@@ -829,6 +832,31 @@ pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev,
         else TRY(minibatch_step<false>(n, x_dev, y_dev, N, r0, s));
     }
     return PNN_OK;
+}
+
+pnn_status pnn_train_epoch_order(pnn_net* n, const float* x_dev, const int32_t* y_dev, int64_t N,
+                                 const int32_t* order_dev, void* hip_stream) {
+    TRY(usable(n));
+    if (!x_dev || !y_dev || !order_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev / order_dev is NULL");
+    if (N < n->cfg.replicas) return fail(n, PNN_ESHAPE, "N = %lld < K = %d leaves a slice empty", (long long)N, n->cfg.replicas);
+    if (N > INT32_MAX) return fail(n, PNN_ESHAPE, "N = %lld does not fit the int32 order", (long long)N);
+    hipStream_t s = (hipStream_t)hip_stream;
+    const int D = n->sizes[0];
+    if (N > n->ord_rows) {
+        HIP_TRY(n, hipStreamSynchronize(s));
+        if (n->ord_x) (void)hipFree(n->ord_x);
+        if (n->ord_y) (void)hipFree(n->ord_y);
+        n->ord_x = nullptr; n->ord_y = nullptr; n->ord_rows = 0;
+        TRY(dev_alloc(n, &n->ord_x, (size_t)N * D));
+        TRY(dev_alloc(n, &n->ord_y, (size_t)N));
+        n->ord_rows = N;
+    }
+    {
+        Launch l(n, s, "gather_rows");
+        gather_rows_kernel<<<(unsigned)N, 256, 0, s>>>(x_dev, y_dev, order_dev, N, D, n->ord_x, n->ord_y);
+        TRY(l.done());
+    }
+    return pnn_train_epoch(n, n->ord_x, n->ord_y, N, hip_stream);
 }
 
 static pnn_status launch_merge(pnn_net* n, int32_t broadcast, const double* w_dev, double wsum, hipStream_t s) {

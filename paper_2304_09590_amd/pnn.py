@@ -72,6 +72,8 @@ def lib() -> ctypes.CDLL:
         L.pnn_infer.restype = i32
         L.pnn_eval.argtypes = [vp, i32, vp, vp, i64, P(i64), P(ctypes.c_double), vp]
         L.pnn_merge_weighted.argtypes = [vp, P(ctypes.c_double), i32, vp]
+        L.pnn_train_epoch_order.argtypes = [vp, vp, vp, i64, vp, vp]
+        L.pnn_train_epoch_order.restype = i32
         L.pnn_merge_weighted.restype = i32
         L.pnn_eval.restype = i32
         L.pnn_get_params.argtypes = [vp, i32, P(ctypes.c_float)]
@@ -168,6 +170,12 @@ class PNN:
     def train_epoch(self, x, y, stream=None) -> None:
         self._check(self._lib.pnn_train_epoch(self.h, _dev_ptr(x, "torch.float32"), _dev_ptr(y, "torch.int32"),
                                               x.shape[0], _stream_handle(stream)), "pnn_train_epoch")
+
+    def train_epoch_order(self, x, y, order, stream=None) -> None:
+        """One epoch over x[order], y[order] (order: int32 device tensor of N row indices)."""
+        self._check(self._lib.pnn_train_epoch_order(self.h, _dev_ptr(x, "torch.float32"), _dev_ptr(y, "torch.int32"),
+                                                    x.shape[0], _dev_ptr(order, "torch.int32"),
+                                                    _stream_handle(stream)), "pnn_train_epoch_order")
 
     def merge(self, broadcast: bool = False, stream=None) -> None:
         self._check(self._lib.pnn_merge(self.h, 1 if broadcast else 0, _stream_handle(stream)), "pnn_merge")

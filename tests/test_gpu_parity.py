@@ -442,3 +442,40 @@ def test_weighted_merge(idx):
             net.merge_weighted(np.array(bad))
         assert ei.value.status == B.PNN_EINVAL
     net.close()
+
+
+# ------------------------------------------------------------------------------------
+# epochs over a caller-given order (seeded per-epoch shuffling)
+
+
+@pytest.mark.parametrize("idx,K", [(1, 3), (2, 4)])
+def test_train_epoch_order(idx, K):
+    w = I.WORKLOADS[idx].scaled(replicas=K)
+    N = K * (70 if w.batch == 1 else 3 * w.batch) + 2
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    a = make_net(w, th0)
+    b = make_net(w, th0)
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    xd, yd = dev(X), dev(y)
+    for epoch in range(2):
+        # a per-CN shuffle: each slice permuted within its own range, seeded per epoch
+        rng = np.random.Generator(np.random.PCG64(1000 + epoch))
+        order = np.concatenate([s + rng.permutation(n) for s, n in (o.shard(N, k) for k in range(K))]).astype(np.int32)
+        a.train_epoch_order(xd, yd, dev(order))
+        b.train_epoch(dev(X[order]), dev(y[order]))
+        o.train_epoch(ref, X[order], y[order], threads=K)
+    for k in range(K):
+        assert np.array_equal(a.get_params(k), b.get_params(k))
+        assert_close(w.sizes, a.get_params(k), ref[k], EPOCH_TOL, f"replica {k}")
+    # entries outside [0, N) select row 0
+    bad = np.arange(N, dtype=np.int32)
+    bad[1], bad[N - 1] = -5, N + 3
+    fix = bad.copy()
+    fix[1] = fix[N - 1] = 0
+    a.train_epoch_order(xd, yd, dev(bad))
+    b.train_epoch(dev(X[fix]), dev(y[fix]))
+    assert np.array_equal(a.get_params(0), b.get_params(0))
+    a.close()
+    b.close()
