@@ -2226,9 +2226,18 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 const int c = pub / NB, b = pub % NB, tc = chunk_len(c);
                 float* dout = a.d1 + ((size_t)(c & 1) * K + k) * T * H;  // [h][T] errors of chunk c
                 const int s0 = BS * b;
-                for (int q = lane; q < H * (BS / 4); q += 64) {
-                    const int hh = q / (BS / 4), s4 = s0 + (q % (BS / 4)) * 4;
-                    *(float4*)(dout + (size_t)hh * T + s4) = *(const float4*)(hist + hh * TS + s4);
+                // all of the lane's LDS reads first, then the stores (HW * BS / 4 float4 per block)
+                constexpr int NQ = HW * (BS / 4) / 64;
+                float4 dv[NQ];
+#pragma unroll
+                for (int i = 0; i < NQ; ++i) {
+                    const int q = lane + 64 * i, hh = q / (BS / 4), s4 = s0 + (q % (BS / 4)) * 4;
+                    dv[i] = *(const float4*)(hist + hh * TS + s4);
+                }
+#pragma unroll
+                for (int i = 0; i < NQ; ++i) {
+                    const int q = lane + 64 * i, hh = q / (BS / 4), s4 = s0 + (q % (BS / 4)) * 4;
+                    if (hh < H) *(float4*)(dout + (size_t)hh * T + s4) = dv[i];
                 }
                 ++pub;
                 lds_publish(pubd, pub);  // (the hist reads completed: the stores consumed them)
