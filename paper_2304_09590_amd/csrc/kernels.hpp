@@ -1899,9 +1899,9 @@ __device__ inline void lds_publish(int* f, int v) {
 // Who adds which term d1_s (x_s . x_r) of row r (block B):
 //   s < BS(B-1):        folded into the stored input sums Pl of row r in the background, on
 //                       the matrix cores, a whole block at a time;
-//   s in [BS(B-1), r-5]: the window correction cpre[r] (at most 2 BS - 5 terms), computed by
-//                       wave 1 while the live wave runs steps r-4 to r-1;
-//   s = r-4 .. r-1:     the live wave, with its own fresh errors.
+//   s in [BS(B-1), r-6]: the window correction cpre[r] (at most 2 BS - 6 terms), computed by
+//                       wave 1 while the live wave runs steps r-5 to r-1;
+//   s = r-5 .. r-1:     the live wave, with its own fresh errors.
 //
 // Waves (256 threads), each in its own loop, coordinated through counters in LDS:
 //   wave 0, live:  the steps.  Lane l owns hidden neurons l and l + 64 (NH = 2) or l
@@ -1939,8 +1939,8 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     float* hist = Pl + HW * TS;         // [HW][TS]   first-layer errors by step mod T
     float* Gin = hist + HW * TS;        // [2][T][GS] Gram blocks within a chunk, by parity
     float* GX = Gin + 2 * T * GS;       // [T][GS]    a chunk (rows) against the previous one
-    float* cpre = GX + T * GS;          // [4][HW]    window corrections by row mod 4
-    int* yb = (int*)(cpre + 4 * HW);    // [2][T]     labels by chunk parity
+    float* cpre = GX + T * GS;          // [8][HW]    window corrections by row mod 8
+    int* yb = (int*)(cpre + 8 * HW);    // [2][T]     labels by chunk parity
     int* lf = yb + 2 * T;
     int* d1done = lf;
     int* cdone = lf + 1;
@@ -1986,7 +1986,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         const int act1 = A1 >= 0 ? A1 : a.act1;
         const int act2 = A2 >= 0 ? A2 : a.act2;
         const int loss = LS >= 0 ? LS : a.loss;
-        float w2[NH][OC], b1[NH], corr[NH], dprev[NH], dprev2[NH], dprev3[NH], pln[NH];
+        float w2[NH][OC], b1[NH], corr[NH], dprev[NH], dprev2[NH], dprev3[NH], dprev4[NH], pln[NH];
         const int ol = lane & 15;
         const int own = OC == 10 ? own10(ol) : ol;  // output whose total this lane holds
         const bool owner = own >= 0 && own < O;
@@ -2000,6 +2000,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             dprev[j] = 0.f;
             dprev2[j] = 0.f;
             dprev3[j] = 0.f;
+            dprev4[j] = 0.f;
             pln[j] = Pl[h * TS];
         }
         float b2v = owner ? th[a.off_b2 + own] : 0.f;
@@ -2035,7 +2036,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             float cp[NH], pnx[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) pnx[j] = Pl[(lane + 64 * j) * TS + tn];
-            // Gram entries of the next row against steps r .. r-3: within the next row's chunk
+            // Gram entries of the next row against steps r .. r-4: within the next row's chunk
             // from its G block, against the chunk before it from GX (which holds the next
             // row's chunk against the previous one whenever the next row needs it)
             const float* gin = grow_in(cn) + tn * GS;
@@ -2047,6 +2048,8 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             const float g2v = (cross || t < 2) ? gx[tp2] : gin[tp2];
             const int tp3 = (t + T - 3) & (T - 1);     // position of step r-3 in its chunk
             const float g3v = (cross || t < 3) ? gx[tp3] : gin[tp3];
+            const int tp4 = (t + T - 4) & (T - 1);     // position of step r-4 in its chunk
+            const float g4v = (cross || t < 4) ? gx[tp4] : gin[tp4];
             const int labn = yb[(cn & 1) * T + tn];
 
             float a1[NH], na[NH];
@@ -2080,7 +2083,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             const int cd = __hip_atomic_load(cdone, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             asm volatile("" ::: "memory");
 #pragma unroll
-            for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 3) * HW + lane + 64 * j];
+            for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 7) * HW + lane + 64 * j];
             float x2;
             if (act2 == ACT_SOFTMAX) {
                 const float m = row_allmax16(owner ? z2 : -INFINITY);
@@ -2111,18 +2114,20 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             if (more && __builtin_amdgcn_readfirstlane(cd) < r + 2) {
                 lds_wait_geq(cdone, r + 2, lab, gabort, a.spin_limit, false);
 #pragma unroll
-                for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 3) * HW + lane + 64 * j];
+                for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 7) * HW + lane + 64 * j];
                 __builtin_amdgcn_s_waitcnt(0xC07F);  // (slow path) lgkmcnt(0) here, not after the join
             }
-            // terms of steps r .. r-3 (all four lie in the next row's two-block window, not
-            // yet folded: they are at most four steps back).  Also done after the last step
+            // terms of steps r .. r-4 (all five lie in the next row's two-block window, not
+            // yet folded: they are at most five steps back).  Also done after the last step
             // (unused then): every path consumes the loads it issued, so none is still in
             // flight into a register at the loop head.
             {
                 const float g1 = g1v, g0 = r >= 1 ? g0v : 0.f, g2 = r >= 2 ? g2v : 0.f, g3 = r >= 3 ? g3v : 0.f;
+                const float g4 = r >= 4 ? g4v : 0.f;
 #pragma unroll
                 for (int j = 0; j < NH; ++j) {
-                    corr[j] = cp[j] + dprev3[j] * g3 + dprev2[j] * g2 + dprev[j] * g0 + d1[j] * g1;
+                    corr[j] = cp[j] + dprev4[j] * g4 + dprev3[j] * g3 + dprev2[j] * g2 + dprev[j] * g0 + d1[j] * g1;
+                    dprev4[j] = dprev3[j];
                     dprev3[j] = dprev2[j];
                     dprev2[j] = dprev[j];
                     dprev[j] = d1[j];
@@ -2148,19 +2153,19 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         if (lane < 16 && owner) th[a.off_b2 + own] = b2v;
     } else if (wave == 1) {
         // ================= window corrections: for row q = r + 1 (block B = q / BS),
-        // cpre[q] = sum over s in [BS(B-1), q-5] of d1_s (x_s . x_q)
+        // cpre[q] = sum over s in [BS(B-1), q-6] of d1_s (x_s . x_q)
         for (int r = 0; r + 1 < nsteps; ++r) {
             const int q = r + 1;
             const int cq = q >> 6, tq = q & (T - 1), B = q / BS;
-            // the live wave has finished step r-4: d1 up to q-5 is in hist and the slot
-            // (q & 3) (last holding the correction of row q-4, read in step q-5) is free
-            lds_wait_geq(d1done, r - 3, lab, gabort, a.spin_limit, false);
+            // the live wave has finished step r-5: d1 up to q-6 is in hist.  The slot (q & 7)
+            // last held the correction of row q-8, read in step q-9: long free.
+            lds_wait_geq(d1done, r - 4, lab, gabort, a.spin_limit, false);
             // a chunk's first rows read its Gram blocks (and GX) before the live wave enters it
             if (tq < BS && cq >= 1) lds_wait_geq(gready, cq + 1, lab, gabort, a.spin_limit, true);
             float sum[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) sum[j] = 0.f;
-            const int lo = max(0, BS * (B - 1)), hi = q - 5;  // inclusive range
+            const int lo = max(0, BS * (B - 1)), hi = q - 6;  // inclusive range
             // two aligned groups of BS steps: the previous block and the row's own block
 #pragma unroll
             for (int part = 0; part < 2; ++part) {
@@ -2188,7 +2193,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 }
             }
 #pragma unroll
-            for (int j = 0; j < NH; ++j) cpre[(q & 3) * HW + lane + 64 * j] = sum[j];
+            for (int j = 0; j < NH; ++j) cpre[(q & 7) * HW + lane + 64 * j] = sum[j];
             lds_publish(cdone, q + 1);
         }
     } else {

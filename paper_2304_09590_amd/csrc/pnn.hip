@@ -731,9 +731,9 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         const int nrb = (H + 15) / 16;
         const int HW = live_width(H);
         // input sums [HW][T+4], errors [HW][T+4], Gram blocks 3 x [T][T+4], window
-        // corrections [4][HW], labels [2][T], 12 counters
+        // corrections [8][HW], labels [2][T], 12 counters
         const size_t rec_smem =
-            (size_t)(2 * HW * (PT + 4) + 3 * PT * (PT + 4) + 4 * HW + 2 * PT + 12) * sizeof(float);
+            (size_t)(2 * HW * (PT + 4) + 3 * PT * (PT + 4) + 8 * HW + 2 * PT + 12) * sizeof(float);
         const size_t tile_smem = (size_t)4 * (PT / 16) * 64 * 4 * sizeof(float);
         n->psmem = std::max(rec_smem, tile_smem);
         n->pspecial = n->act[0] == PNN_SIGMOID && n->act[1] == PNN_SIGMOID && cfg->loss == PNN_LOSS_MSE && O == 10;
