@@ -1901,7 +1901,7 @@ __device__ inline void lds_publish(int* f, int v) {
 //                       the matrix cores, a whole block at a time;
 //   s in [BS(B-1), r-6]: the window correction cpre[r] (at most 2 BS - 6 terms), computed by
 //                       wave 1 while the live wave runs steps r-5 to r-1;
-//   s = r-5 .. r-1:     the live wave, with its own fresh errors.
+//   s = r-5 .. r-1:     the live wave, with its own fresh errors (NLIVE = 5 terms).
 //
 // Waves (256 threads), each in its own loop, coordinated through counters in LDS:
 //   wave 0, live:  the steps.  Lane l owns hidden neurons l and l + 64 (NH = 2) or l
@@ -1929,6 +1929,8 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     constexpr int TS = T + 4;       // row stride of the error history ([neuron][step in chunk])
     constexpr int GS = T + 4;       // row stride of the Gram blocks (conflict-free MFMA operand reads)
     constexpr int BS = 8;           // steps per fold block
+    constexpr int NLIVE = 5;        // latest errors whose terms the live wave adds itself (<= BS; the
+                                    // live step below is written out for five)
     constexpr int NB = T / BS;      // blocks per chunk
     static_assert(T == 64, "chunks of 64 steps");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -2036,7 +2038,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
             float cp[NH], pnx[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) pnx[j] = Pl[(lane + 64 * j) * TS + tn];
-            // Gram entries of the next row against steps r .. r-4: within the next row's chunk
+            // Gram entries of the next row against steps r .. r-4 (NLIVE): within the next row's chunk
             // from its G block, against the chunk before it from GX (which holds the next
             // row's chunk against the previous one whenever the next row needs it)
             const float* gin = grow_in(cn) + tn * GS;
@@ -2117,8 +2119,8 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 for (int j = 0; j < NH; ++j) cp[j] = cpre[(rn & 7) * HW + lane + 64 * j];
                 __builtin_amdgcn_s_waitcnt(0xC07F);  // (slow path) lgkmcnt(0) here, not after the join
             }
-            // terms of steps r .. r-4 (all five lie in the next row's two-block window, not
-            // yet folded: they are at most five steps back).  Also done after the last step
+            // terms of steps r .. r-4, the NLIVE latest (all lie in the next row's two-block
+            // window, not yet folded: they are at most five steps back).  Also done after the last step
             // (unused then): every path consumes the loads it issued, so none is still in
             // flight into a register at the loop head.
             {
@@ -2153,19 +2155,19 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
         if (lane < 16 && owner) th[a.off_b2 + own] = b2v;
     } else if (wave == 1) {
         // ================= window corrections: for row q = r + 1 (block B = q / BS),
-        // cpre[q] = sum over s in [BS(B-1), q-6] of d1_s (x_s . x_q)
+        // cpre[q] = sum over s in [BS(B-1), q-1-NLIVE] of d1_s (x_s . x_q)
         for (int r = 0; r + 1 < nsteps; ++r) {
             const int q = r + 1;
             const int cq = q >> 6, tq = q & (T - 1), B = q / BS;
-            // the live wave has finished step r-5: d1 up to q-6 is in hist.  The slot (q & 7)
-            // last held the correction of row q-8, read in step q-9: long free.
-            lds_wait_geq(d1done, r - 4, lab, gabort, a.spin_limit, false);
+            // the live wave has finished step q-1-NLIVE: d1 up to there is in hist.  The slot
+            // (q & 7) last held the correction of row q-8, read in step q-9: free.
+            lds_wait_geq(d1done, r + 1 - NLIVE, lab, gabort, a.spin_limit, false);
             // a chunk's first rows read its Gram blocks (and GX) before the live wave enters it
             if (tq < BS && cq >= 1) lds_wait_geq(gready, cq + 1, lab, gabort, a.spin_limit, true);
             float sum[NH];
 #pragma unroll
             for (int j = 0; j < NH; ++j) sum[j] = 0.f;
-            const int lo = max(0, BS * (B - 1)), hi = q - 6;  // inclusive range
+            const int lo = max(0, BS * (B - 1)), hi = q - 1 - NLIVE;  // inclusive range
             // two aligned groups of BS steps: the previous block and the row's own block
 #pragma unroll
             for (int part = 0; part < 2; ++part) {
@@ -2273,7 +2275,10 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 // the chunk's rows of blocks 0 and 1 (the folds that read it).  The buffers of
                 // that parity last served the chunk before the current one.
                 const int c = loaded - 1;  // chunk the live wave is in (or before)
+                // (The live wave reads the cross block for the chunk's rows tn < NLIVE, in steps up
+                // to T c + NLIVE - 2.)
                 const bool gx_free = (c == 0) || (lds_read(cdone) >= min(T * c + BS + 1, nsteps) &&
+                                                  lds_read(d1done) >= min(T * c + NLIVE, nsteps) &&
                                                   lds_read(rdy) >= NB * c + 2 && lds_read(rdy + 1) >= NB * c + 2);
                 if (gx_free) {
                     const int cn = loaded, tcn = chunk_len(cn);
