@@ -2360,29 +2360,35 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     }
 }
 
-template <int T>
+// A tile workgroup owns RT x 16 neurons (RT sub-tiles of 16 rows of W1) of one CN: more CNs
+// fit the chip with RT = 2, and the input rows each sub-tile needs are loaded once for all.
+template <int T, int RT>
 __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs& a, int k, int rb, float* smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int H = a.H, In = a.In, K = a.k_rep;
-    const int h = rb * 16 + (lane & 15);
+    const int hb = rb * RT * 16;  // first neuron of the tile
     const int g = lane >> 4;
     const int nib = (In + 15) / 16;  // input blocks of 16; wave w owns blocks w, w+4, ...
     float* th = a.theta + (size_t)k * a.pstride;
-    float W[MAX_IB][4];
+    float W[RT][MAX_IB][4];
 #pragma unroll
-    for (int j = 0; j < MAX_IB; ++j)
+    for (int r = 0; r < RT; ++r) {
+        const int h = hb + r * 16 + (lane & 15);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
-            W[j][q] = (ib < nib && h < H && i < In) ? th[a.off_w1 + (size_t)h * In + i] : 0.f;
-        }
+        for (int j = 0; j < MAX_IB; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
+                W[r][j][q] = (ib < nib && h < H && i < In) ? th[a.off_w1 + (size_t)h * In + i] : 0.f;
+            }
+    }
     const int64_t nz = shard_len(a.n_total, K, k), xs = shard_start(a.n_total, K, k);
     const int nchk = (int)((nz + T - 1) / T);
     int* qready = a.flags + k;
     int* dready = a.flags + K + k;
     int* abort = a.flags + 2 * K;
     constexpr int NMT = T / 16;
-    float* red4 = smem;  // [4 waves][NMT][64][4]
+    float* red4 = smem;  // [4 waves][NMT][RT][64][4]
 
     // Q_c = W1 (current registers) x_t for the rows of chunk c, published to qbuf[c & 1].
     // Out-of-range rows and inputs are read from a clamped (valid) address and masked.
@@ -2402,24 +2408,28 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
                 const float4 v = *(const float4*)(xr + (ok ? i : 0));
                 xv[j] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
             }
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int j = 0; j < MAX_IB; ++j) {
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].x, W[j][0], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].y, W[j][1], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].z, W[j][2], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].w, W[j][3], acc, 0, 0, 0);
+            for (int r = 0; r < RT; ++r) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < MAX_IB; ++j) {
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].x, W[r][j][0], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].y, W[r][j][1], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].z, W[r][j][2], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[j].w, W[r][j][3], acc, 0, 0, 0);
+                }
+                *(f4*)(red4 + (((size_t)(wave * NMT + mt) * RT + r) * 64 + lane) * 4) = acc;
             }
-            *(f4*)(red4 + ((size_t)(wave * NMT + mt) * 64 + lane) * 4) = acc;
         }
         __syncthreads();
         float* Q = a.qbuf + ((size_t)(c & 1) * K + k) * a.qslot;
-        for (int e = tid; e < NMT * 256; e += 256) {
-            const int mt = e >> 8, rem = e & 255, ln = rem >> 2, r = rem & 3;
+        for (int e = tid; e < NMT * RT * 256; e += 256) {
+            const int mr = e >> 8, rem = e & 255, ln = rem >> 2, rr = rem & 3;  // mr = mt * RT + r
+            const int mt = mr / RT, r = mr - mt * RT;
             float sum = 0.f;
 #pragma unroll
-            for (int w = 0; w < 4; ++w) sum += red4[((size_t)(w * NMT + mt) * 64 + ln) * 4 + r];
-            const int t = mt * 16 + 4 * (ln >> 4) + r, hh = rb * 16 + (ln & 15);
+            for (int w = 0; w < 4; ++w) sum += red4[(((size_t)(w * NMT + mt) * RT + r) * 64 + ln) * 4 + rr];
+            const int t = mt * 16 + 4 * (ln >> 4) + rr, hh = hb + r * 16 + (ln & 15);
             if (t < tc && hh < H) Q[(size_t)hh * a.qstride + t] = sum;
         }
         signal_add(qready, 1);
@@ -2428,16 +2438,20 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
     auto update = [&](int c) {
         const int tc = (int)min<int64_t>(T, nz - (int64_t)c * T);
         const int64_t xb = xs + (int64_t)c * T;
-        const float* D = a.d1 + ((size_t)(c & 1) * K + k) * H * T + (size_t)(h < H ? h : 0) * T;
-        float bv[T / 4];
+        float bv[RT][T / 4];
 #pragma unroll
-        for (int sl = 0; sl < T / 16; ++sl) {
-            const float4 d = *(const float4*)(D + sl * 16 + 4 * g);
-            const int t0 = sl * 16 + 4 * g;
-            bv[4 * sl + 0] = (h < H && t0 + 0 < tc) ? d.x : 0.f;
-            bv[4 * sl + 1] = (h < H && t0 + 1 < tc) ? d.y : 0.f;
-            bv[4 * sl + 2] = (h < H && t0 + 2 < tc) ? d.z : 0.f;
-            bv[4 * sl + 3] = (h < H && t0 + 3 < tc) ? d.w : 0.f;
+        for (int r = 0; r < RT; ++r) {
+            const int h = hb + r * 16 + (lane & 15);
+            const float* D = a.d1 + ((size_t)(c & 1) * K + k) * H * T + (size_t)(h < H ? h : 0) * T;
+#pragma unroll
+            for (int sl = 0; sl < T / 16; ++sl) {
+                const float4 d = *(const float4*)(D + sl * 16 + 4 * g);
+                const int t0 = sl * 16 + 4 * g;
+                bv[r][4 * sl + 0] = (h < H && t0 + 0 < tc) ? d.x : 0.f;
+                bv[r][4 * sl + 1] = (h < H && t0 + 1 < tc) ? d.y : 0.f;
+                bv[r][4 * sl + 2] = (h < H && t0 + 2 < tc) ? d.z : 0.f;
+                bv[r][4 * sl + 3] = (h < H && t0 + 3 < tc) ? d.w : 0.f;
+            }
         }
         const float* xrow[T / 4];
 #pragma unroll
@@ -2454,11 +2468,14 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
             float av[T / 4];
 #pragma unroll
             for (int u = 0; u < T / 4; ++u) av[u] = xrow[u][ic];  // bv is zero where the row is out of range
-            f4 dacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int u = 0; u < T / 4; ++u) dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], dacc, 0, 0, 0);
+            for (int r = 0; r < RT; ++r) {
+                f4 dacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int r = 0; r < 4; ++r) W[j][r] -= a.lr * dacc[r];
+                for (int u = 0; u < T / 4; ++u) dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[r][u], dacc, 0, 0, 0);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) W[r][j][q] -= a.lr * dacc[q];
+            }
         }
     };
 
@@ -2479,22 +2496,26 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
     }
     if (!ok) return;
 #pragma unroll
-    for (int j = 0; j < MAX_IB; ++j)
+    for (int r = 0; r < RT; ++r) {
+        const int h = hb + r * 16 + (lane & 15);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
-            if (ib < nib && h < H && i < In) th[a.off_w1 + (size_t)h * In + i] = W[j][q];
-        }
+        for (int j = 0; j < MAX_IB; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
+                if (ib < nib && h < H && i < In) th[a.off_w1 + (size_t)h * In + i] = W[r][j][q];
+            }
+    }
 }
 
-template <int T, int NH, int A1, int A2, int LS, int OC>
+template <int T, int NH, int A1, int A2, int LS, int OC, int RT>
 __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
     extern __shared__ float smem[];
     const int b = blockIdx.x, K = a.k_rep;
     if (b < K) psgd_rec<T, NH, A1, A2, LS, OC>(a, b, smem);
     else {
         const int j = b - K;
-        psgd_tile<T>(a, j / a.nrb, j % a.nrb, smem);
+        psgd_tile<T, RT>(a, j / a.nrb, j % a.nrb, smem);
     }
 }
 

@@ -85,7 +85,8 @@ struct pnn_net {
     // persistent variant: nrb tiles of 16 rows of W1 per CN
     bool persistent = false;
     bool pspecial = false;   // sigmoid / sigmoid / quadratic loss / 10 outputs
-    int nrb = 0;
+    int nrb = 0;             // tile workgroups per CN
+    int prt = 1;             // 16-row sub-tiles per tile workgroup
     int* flags = nullptr;    // qready[K], dready[K], abort
     float* qbuf = nullptr;   // [2][K][T][H]
     float* gramx = nullptr;  // [K][nch-1][T][T]
@@ -450,15 +451,18 @@ constexpr int PT = 64;            // chunk length of the persistent per-sample p
 constexpr long SPIN_LIMIT = 1L << 22;
 
 // kernel instance: hidden neurons per lane of the live wave (1: <= 64, 2: <= 128) x
-// activation specialisation
-const void* persistent_fn(const pnn_net* n) {
+// activation specialisation x 16-row sub-tiles per tile workgroup (1, or 2 when more CNs must
+// fit the chip)
+template <int RT>
+const void* persistent_fn_rt(const pnn_net* n) {
     const bool narrow = n->sizes[1] <= 64;
     if (n->pspecial)
-        return narrow ? (const void*)psgd_persistent_kernel<PT, 1, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>
-                      : (const void*)psgd_persistent_kernel<PT, 2, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10>;
-    return narrow ? (const void*)psgd_persistent_kernel<PT, 1, -1, -1, -1, 16>
-                  : (const void*)psgd_persistent_kernel<PT, 2, -1, -1, -1, 16>;
+        return narrow ? (const void*)psgd_persistent_kernel<PT, 1, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10, RT>
+                      : (const void*)psgd_persistent_kernel<PT, 2, ACT_SIGMOID, ACT_SIGMOID, LOSS_MSE, 10, RT>;
+    return narrow ? (const void*)psgd_persistent_kernel<PT, 1, -1, -1, -1, 16, RT>
+                  : (const void*)psgd_persistent_kernel<PT, 2, -1, -1, -1, 16, RT>;
 }
+const void* persistent_fn(const pnn_net* n) { return n->prt == 2 ? persistent_fn_rt<2>(n) : persistent_fn_rt<1>(n); }
 
 // width of the live wave's neuron set (input-sum rows are padded to it)
 int live_width(int H) { return H <= 64 ? 64 : 128; }
@@ -728,13 +732,16 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, n->device) != hipSuccess) cus = 0;
         const int H = n->sizes[1], In = n->sizes[0], O = n->sizes[2];
-        const int nrb = (H + 15) / 16;
         const int HW = live_width(H);
+        // tile workgroups of 16 rows of W1 each, or of 32 when the 16-row tiles do not fit
+        const int rt = (int64_t)K * (1 + (H + 15) / 16) <= cus ? 1 : 2;
+        const int nrb = (H + 16 * rt - 1) / (16 * rt);
+        n->prt = rt;
         // input sums [HW][T+4], errors [HW][T+4], Gram blocks 3 x [T][T+4], window
         // corrections [8][HW], labels [2][T], 12 counters
         const size_t rec_smem =
             (size_t)(2 * HW * (PT + 4) + 3 * PT * (PT + 4) + 8 * HW + 2 * PT + 12) * sizeof(float);
-        const size_t tile_smem = (size_t)4 * (PT / 16) * 64 * 4 * sizeof(float);
+        const size_t tile_smem = (size_t)4 * (PT / 16) * rt * 64 * 4 * sizeof(float);
         n->psmem = std::max(rec_smem, tile_smem);
         n->pspecial = n->act[0] == PNN_SIGMOID && n->act[1] == PNN_SIGMOID && cfg->loss == PNN_LOSS_MSE && O == 10;
         const void* fn = persistent_fn(n);

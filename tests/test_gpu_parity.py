@@ -100,6 +100,9 @@ EPOCH_CASES = [
     (2, dict(sizes=(784, 96, 10), acts=(I.LEAKY_RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=8, replicas=4),
      4 * 40 + 3, 2),                                          # mini-batch leaky ReLU / softmax
     (2, dict(batch=101, replicas=4), 4 * 100 + 3, 3),         # full batch: one step per slice and epoch
+    # per-sample with more CNs than 16-row tile workgroups fit: 32-row tiles
+    (1, dict(replicas=32), 32 * 70 + 5, 1),
+    (1, dict(sizes=(784, 64, 10), replicas=60), 60 * 40 + 7, 1),
 ]
 
 
