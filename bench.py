@@ -63,6 +63,11 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
       once and reads its input row, 8 P + 4 n_in bytes, times the N steps of the launch.
       (The kernel keeps the parameters on chip, so its real traffic is far lower: this is
       the rate at which an HBM-streaming implementation would have to run to match it.)
+    mb_persistent: one launch trains every CN for one epoch (mini-batch gradient descent, one
+      hidden layer).  Priced like psgd_persistent in effective HBM bytes: a batch step of a
+      streaming implementation reads and writes every parameter once, 8 P bytes, and the
+      batch's input rows are read once, 4 n_in bytes a row; the flops are the method's per
+      sample times the N rows of the launch.
     Mini-batch plan, totals over the profiled step divided by the launches; a layer of `in`
     inputs and `out` neurons, `rows` sample rows over all CNs and epochs, `bsteps` batch steps
     per CN; weight operands are 4 bytes (fp32) or 2 (bf16 shadow), activations and errors 4
@@ -82,6 +87,9 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
     L = len(s) - 1
     if name == "psgd_persistent":
         return N * method_flops_per_sample(w), N * (8.0 * w.param_count() + 4.0 * s[0])
+    if name == "mb_persistent":
+        bsteps_epoch = float(-(-(-(-N // K)) // w.batch))
+        return N * method_flops_per_sample(w), K * bsteps_epoch * 8.0 * w.param_count() + N * 4.0 * s[0]
     if name == "merge":
         P = w.param_count()
         return 0.0, (K * P + P + (K * P if w.merge_every_epoch else 0)) * 4.0

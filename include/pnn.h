@@ -176,6 +176,21 @@ const char* pnn_last_error(const pnn_net* net);
 pnn_status pnn_profile(pnn_net* net, int32_t enable);
 int32_t pnn_profile_read(pnn_net* net, const char** names, double* total_ms, int64_t* launches, int32_t cap);
 
+/* Name of the training plan that pnn_init chose for the handle (a static string; "" for
+ * a NULL handle).  All plans compute the update of pnn_train_epoch and differ only in the
+ * order of fp32 roundings:
+ *  "per-sample persistent"  B = 1, one hidden layer of <= 128 neurons, every CN's
+ *                           workgroups co-resident on the device: one launch per epoch;
+ *  "per-sample chunked"     B = 1 otherwise;
+ *  "mini-batch persistent"  fp32, one hidden layer, 2 <= B <= 32, <= 16 outputs,
+ *                           sizes[0] % 4 == 0 and <= 832, H <= 512, every CN's
+ *                           ceil(H / 16) (else ceil(H / 32)) tile workgroups co-resident:
+ *                           one launch per epoch;
+ *  "mini-batch"             kernel launches per layer and batch step.
+ * The environment variable PNN_MB_PLAN=launch, read by pnn_init, selects "mini-batch"
+ * where "mini-batch persistent" would apply. */
+const char* pnn_plan(const pnn_net* net);
+
 /* Releases the handle and everything it owns (NULL is ignored). */
 void pnn_destroy(pnn_net* net);
 

@@ -2519,6 +2519,394 @@ __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
     }
 }
 
+// ------------------------------------------------------------------------------------
+// Mini-batch gradient descent of a one-hidden-layer fp32 network with batches of at most
+// 32 rows: one persistent launch per epoch (forward eq. (2)-(3), output error eq. (9)-(10),
+// hidden error eq. (11), updates eq. (12)-(13) with the gradients averaged over each batch).
+//
+// Tile workgroup (k, rb) owns, for CN k, the hidden neurons j in [16 RT rb, 16 RT (rb + 1)):
+// their rows of W1 in registers (laid out as in psgd_tile), their biases b1 and their
+// columns of W2 in LDS, and a private copy of b2.  Batch step c (rows of the step t < B_c):
+//   1. a1[t][j] = phi(W1[j] . x_t + b1[j]) for the tile's neurons; the batch's rows (loaded
+//      during the previous step's update) are staged in LDS on the way;
+//   2. the tile's share of the output sums, Z2_rb[t][o] = sum_j W2[o][j] a1[t][j], goes to
+//      global memory;
+//   3. every tile reads the nrb shares of its CN, adds them in the same order, adds b2 and
+//      forms the output error delta2 (the same values in every tile of the CN);
+//   4. d1[t][j] = phi'(a1[t][j]) sum_o W2[o][j] delta2[t][o] with the pre-update W2; then W2
+//      (tile columns), b2, b1 and W1 (tile rows) -= eta / B_c * their gradients summed over
+//      the batch (every tile updates its copy of b2 identically).
+// Each share value is one 64-bit word written and read with agent-scope relaxed atomics:
+// the float in the low half and the step's tag (tag0 + c, increasing across launches) in
+// the high half, so a reader polls each value until it carries the step's tag and needs no
+// cache-wide release or acquire.  Shares are double buffered by step parity: a tile writes
+// step c+2's share only after it has read every share of step c+1, and every tile computed
+// its step c+1 share from the step c shares it had read.
+
+constexpr int MBP_TB = 32;    // most rows of a batch step
+constexpr int MBP_NRB = 16;   // most tile workgroups per CN
+
+struct MbpArgs {
+    float* theta;
+    int64_t pstride, off_w1, off_b1, off_w2, off_b2;
+    const float* X;
+    const int32_t* y;
+    int64_t n_total;
+    unsigned long long* zpart;  // [2][K][nrb][MBP_TB][16] tagged output-sum shares
+    int* flags;                 // [K]: abort
+    int k_rep, H, O, In, act1, act2, loss, nrb, B;
+    int xcd_map;                // 1: the tiles of a CN run on one XCD (grid a multiple of 8)
+    unsigned tag0;              // tag of step 0 (>= 1)
+    float lr;
+    long spin_limit;
+};
+
+// LDS floats: the batch's rows transposed [64 MAX_IB][36] (every input block of the four
+// waves, zero past the inputs), partial input sums of the 4 waves, activations
+// [32][16 RT + 1], W2 columns [16][16 RT + 1], output errors [32][17], hidden errors
+// [16 RT][36], b1 [16 RT], b2 [16]
+__host__ __device__ constexpr int mbp_lds_floats(int rt) {
+    return 64 * MAX_IB * (MBP_TB + 4) + 4 * (MBP_TB / 16) * rt * 256 + MBP_TB * (16 * rt + 1) +
+           16 * (16 * rt + 1) + MBP_TB * 17 + 16 * rt * (MBP_TB + 4) + 16 * rt + 16;
+}
+
+template <int RT>
+__global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
+    extern __shared__ __attribute__((aligned(16))) float smem[];
+    constexpr int NR = 16 * RT, NMT = MBP_TB / 16, LA = NR + 1, LD1 = MBP_TB + 4, ZS = MBP_TB * 16;
+    constexpr int XT = MBP_TB + 4;  // row stride of the transposed batch rows
+    const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, l16 = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // (uniform: keeps the block tests scalar)
+    const int H = a.H, O = a.O, In = a.In, K = a.k_rep, nrb = a.nrb;
+    // workgroups go to the 8 XCDs in turn by id: with xcd_map, ids x, x + 8, x + 16, ... hold
+    // consecutive tiles, so that a CN's tiles share one L2
+    int lin = blockIdx.x;
+    if (a.xcd_map) lin = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+    const int k = lin / nrb, rb = lin - k * nrb;
+    const int hb = rb * NR;
+    const int nib = (In + 15) / 16;
+    float* xsm = smem;                       // [64 MAX_IB][XT] the batch's rows transposed: [input][row]
+    float* red4 = xsm + 64 * MAX_IB * XT;    // [4 waves][NMT][RT][64][4]
+    float* a1s = red4 + 4 * NMT * RT * 256;  // [MBP_TB][LA]
+    float* w2s = a1s + MBP_TB * LA;          // [16][LA], rows o >= O and columns past H zero
+    float* dls = w2s + 16 * LA;              // [MBP_TB][17]
+    float* d1s = dls + MBP_TB * 17;          // [NR][LD1]
+    float* b1s = d1s + NR * LD1;             // [NR]
+    float* b2s = b1s + NR;                   // [16]
+    float* th = a.theta + (size_t)k * a.pstride;
+
+    float W[RT][MAX_IB][4];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        const int h = hb + r * 16 + l16;
+#pragma unroll
+        for (int j = 0; j < MAX_IB; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
+                W[r][j][q] = (ib < nib && h < H && i < In) ? th[a.off_w1 + (size_t)h * In + i] : 0.f;
+            }
+    }
+    for (int e = tid; e < 16 * NR; e += 256) {
+        const int o = e / NR, j = e - o * NR;
+        w2s[o * LA + j] = (o < O && hb + j < H) ? th[a.off_w2 + (size_t)o * H + hb + j] : 0.f;
+    }
+    if (tid < NR) b1s[tid] = hb + tid < H ? th[a.off_b1 + hb + tid] : 0.f;
+    if (tid < 16) b2s[tid] = tid < O ? th[a.off_b2 + tid] : 0.f;
+
+    const int64_t nz = shard_len(a.n_total, K, k), xs = shard_start(a.n_total, K, k);
+    const int nsteps = (int)((nz + a.B - 1) / a.B);
+    int* abort = a.flags + K;
+    // the batch's rows as operands of the input sums (lane: row mt * 16 + l16, inputs
+    // 16 ib + 4 g .. + 3 of the blocks ib = wave + 4 j), zero past the batch and past In;
+    // loaded one step ahead
+    float4 xn[NMT][MAX_IB];
+    int yn[ZS / 256];  // labels of the rows (tid + 256 u) / 16
+    auto load_rows = [&](int c) {
+        const int tcn = (int)min<int64_t>(a.B, nz - (int64_t)c * a.B);
+        const int64_t xbn = xs + (int64_t)c * a.B;
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) {
+            const int row = mt * 16 + l16;
+            const bool rok = row < tcn;
+            const float* xr = a.X + (size_t)(xbn + (rok ? row : 0)) * In;
+#pragma unroll
+            for (int j = 0; j < MAX_IB; ++j) {
+                const int ib = wave + 4 * j, i = ib * 16 + 4 * g;
+                const bool iok = rok && ib < nib && i < In;
+                const float4 v = *(const float4*)(xr + (iok ? i : 0));
+                xn[mt][j] = iok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < ZS / 256; ++u) {
+            const int t = (tid + 256 * u) >> 4;
+            yn[u] = a.y[xbn + (t < tcn ? t : 0)];
+        }
+    };
+    if (nsteps > 0) load_rows(0);
+    __syncthreads();
+    bool ok = true;
+    for (int c = 0; c < nsteps; ++c) {
+        const int tc = (int)min<int64_t>(a.B, nz - (int64_t)c * a.B);
+        const int64_t xb = xs + (int64_t)c * a.B;
+        const float scale = a.lr / (float)tc;
+        const unsigned long long tag = (unsigned long long)(a.tag0 + (unsigned)c) << 32;
+        int yc[ZS / 256];
+#pragma unroll
+        for (int u = 0; u < ZS / 256; ++u) yc[u] = yn[u];
+        // 1. input sums of the tile's neurons (wave w adds the input blocks w, w + 4, ...),
+        //    then the activations; rows past the batch and neurons past H are zero.  The rows
+        //    are staged transposed for the weight update.
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) {
+            const int row = mt * 16 + l16;
+#pragma unroll
+            for (int j = 0; j < MAX_IB; ++j) {
+                float* xt = xsm + ((wave + 4 * j) * 16 + 4 * g) * XT + row;
+                xt[0] = xn[mt][j].x;
+                xt[XT] = xn[mt][j].y;
+                xt[2 * XT] = xn[mt][j].z;
+                xt[3 * XT] = xn[mt][j].w;
+            }
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < MAX_IB; ++j) {
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].x, W[r][j][0], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].y, W[r][j][1], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].z, W[r][j][2], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].w, W[r][j][3], acc, 0, 0, 0);
+                }
+                *(f4*)(red4 + (((size_t)(wave * NMT + mt) * RT + r) * 64 + lane) * 4) = acc;
+            }
+        }
+        __syncthreads();
+        for (int e = tid; e < NMT * RT * 256; e += 256) {
+            const int mr = e >> 8, rem = e & 255, ln = rem >> 2, rr = rem & 3;  // mr = mt * RT + r
+            const int mt = mr / RT, r = mr - mt * RT;
+            float sum = 0.f;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) sum += red4[(((size_t)(w * NMT + mt) * RT + r) * 64 + ln) * 4 + rr];
+            const int t = mt * 16 + 4 * (ln >> 4) + rr, jj = r * 16 + (ln & 15);
+            a1s[t * LA + jj] = (t < tc && hb + jj < H) ? act_fn(a.act1, sum + b1s[jj]) : 0.f;
+        }
+        __syncthreads();
+        // 2. the tile's share of the output sums, Z2_rb = a1 W2_rb^T: wave mt takes rows
+        //    16 mt .. 16 mt + 15 (lane: rows 16 mt + 4 g + i, output l16)
+        unsigned long long* zp = a.zpart + (size_t)((c & 1) * K + k) * nrb * ZS;
+        if (wave < NMT) {
+            f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int r = 0; r < RT; ++r)
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const int jj = r * 16 + 4 * ks + g;
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1s[(wave * 16 + l16) * LA + jj], w2s[l16 * LA + jj], acc,
+                                                               0, 0, 0);
+                }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int t = wave * 16 + 4 * g + i;
+                if (t < tc && l16 < O)
+                    __hip_atomic_store(zp + (size_t)rb * ZS + t * 16 + l16, tag | __float_as_uint(acc[i]), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        // 3. every share of the CN, polled until it carries this step's tag (bounded: on
+        //    expiry, or when another workgroup gave up, the abort flag ends every workgroup)
+        float sv[ZS / 256][MBP_NRB];
+        {
+            unsigned need = 0;
+#pragma unroll
+            for (int u = 0; u < ZS / 256; ++u) {
+                const int e = tid + 256 * u, t = e >> 4, o = e & 15;
+#pragma unroll
+                for (int q = 0; q < MBP_NRB; ++q)
+                    if (q < nrb && t < tc && o < O) need |= 1u << (u * MBP_NRB + q);
+            }
+            long it = 0;
+            bool good = true;
+            while (need) {
+                unsigned long long v[ZS / 256][MBP_NRB];
+#pragma unroll
+                for (int u = 0; u < ZS / 256; ++u)
+#pragma unroll
+                    for (int q = 0; q < MBP_NRB; ++q)
+                        if (need & (1u << (u * MBP_NRB + q)))
+                            v[u][q] = __hip_atomic_load(zp + (size_t)q * ZS + tid + 256 * u, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+                for (int u = 0; u < ZS / 256; ++u)
+#pragma unroll
+                    for (int q = 0; q < MBP_NRB; ++q)
+                        if ((need & (1u << (u * MBP_NRB + q))) && (v[u][q] >> 32) == (tag >> 32)) {
+                            sv[u][q] = __uint_as_float((unsigned)v[u][q]);
+                            need &= ~(1u << (u * MBP_NRB + q));
+                        }
+                if (!need) break;
+                if (__hip_atomic_load(abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) { good = false; break; }
+                if (++it > a.spin_limit) {
+                    __hip_atomic_store(abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    good = false;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            if (__syncthreads_or(!good)) { ok = false; break; }
+        }
+        // output sums, output activation and output error; the 16 outputs of a row are 16
+        // adjacent lanes
+#pragma unroll
+        for (int u = 0; u < ZS / 256; ++u) {
+            const int e = tid + 256 * u, t = e >> 4, o = e & 15;
+            const bool live = t < tc && o < O;
+            float zv = 0.f;
+            if (live) {
+                float s = 0.f;
+#pragma unroll
+                for (int q = 0; q < MBP_NRB; ++q)
+                    if (q < nrb) s += sv[u][q];
+                zv = s + b2s[o];
+            }
+            float xo;
+            if (a.act2 == ACT_SOFTMAX) {
+                float m = live ? zv : -INFINITY;
+#pragma unroll
+                for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
+                const float ex = live ? expf(zv - m) : 0.f;
+                float sm = ex;
+#pragma unroll
+                for (int sh = 1; sh < 16; sh <<= 1) sm += __shfl_xor(sm, sh, 16);
+                xo = ex * (1.0f / sm);
+            } else {
+                xo = act_fn(a.act2, zv);
+            }
+            float dv = 0.f;
+            if (live) {
+                const float t1 = (o == yc[u]) ? 1.0f : 0.0f;
+                dv = (a.loss == LOSS_XENT) ? (xo - t1) : (xo - t1) * act_deriv(a.act2, xo);
+            }
+            dls[t * 17 + o] = dv;
+        }
+        __syncthreads();
+        // 4. hidden errors of the tile's neurons with the pre-update W2, S = delta2 W2_rb:
+        //    wave mt takes rows 16 mt .. 16 mt + 15 (lane: rows 16 mt + 4 g + i, neuron l16)
+        if (wave < NMT) {
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                f4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+                    sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(dls[(wave * 16 + l16) * 17 + 4 * ks + g],
+                                                                w2s[(4 * ks + g) * LA + r * 16 + l16], sacc, 0, 0, 0);
+                const int t0 = wave * 16 + 4 * g, jj = r * 16 + l16;
+                float4 d;
+                d.x = sacc[0] * act_deriv(a.act1, a1s[(t0 + 0) * LA + jj]);
+                d.y = sacc[1] * act_deriv(a.act1, a1s[(t0 + 1) * LA + jj]);
+                d.z = sacc[2] * act_deriv(a.act1, a1s[(t0 + 2) * LA + jj]);
+                d.w = sacc[3] * act_deriv(a.act1, a1s[(t0 + 3) * LA + jj]);
+                *(float4*)(d1s + jj * LD1 + t0) = d;
+            }
+        }
+        __syncthreads();
+        // W2 columns (wave 2: dW2 = delta2^T a1 over the batch, lane: outputs 4 g + i, neuron
+        // l16), b2 (wave 1) and b1 (wave 3); their readers in the next step follow a barrier.
+        // Rows past the batch are zero in delta2, a1 and d1.
+        if (wave == 2) {
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < MBP_TB / 4; ++ks)
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(dls[(4 * ks + g) * 17 + l16], a1s[(4 * ks + g) * LA + r * 16 + l16],
+                                                               acc, 0, 0, 0);
+                const int jj = r * 16 + l16;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int o = 4 * g + i;
+                    if (o < O && hb + jj < H) w2s[o * LA + jj] -= scale * acc[i];
+                }
+            }
+        } else if (wave == 1) {
+            // lane: output l16, rows 8 g .. 8 g + 7; the four partial sums added in lane order
+            float p = 0.f;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) p += dls[(8 * g + t) * 17 + l16];
+            const float s = __shfl(p, l16) + __shfl(p, l16 + 16) + __shfl(p, l16 + 32) + __shfl(p, l16 + 48);
+            if (lane < O) b2s[lane] -= scale * s;
+        } else if (wave == 3) {
+            if (lane < NR && hb + lane < H) {
+                float s = 0.f;
+#pragma unroll
+                for (int t4 = 0; t4 < MBP_TB / 4; ++t4) {
+                    const float4 d = *(const float4*)(d1s + lane * LD1 + 4 * t4);
+                    s += d.x;
+                    s += d.y;
+                    s += d.z;
+                    s += d.w;
+                }
+                b1s[lane] -= scale * s;
+            }
+        }
+        // W1 rows of the tile -= eta / B_c sum_t d1_t x_t^T (a product whose accumulator layout
+        // equals the register layout); the next step's rows are loaded meanwhile
+        if (c + 1 < nsteps) load_rows(c + 1);
+        {
+            float bv[RT][MBP_TB / 4];
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                const float* D = d1s + (r * 16 + l16) * LD1;
+#pragma unroll
+                for (int sl = 0; sl < MBP_TB / 16; ++sl) {
+                    const float4 d = *(const float4*)(D + sl * 16 + 4 * g);
+                    bv[r][4 * sl + 0] = d.x;
+                    bv[r][4 * sl + 1] = d.y;
+                    bv[r][4 * sl + 2] = d.z;
+                    bv[r][4 * sl + 3] = d.w;
+                }
+            }
+            // (blocks past the inputs hold zero rows and weights: one branch-free sequence)
+#pragma unroll
+            for (int j = 0; j < MAX_IB; ++j) {
+                // rows (u >> 2) * 16 + 4 g + (u & 3) of input (wave + 4 j) * 16 + l16
+                const float* xt = xsm + ((wave + 4 * j) * 16 + l16) * XT + 4 * g;
+                const float4 x0 = *(const float4*)xt, x1 = *(const float4*)(xt + 16);
+                const float av[MBP_TB / 4] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+                for (int r = 0; r < RT; ++r) {
+                    f4 dacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int u = 0; u < MBP_TB / 4; ++u)
+                        dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[r][u], dacc, 0, 0, 0);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) W[r][j][q] -= scale * dacc[q];
+                }
+            }
+        }
+        __syncthreads();  // (the next step's forward overwrites the staged rows)
+    }
+    if (!ok) return;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        const int h = hb + r * 16 + l16;
+#pragma unroll
+        for (int j = 0; j < MAX_IB; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int ib = wave + 4 * j, i = ib * 16 + 4 * g + q;
+                if (ib < nib && h < H && i < In) th[a.off_w1 + (size_t)h * In + i] = W[r][j][q];
+            }
+    }
+    for (int e = tid; e < 16 * NR; e += 256) {
+        const int o = e / NR, j = e - o * NR;
+        if (o < O && hb + j < H) th[a.off_w2 + (size_t)o * H + hb + j] = w2s[o * LA + j];
+    }
+    if (tid < NR && hb + tid < H) th[a.off_b1 + hb + tid] = b1s[tid];
+    if (rb == 0 && tid < O) th[a.off_b2 + tid] = b2s[tid];
+}
+
 // Rows of an epoch in a given order: row r of (xo, yo) is data-set row order[r] (entries
 // outside [0, N) select row 0).  One workgroup per row.
 __global__ __launch_bounds__(256) void gather_rows_kernel(const float* x, const int32_t* y, const int32_t* order,

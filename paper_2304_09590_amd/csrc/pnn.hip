@@ -21,6 +21,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <string>
@@ -92,6 +93,13 @@ struct pnn_net {
     float* gramx = nullptr;  // [K][nch-1][T][T]
     size_t gramx_elems = 0;
     size_t psmem = 0;
+    // persistent mini-batch plan (one hidden layer, fp32, batches of 2..32 rows): nrb tile
+    // workgroups of 16 mrt neurons per CN; flags[K] = abort
+    bool mbp = false;
+    int mrt = 1;
+    unsigned long long* zpart = nullptr;  // [2][K][nrb][32][16] tagged output-sum shares
+    size_t zpart_elems = 0;
+    unsigned mbp_tag = 1;                 // tag of the next launch's first batch step
 
     // profiling
     bool prof = false;
@@ -531,6 +539,54 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
     return l.done();
 }
 
+// ---------------------------------------------------------------------------------------
+// persistent mini-batch plan
+
+const void* mbp_fn(int rt) { return rt == 2 ? (const void*)mbp_kernel<2> : (const void*)mbp_kernel<1>; }
+
+pnn_status mbp_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
+    const int K = n->cfg.replicas;
+    const int64_t nsteps = (shard_len(N, K, 0) + n->cfg.batch - 1) / n->cfg.batch;
+    if ((uint64_t)n->mbp_tag + (uint64_t)nsteps >= 0xFFFFFFFFull) {
+        // the step tags would wrap: clear the shares (so that no stale tag can match) and restart
+        const int ni = (int)(2 * n->zpart_elems);
+        Launch l(n, s, "zero_flags");
+        zero_ints_kernel<<<(ni + 255) / 256, 256, 0, s>>>((int*)n->zpart, ni);
+        TRY(l.done());
+        n->mbp_tag = 1;
+    }
+    {
+        Launch l(n, s, "zero_flags");
+        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, K + 1);
+        TRY(l.done());
+    }
+    MbpArgs a;
+    memset(&a, 0, sizeof a);
+    a.theta = n->theta; a.pstride = n->pstride;
+    a.off_w1 = n->off_w[0]; a.off_b1 = n->off_b[0]; a.off_w2 = n->off_w[1]; a.off_b2 = n->off_b[1];
+    a.X = X; a.y = Y; a.n_total = N;
+    a.zpart = n->zpart; a.flags = n->flags;
+    a.k_rep = K; a.H = n->sizes[1]; a.O = n->sizes[2]; a.In = n->sizes[0];
+    a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
+    a.nrb = n->nrb; a.B = n->cfg.batch;
+    const int grid = K * n->nrb;
+    a.xcd_map = grid % 8 == 0;
+    a.tag0 = n->mbp_tag;
+    n->mbp_tag += (unsigned)nsteps;
+    a.lr = n->cfg.lr;
+    a.spin_limit = SPIN_LIMIT;
+    void* params[] = {&a};
+    Launch l(n, s, "mb_persistent");
+    hipError_t e = hipLaunchCooperativeKernel(mbp_fn(n->mrt), dim3((unsigned)grid), dim3(256), params,
+                                              (unsigned)n->psmem, s);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        n->broken = true;
+        return fail(n, PNN_EHIP, "cooperative launch of the mini-batch kernel failed: %s", hipGetErrorString(e));
+    }
+    return l.done();
+}
+
 pnn_status psgd_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
     if (n->persistent) return psgd_persistent_epoch(n, X, Y, N, s);
     const int K = n->cfg.replicas, T = n->T, H = n->sizes[1], In = n->sizes[0];
@@ -638,19 +694,21 @@ void free_all(pnn_net* n) {
     auto f = [](void* p) { if (p) (void)hipFree(p); };
     f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
     for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
-    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ord_x); f(n->ord_y); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx);
+    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ord_x); f(n->ord_y); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx); f(n->zpart);
     for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : n->free_events) (void)hipEventDestroy(e);
 }
 
-// a per-sample persistent launch that gave up waiting leaves its abort flag set
+// a persistent launch that gave up waiting leaves its abort flag set
 pnn_status check_abort(pnn_net* n) {
-    if (!n->persistent || !n->flags) return PNN_OK;
+    if (!(n->persistent || n->mbp) || !n->flags) return PNN_OK;
     int ab = 0;
-    HIP_TRY(n, hipMemcpy(&ab, n->flags + 2 * n->cfg.replicas, sizeof(int), hipMemcpyDeviceToHost));
+    const int at = n->persistent ? 2 * n->cfg.replicas : n->cfg.replicas;
+    HIP_TRY(n, hipMemcpy(&ab, n->flags + at, sizeof(int), hipMemcpyDeviceToHost));
     if (ab) {
         n->broken = true;
-        return fail(n, PNN_EHIP, "the per-sample training kernel timed out waiting for a peer workgroup");
+        return fail(n, PNN_EHIP, "the %s training kernel timed out waiting for a peer workgroup",
+                    n->persistent ? "per-sample" : "mini-batch");
     }
     return PNN_OK;
 }
@@ -801,6 +859,40 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
                 if ((st = dev_alloc(n, &n->ppart, (size_t)n->ksplit * K * B * N1)) != PNN_OK) return bail(st);
             }
         }
+        // persistent mini-batch plan: one hidden layer in fp32, batches of 2..32 rows, at most
+        // 16 outputs, and every CN's ceil(H / 16 rt) tile workgroups co-resident (rt = 1, or 2
+        // when 16-neuron tiles do not fit); PNN_MB_PLAN=launch selects the per-layer launches
+        const char* plan = getenv("PNN_MB_PLAN");
+        const bool forced_launch = plan && strcmp(plan, "launch") == 0;
+        if (!forced_launch && !n->bf16 && n->L == 2 && B >= 2 && B <= MBP_TB && n->sizes[2] <= 16 &&
+            n->sizes[0] % 4 == 0 && n->sizes[0] <= 4 * MAX_IB * 16) {
+            int cus = 0;
+            if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, n->device) != hipSuccess) cus = 0;
+            const int H = n->sizes[1];
+            int rt = 0;
+            if ((H + 15) / 16 <= MBP_NRB && (int64_t)K * ((H + 15) / 16) <= cus) rt = 1;
+            else if ((H + 31) / 32 <= MBP_NRB && (int64_t)K * ((H + 31) / 32) <= cus) rt = 2;
+            if (rt > 0) {
+                const int nrb = (H + 16 * rt - 1) / (16 * rt);
+                const size_t smem = (size_t)mbp_lds_floats(rt) * sizeof(float);
+                const void* fn = mbp_fn(rt);
+                int per_cu = 0;
+                bool fits = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem) == hipSuccess;
+                if (fits && hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, smem) != hipSuccess) fits = false;
+                if (fits && (int64_t)per_cu * cus < (int64_t)K * nrb) fits = false;
+                (void)hipGetLastError();
+                if (fits) {
+                    n->mbp = true;
+                    n->mrt = rt;
+                    n->nrb = nrb;
+                    n->psmem = smem;
+                    n->zpart_elems = (size_t)2 * K * nrb * MBP_TB * 16;
+                    // (zeroed: a share is valid only with its step's tag, which is >= 1)
+                    if ((st = dev_alloc(n, &n->zpart, n->zpart_elems)) != PNN_OK) return bail(st);
+                    if ((st = dev_alloc(n, &n->flags, (size_t)(K + 1))) != PNN_OK) return bail(st);
+                }
+            }
+        }
         // the fused last layer may stage up to 160 KiB of LDS
         const void* tk[3] = {(const void*)tail_kernel<float, 1>, (const void*)tail_kernel<float, 2>,
                              (const void*)tail_kernel<float, 4>};
@@ -833,6 +925,7 @@ pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev,
     if (N < n->cfg.replicas) return fail(n, PNN_ESHAPE, "N = %lld < K = %d leaves a slice empty", (long long)N, n->cfg.replicas);
     hipStream_t s = (hipStream_t)hip_stream;
     if (n->psgd) return psgd_epoch(n, x_dev, y_dev, N, s);
+    if (n->mbp) return mbp_epoch(n, x_dev, y_dev, N, s);
     const int64_t nmax = shard_len(N, n->cfg.replicas, 0);
     for (int64_t r0 = 0; r0 < nmax; r0 += n->cfg.batch) {
         if (n->bf16) TRY(minibatch_step<true>(n, x_dev, y_dev, N, r0, s));
@@ -1026,6 +1119,12 @@ pnn_status pnn_eval(pnn_net* n, int32_t which, const float* x_dev, const int32_t
     if (correct_host) *correct_host = (int64_t)c;
     if (cost_host) *cost_host = cs / (double)nrows;
     return PNN_OK;
+}
+
+const char* pnn_plan(const pnn_net* n) {
+    if (!n) return "";
+    if (n->psgd) return n->persistent ? "per-sample persistent" : "per-sample chunked";
+    return n->mbp ? "mini-batch persistent" : "mini-batch";
 }
 
 pnn_status pnn_get_params(pnn_net* n, int32_t which, float* host_out) {

@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.pnn_set_params.restype = i32
         L.pnn_last_error.argtypes = [vp]
         L.pnn_last_error.restype = ctypes.c_char_p
+        L.pnn_plan.argtypes = [vp]
+        L.pnn_plan.restype = ctypes.c_char_p
         L.pnn_profile.argtypes = [vp, i32]
         L.pnn_profile.restype = i32
         L.pnn_profile_read.argtypes = [vp, P(ctypes.c_char_p), P(ctypes.c_double), P(i64), i32]
@@ -226,6 +228,11 @@ class PNN:
         cnt = (ctypes.c_int64 * cap)()
         n = self._lib.pnn_profile_read(self.h, names, ms, cnt, cap)
         return {names[i].decode(): (ms[i], cnt[i]) for i in range(min(n, cap))}
+
+    @property
+    def plan(self) -> str:
+        """Training plan chosen at init (see pnn_plan in include/pnn.h)."""
+        return self._lib.pnn_plan(self.h).decode()
 
     def close(self) -> None:
         if getattr(self, "h", None):

@@ -80,4 +80,5 @@ def test_null_arguments_are_rejected():
     assert L.pnn_merge(None, 0, None) == pnn.PNN_EINVAL
     assert L.pnn_eval(None, -1, None, None, 10, None, None, None) == pnn.PNN_EINVAL
     assert L.pnn_shard(10, 0, 0, None, None) == pnn.PNN_EINVAL
+    assert L.pnn_plan(None) == b""
     L.pnn_destroy(None)  # ignored

@@ -103,6 +103,12 @@ EPOCH_CASES = [
     # per-sample with more CNs than 16-row tile workgroups fit: 32-row tiles
     (1, dict(replicas=32), 32 * 70 + 5, 1),
     (1, dict(sizes=(784, 64, 10), replicas=60), 60 * 40 + 7, 1),
+    # persistent mini-batch plan: a hidden width that leaves the last 16-neuron tile half
+    # empty, batches of 7 and a grid that is no multiple of 8; 32-neuron tiles (20 CNs of 256
+    # neurons); batches of 2 with ReLU / softmax
+    (2, dict(sizes=(784, 56, 10), acts=(I.SIGMOID, I.SIGMOID), batch=7, replicas=5), 5 * 40 + 3, 2),
+    (2, dict(replicas=20), 20 * 40 + 3, 1),
+    (2, dict(acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=2, replicas=3), 3 * 30 + 2, 1),
 ]
 
 
@@ -115,6 +121,7 @@ def test_epochs(idx, over, N, epochs):
     Xt, yt = I.test_set(w, 3000)
     th0 = I.init_params(w)
     net = make_net(w, th0)
+    log(f"plan: {net.plan}")
     xd, yd = dev(X), dev(y)
     o = O.Oracle.from_workload(w)
     ref = o.replicate(th0)
@@ -142,6 +149,55 @@ def test_epochs(idx, over, N, epochs):
     argmax_agrees(out_ref, p, margin=1e-5 if w.precision == I.FP32 else 2e-2)
     assert correct == int((p == yt).sum())
     np.testing.assert_allclose(out.cpu().numpy(), out_ref, rtol=0, atol=1e-5 if w.precision == I.FP32 else 2e-2)
+    net.close()
+
+
+PLAN_CASES = [
+    # workload, overrides, plan chosen at init
+    (1, {}, "per-sample persistent"),
+    (1, dict(sizes=(784, 256, 10)), "per-sample chunked"),
+    (2, {}, "mini-batch persistent"),                          # 16 CNs x 16 tiles of 16 neurons
+    (2, dict(replicas=20), "mini-batch persistent"),          # 32-neuron tiles
+    (2, dict(replicas=40), "mini-batch"),                     # 40 x 8 tiles do not fit
+    (2, dict(batch=33), "mini-batch"),
+    (3, dict(replicas=8), "mini-batch"),                      # bf16, two hidden layers
+    (4, dict(replicas=4), "mini-batch"),
+]
+
+
+@pytest.mark.parametrize("idx,over,plan", PLAN_CASES)
+def test_plan_selection(idx, over, plan, monkeypatch):
+    w = I.WORKLOADS[idx].scaled(**over)
+    net = make_net(w, I.init_params(w))
+    assert net.plan == plan
+    net.close()
+    monkeypatch.setenv("PNN_MB_PLAN", "launch")
+    net = make_net(w, I.init_params(w))
+    assert net.plan == ("mini-batch" if plan == "mini-batch persistent" else plan)
+    net.close()
+
+
+@pytest.mark.parametrize("over,N,epochs", [
+    ({}, 16 * 100 + 5, 2),
+    (dict(sizes=(784, 56, 10), acts=(I.SIGMOID, I.SIGMOID), batch=7, replicas=5), 5 * 40 + 3, 1),
+])
+def test_epochs_launch_plan(over, N, epochs, monkeypatch):
+    """The per-layer launch plan on nets that would otherwise get the persistent mini-batch
+    kernel, against the oracle."""
+    monkeypatch.setenv("PNN_MB_PLAN", "launch")
+    w = I.WORKLOADS[2].scaled(**over)
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    assert net.plan == "mini-batch"
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    xd, yd = dev(X), dev(y)
+    for e in range(epochs):
+        net.train_epoch(xd, yd)
+        o.train_epoch(ref, X, y, threads=8)
+        for k in range(w.replicas):
+            close_epoch(w, net.get_params(k), ref[k], f"epoch {e} replica {k}")
     net.close()
 
 
