@@ -183,7 +183,7 @@ int32_t pnn_profile_read(pnn_net* net, const char** names, double* total_ms, int
  *                           workgroups co-resident on the device: one launch per epoch;
  *  "per-sample chunked"     B = 1 otherwise;
  *  "mini-batch persistent"  fp32, one hidden layer, 2 <= B <= 32, <= 16 outputs,
- *                           sizes[0] % 4 == 0 and <= 832, H <= 512, every CN's
+ *                           sizes[0] % 16 == 0 and <= 832, H <= 512, every CN's
  *                           ceil(H / 16) (else ceil(H / 32)) tile workgroups co-resident:
  *                           one launch per epoch;
  *  "mini-batch"             kernel launches per layer and batch step.

@@ -2622,21 +2622,20 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
     // loaded one step ahead
     float4 xn[NMT][MAX_IB];
     int yn[ZS / 256];  // labels of the rows (tid + 256 u) / 16
+    // (bounds-checked buffer loads over the step's rows: rows past the step read as zero;
+    // blocks past In (In is a multiple of 16) read the next row, or zero after the last, and
+    // meet zero weights in the input sums and a zero mask in the weight update)
     auto load_rows = [&](int c) {
         const int tcn = (int)min<int64_t>(a.B, nz - (int64_t)c * a.B);
         const int64_t xbn = xs + (int64_t)c * a.B;
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void*)(a.X + (size_t)xbn * In), (short)0, tcn * In * 4, 0x00020000);
 #pragma unroll
         for (int mt = 0; mt < NMT; ++mt) {
-            const int row = mt * 16 + l16;
-            const bool rok = row < tcn;
-            const float* xr = a.X + (size_t)(xbn + (rok ? row : 0)) * In;
+            const unsigned vo = (unsigned)((mt * 16 + l16) * In + wave * 16 + 4 * g) * 4u;
 #pragma unroll
-            for (int j = 0; j < MAX_IB; ++j) {
-                const int ib = wave + 4 * j, i = ib * 16 + 4 * g;
-                const bool iok = rok && ib < nib && i < In;
-                const float4 v = *(const float4*)(xr + (iok ? i : 0));
-                xn[mt][j] = iok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-            }
+            for (int j = 0; j < MAX_IB; ++j)
+                xn[mt][j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + 256u * j, 0, 0));
         }
 #pragma unroll
         for (int u = 0; u < ZS / 256; ++u) {
@@ -2870,10 +2869,13 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
             // (blocks past the inputs hold zero rows and weights: one branch-free sequence)
 #pragma unroll
             for (int j = 0; j < MAX_IB; ++j) {
-                // rows (u >> 2) * 16 + 4 g + (u & 3) of input (wave + 4 j) * 16 + l16
+                // rows (u >> 2) * 16 + 4 g + (u & 3) of input (wave + 4 j) * 16 + l16; blocks
+                // past In stay zero
+                const bool jok = wave + 4 * j < nib;
                 const float* xt = xsm + ((wave + 4 * j) * 16 + l16) * XT + 4 * g;
                 const float4 x0 = *(const float4*)xt, x1 = *(const float4*)(xt + 16);
-                const float av[MBP_TB / 4] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+                const float av[MBP_TB / 4] = {jok ? x0.x : 0.f, jok ? x0.y : 0.f, jok ? x0.z : 0.f, jok ? x0.w : 0.f,
+                                              jok ? x1.x : 0.f, jok ? x1.y : 0.f, jok ? x1.z : 0.f, jok ? x1.w : 0.f};
 #pragma unroll
                 for (int r = 0; r < RT; ++r) {
                     f4 dacc = {0.f, 0.f, 0.f, 0.f};

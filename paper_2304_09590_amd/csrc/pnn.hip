@@ -865,7 +865,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         const char* plan = getenv("PNN_MB_PLAN");
         const bool forced_launch = plan && strcmp(plan, "launch") == 0;
         if (!forced_launch && !n->bf16 && n->L == 2 && B >= 2 && B <= MBP_TB && n->sizes[2] <= 16 &&
-            n->sizes[0] % 4 == 0 && n->sizes[0] <= 4 * MAX_IB * 16) {
+            n->sizes[0] % 16 == 0 && n->sizes[0] <= 4 * MAX_IB * 16) {
             int cus = 0;
             if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, n->device) != hipSuccess) cus = 0;
             const int H = n->sizes[1];
