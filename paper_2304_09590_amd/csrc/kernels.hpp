@@ -2625,25 +2625,33 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
     // (bounds-checked buffer loads over the step's rows: rows past the step read as zero;
     // blocks past In (In is a multiple of 16) read the next row, or zero after the last, and
     // meet zero weights in the input sums and a zero mask in the weight update)
-    auto load_rows = [&](int c) {
+    // rows_rsrc(c): descriptor of step c's rows; load_row_block(rs, idx): operand idx = mt * MAX_IB
+    // + j of buffer xn (issued one by one so that they can be spread over other work)
+    auto rows_rsrc = [&](int c) {
         const int tcn = (int)min<int64_t>(a.B, nz - (int64_t)c * a.B);
         const int64_t xbn = xs + (int64_t)c * a.B;
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc((void*)(a.X + (size_t)xbn * In), (short)0, tcn * In * 4, 0x00020000);
-#pragma unroll
-        for (int mt = 0; mt < NMT; ++mt) {
-            const unsigned vo = (unsigned)((mt * 16 + l16) * In + wave * 16 + 4 * g) * 4u;
-#pragma unroll
-            for (int j = 0; j < MAX_IB; ++j)
-                xn[mt][j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + 256u * j, 0, 0));
-        }
+        return __builtin_amdgcn_make_buffer_rsrc((void*)(a.X + (size_t)xbn * In), (short)0, tcn * In * 4, 0x00020000);
+    };
+    auto load_row_block = [&](__amdgpu_buffer_rsrc_t rs, int idx) {
+        const int mt = idx / MAX_IB, j = idx - mt * MAX_IB;
+        const unsigned vo = (unsigned)((mt * 16 + l16) * In + wave * 16 + 4 * g) * 4u;
+        xn[mt][j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + 256u * j, 0, 0));
+    };
+    auto load_labels = [&](int c) {
+        const int tcn = (int)min<int64_t>(a.B, nz - (int64_t)c * a.B);
+        const int64_t xbn = xs + (int64_t)c * a.B;
 #pragma unroll
         for (int u = 0; u < ZS / 256; ++u) {
             const int t = (tid + 256 * u) >> 4;
             yn[u] = a.y[xbn + (t < tcn ? t : 0)];
         }
     };
-    if (nsteps > 0) load_rows(0);
+    if (nsteps > 0) {
+        const __amdgpu_buffer_rsrc_t rs0 = rows_rsrc(0);
+#pragma unroll
+        for (int idx = 0; idx < NMT * MAX_IB; ++idx) load_row_block(rs0, idx);
+        load_labels(0);
+    }
     __syncthreads();
     bool ok = true;
     for (int c = 0; c < nsteps; ++c) {
@@ -2660,8 +2668,19 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
 #pragma unroll
         for (int mt = 0; mt < NMT; ++mt) {
             const int row = mt * 16 + l16;
+            f4 acc[RT];
+#pragma unroll
+            for (int r = 0; r < RT; ++r) acc[r] = f4{0.f, 0.f, 0.f, 0.f};
+            // (each block's staging stores follow its matrix instructions, which run meanwhile)
 #pragma unroll
             for (int j = 0; j < MAX_IB; ++j) {
+#pragma unroll
+                for (int r = 0; r < RT; ++r) {
+                    acc[r] = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].x, W[r][j][0], acc[r], 0, 0, 0);
+                    acc[r] = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].y, W[r][j][1], acc[r], 0, 0, 0);
+                    acc[r] = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].z, W[r][j][2], acc[r], 0, 0, 0);
+                    acc[r] = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].w, W[r][j][3], acc[r], 0, 0, 0);
+                }
                 float* xt = xsm + ((wave + 4 * j) * 16 + 4 * g) * XT + row;
                 xt[0] = xn[mt][j].x;
                 xt[XT] = xn[mt][j].y;
@@ -2669,17 +2688,8 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
                 xt[3 * XT] = xn[mt][j].w;
             }
 #pragma unroll
-            for (int r = 0; r < RT; ++r) {
-                f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int j = 0; j < MAX_IB; ++j) {
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].x, W[r][j][0], acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].y, W[r][j][1], acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].z, W[r][j][2], acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xn[mt][j].w, W[r][j][3], acc, 0, 0, 0);
-                }
-                *(f4*)(red4 + (((size_t)(wave * NMT + mt) * RT + r) * 64 + lane) * 4) = acc;
-            }
+            for (int r = 0; r < RT; ++r)
+                *(f4*)(red4 + (((size_t)(wave * NMT + mt) * RT + r) * 64 + lane) * 4) = acc[r];
         }
         __syncthreads();
         for (int e = tid; e < NMT * RT * 256; e += 256) {
@@ -2814,13 +2824,17 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
         // l16), b2 (wave 1) and b1 (wave 3); their readers in the next step follow a barrier.
         // Rows past the batch are zero in delta2, a1 and d1.
         if (wave == 2) {
+            float da[MBP_TB / 4];
+#pragma unroll
+            for (int ks = 0; ks < MBP_TB / 4; ++ks) da[ks] = dls[(4 * ks + g) * 17 + l16];
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
+                float xa[MBP_TB / 4];
+#pragma unroll
+                for (int ks = 0; ks < MBP_TB / 4; ++ks) xa[ks] = a1s[(4 * ks + g) * LA + r * 16 + l16];
                 f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < MBP_TB / 4; ++ks)
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(dls[(4 * ks + g) * 17 + l16], a1s[(4 * ks + g) * LA + r * 16 + l16],
-                                                               acc, 0, 0, 0);
+                for (int ks = 0; ks < MBP_TB / 4; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(da[ks], xa[ks], acc, 0, 0, 0);
                 const int jj = r * 16 + l16;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -2850,8 +2864,17 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
             }
         }
         // W1 rows of the tile -= eta / B_c sum_t d1_t x_t^T (a product whose accumulator layout
-        // equals the register layout); the next step's rows are loaded meanwhile
-        if (c + 1 < nsteps) load_rows(c + 1);
+        // equals the register layout); the next step's rows are loaded meanwhile, a few loads
+        // per pair of blocks
+        // (with 32-neuron tiles all of them at once: spreading them costs registers that tile
+        // does not have)
+        const bool more = c + 1 < nsteps;
+        const __amdgpu_buffer_rsrc_t rsn = rows_rsrc(more ? c + 1 : c);
+        if (more) load_labels(c + 1);
+        if (RT > 1 && more) {
+#pragma unroll
+            for (int idx = 0; idx < NMT * MAX_IB; ++idx) load_row_block(rsn, idx);
+        }
         {
             float bv[RT][MBP_TB / 4];
 #pragma unroll
@@ -2866,28 +2889,57 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
                     bv[r][4 * sl + 3] = d.w;
                 }
             }
-            // (blocks past the inputs hold zero rows and weights: one branch-free sequence)
-#pragma unroll
-            for (int j = 0; j < MAX_IB; ++j) {
-                // rows (u >> 2) * 16 + 4 g + (u & 3) of input (wave + 4 j) * 16 + l16; blocks
-                // past In stay zero
+            // Blocks in pairs: two independent accumulation chains interleaved, and the next
+            // pair's staged rows read before this pair's matrix instructions (blocks past the
+            // inputs hold zero rows and weights: one branch-free sequence).
+            // rows (u >> 2) * 16 + 4 g + (u & 3) of input (wave + 4 j) * 16 + l16; blocks past In
+            // stay zero
+            auto read_block = [&](int j, float (&av)[MBP_TB / 4]) {
                 const bool jok = wave + 4 * j < nib;
                 const float* xt = xsm + ((wave + 4 * j) * 16 + l16) * XT + 4 * g;
                 const float4 x0 = *(const float4*)xt, x1 = *(const float4*)(xt + 16);
-                const float av[MBP_TB / 4] = {jok ? x0.x : 0.f, jok ? x0.y : 0.f, jok ? x0.z : 0.f, jok ? x0.w : 0.f,
-                                              jok ? x1.x : 0.f, jok ? x1.y : 0.f, jok ? x1.z : 0.f, jok ? x1.w : 0.f};
+                av[0] = jok ? x0.x : 0.f; av[1] = jok ? x0.y : 0.f; av[2] = jok ? x0.z : 0.f; av[3] = jok ? x0.w : 0.f;
+                av[4] = jok ? x1.x : 0.f; av[5] = jok ? x1.y : 0.f; av[6] = jok ? x1.z : 0.f; av[7] = jok ? x1.w : 0.f;
+            };
+            float avA[MBP_TB / 4], avB[MBP_TB / 4];
+            read_block(0, avA);
+            if (1 < MAX_IB) read_block(1, avB);
+            constexpr int LPP = (NMT * MAX_IB + (MAX_IB + 1) / 2 - 1) / ((MAX_IB + 1) / 2);  // loads per pair
+#pragma unroll
+            for (int j = 0; j < MAX_IB; j += 2) {
+                const bool two = j + 1 < MAX_IB;
+                if (RT == 1 && more) {
+#pragma unroll
+                    for (int i = 0; i < LPP; ++i)
+                        if ((j / 2) * LPP + i < NMT * MAX_IB) load_row_block(rsn, (j / 2) * LPP + i);
+                }
+                float nA[MBP_TB / 4], nB[MBP_TB / 4];
+                if (j + 2 < MAX_IB) read_block(j + 2, nA);
+                if (j + 3 < MAX_IB) read_block(j + 3, nB);
 #pragma unroll
                 for (int r = 0; r < RT; ++r) {
-                    f4 dacc = {0.f, 0.f, 0.f, 0.f};
+                    f4 dA = {0.f, 0.f, 0.f, 0.f}, dB = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int u = 0; u < MBP_TB / 4; ++u)
-                        dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[r][u], dacc, 0, 0, 0);
+                    for (int u = 0; u < MBP_TB / 4; ++u) {
+                        dA = __builtin_amdgcn_mfma_f32_16x16x4f32(avA[u], bv[r][u], dA, 0, 0, 0);
+                        if (two) dB = __builtin_amdgcn_mfma_f32_16x16x4f32(avB[u], bv[r][u], dB, 0, 0, 0);
+                    }
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) W[r][j][q] -= scale * dacc[q];
+                    for (int q = 0; q < 4; ++q) {
+                        W[r][j][q] -= scale * dA[q];
+                        if (two) W[r][j + 1][q] -= scale * dB[q];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < MBP_TB / 4; ++u) {
+                    if (j + 2 < MAX_IB) avA[u] = nA[u];
+                    if (j + 3 < MAX_IB) avB[u] = nB[u];
                 }
             }
         }
-        __syncthreads();  // (the next step's forward overwrites the staged rows)
+        // (the next step's forward overwrites the staged rows; LDS only, so the barrier does not
+        // wait for the next step's row loads, which the forward waits for itself)
+        lds_barrier();
     }
     if (!ok) return;
 #pragma unroll
