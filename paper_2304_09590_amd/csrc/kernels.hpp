@@ -2553,7 +2553,7 @@ struct MbpArgs {
     const int32_t* y;
     int64_t n_total;
     unsigned long long* zpart;  // [2][K][nrb][MBP_TB][16] tagged output-sum shares
-    int* flags;                 // [K]: abort
+    int* flags;                 // [K + 1]; flags[K]: abort
     int k_rep, H, O, In, act1, act2, loss, nrb, B;
     int xcd_map;                // 1: the tiles of a CN run on one XCD (grid a multiple of 8)
     unsigned tag0;              // tag of step 0 (>= 1)
