@@ -188,7 +188,12 @@ int32_t pnn_profile_read(pnn_net* net, const char** names, double* total_ms, int
  *                           one launch per epoch;
  *  "mini-batch"             kernel launches per layer and batch step.
  * The environment variable PNN_MB_PLAN=launch, read by pnn_init, selects "mini-batch"
- * where "mini-batch persistent" would apply. */
+ * where "mini-batch persistent" would apply.  The persistent plans' workgroups wait for each
+ * other with bounded polls (PNN_SPIN_LIMIT, read by pnn_init, default 4194304 polls); a launch
+ * that runs into the bound ends every workgroup (the CNs' parameters are then unspecified),
+ * and the next pnn_get_params returns PNN_EHIP and marks the handle unusable.
+ * PNN_TEST_STALL_SHARES=1 (tests of that path only) makes every wait of the persistent
+ * mini-batch kernel run into the bound. */
 const char* pnn_plan(const pnn_net* net);
 
 /* Releases the handle and everything it owns (NULL is ignored). */

@@ -2557,6 +2557,7 @@ struct MbpArgs {
     int k_rep, H, O, In, act1, act2, loss, nrb, B;
     int xcd_map;                // 1: the tiles of a CN run on one XCD (grid a multiple of 8)
     unsigned tag0;              // tag of step 0 (>= 1)
+    unsigned tag_skew;          // 0; > 0 makes the readers wait for tags never written (abort test)
     float lr;
     long spin_limit;
 };
@@ -2750,7 +2751,7 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
                 for (int u = 0; u < ZS / 256; ++u)
 #pragma unroll
                     for (int q = 0; q < MBP_NRB; ++q)
-                        if ((need & (1u << (u * MBP_NRB + q))) && (v[u][q] >> 32) == (tag >> 32)) {
+                        if ((need & (1u << (u * MBP_NRB + q))) && (v[u][q] >> 32) == (tag >> 32) + a.tag_skew) {
                             sv[u][q] = __uint_as_float((unsigned)v[u][q]);
                             need &= ~(1u << (u * MBP_NRB + q));
                         }

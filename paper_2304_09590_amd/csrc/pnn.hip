@@ -100,6 +100,10 @@ struct pnn_net {
     unsigned long long* zpart = nullptr;  // [2][K][nrb][32][16] tagged output-sum shares
     size_t zpart_elems = 0;
     unsigned mbp_tag = 1;                 // tag of the next launch's first batch step
+    // bounded waits of the persistent kernels: polls before giving up; and a test hook that
+    // makes the mini-batch kernel's readers wait for share tags that are never written
+    long spin_limit = 0;
+    unsigned tag_skew = 0;
 
     // profiling
     bool prof = false;
@@ -525,7 +529,7 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
     a.H = H; a.O = n->sizes[2]; a.In = In; a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
     a.nrb = n->nrb;
     a.lr = n->cfg.lr;
-    a.spin_limit = SPIN_LIMIT;
+    a.spin_limit = n->spin_limit;
     void* params[] = {&a};
     const dim3 grid((unsigned)(K * (1 + n->nrb)));
     Launch l(n, s, "psgd_persistent");
@@ -572,9 +576,10 @@ pnn_status mbp_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hi
     const int grid = K * n->nrb;
     a.xcd_map = grid % 8 == 0;
     a.tag0 = n->mbp_tag;
+    a.tag_skew = n->tag_skew;
     n->mbp_tag += (unsigned)nsteps;
     a.lr = n->cfg.lr;
-    a.spin_limit = SPIN_LIMIT;
+    a.spin_limit = n->spin_limit;
     void* params[] = {&a};
     Launch l(n, s, "mb_persistent");
     hipError_t e = hipLaunchCooperativeKernel(mbp_fn(n->mrt), dim3((unsigned)grid), dim3(256), params,
@@ -772,6 +777,14 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         return st;
     };
     if (hipGetDevice(&n->device) != hipSuccess) return bail(fail(n, PNN_EHIP, "no HIP device"));
+    // failure-handling tests: PNN_SPIN_LIMIT bounds the persistent kernels' waits (polls);
+    // PNN_TEST_STALL_SHARES=1 makes every wait of the mini-batch kernel run into that bound
+    n->spin_limit = SPIN_LIMIT;
+    if (const char* e = getenv("PNN_SPIN_LIMIT")) {
+        const long v = strtol(e, nullptr, 10);
+        if (v > 0) n->spin_limit = v;
+    }
+    if (const char* e = getenv("PNN_TEST_STALL_SHARES")) n->tag_skew = strcmp(e, "1") == 0 ? 1u : 0u;
     const int K = cfg->replicas, B = cfg->batch;
     pnn_status st;
     if ((st = dev_alloc(n, &n->theta, (size_t)K * n->pstride)) != PNN_OK) return bail(st);

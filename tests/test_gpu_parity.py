@@ -201,6 +201,39 @@ def test_epochs_launch_plan(over, N, epochs, monkeypatch):
     net.close()
 
 
+def test_mini_batch_kernel_abort_path(monkeypatch):
+    """Failure handling forced from the host: the persistent mini-batch kernel's readers wait for
+    share tags that are never written, reach a small poll bound, raise the abort flag and every
+    workgroup ends; the handle reports the time-out and refuses further work; a new handle on the
+    same device then trains as the oracle does."""
+    w = I.WORKLOADS[2].scaled(replicas=4)
+    N = 4 * 40 + 3
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    monkeypatch.setenv("PNN_SPIN_LIMIT", "2000")
+    monkeypatch.setenv("PNN_TEST_STALL_SHARES", "1")
+    net = make_net(w, th0)
+    assert net.plan == "mini-batch persistent"
+    net.train_epoch(dev(X), dev(y))
+    with pytest.raises(B.PnnError) as ei:
+        net.get_params(0)
+    assert ei.value.status == B.PNN_EHIP and "timed out" in str(ei.value)
+    with pytest.raises(B.PnnError) as ei:
+        net.train_epoch(dev(X), dev(y))
+    assert ei.value.status == B.PNN_ESTATE
+    net.close()
+    monkeypatch.delenv("PNN_TEST_STALL_SHARES")
+    monkeypatch.delenv("PNN_SPIN_LIMIT")
+    net = make_net(w, th0)
+    net.train_epoch(dev(X), dev(y))
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    o.train_epoch(ref, X, y, threads=4)
+    for k in range(w.replicas):
+        close_epoch(w, net.get_params(k), ref[k], f"replica {k} after the aborted handle")
+    net.close()
+
+
 # ------------------------------------------------------------------------------------
 # step-by-step trajectory: before every step the oracle restarts from the GPU's state
 
