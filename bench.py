@@ -177,7 +177,7 @@ def main():
                     help="epochs of the CN-versus-merged-network comparison")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("this build runs on one GPU only: the CNs of a PNN are independent until the merge, "
+        print("the library runs on one GPU only: the CNs of a PNN are independent until the merge, "
               "so a multi-GPU run would only split the CNs across GPUs and all-reduce at the merge; "
               "no multi-GPU path is built", file=sys.stderr)
         sys.exit(2)
