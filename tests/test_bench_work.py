@@ -46,6 +46,21 @@ def test_minibatch_bytes_cover_every_weight_pass(idx):
     assert total >= K * bsteps * weights * 8.0
 
 
+def test_persistent_minibatch_effective_bytes():
+    # one launch = one epoch: every batch step of every CN would read and write every parameter
+    # once in a streaming implementation, and every input row is read once
+    w = I.WORKLOADS[2]
+    K, N = w.replicas, w.n_train
+    bsteps = -(-(-(-N // K)) // w.batch)
+    f, b = bench.kernel_work(w, "mb_persistent", 1, N, w.epochs)
+    assert b == K * bsteps * 8.0 * w.param_count() + N * 4.0 * w.sizes[0]
+    assert f == N * bench.method_flops_per_sample(w)
+    # the ragged last batch counts as a step: 3750 rows per CN in batches of 32
+    assert bsteps == 118
+    # below the fp32 ridge (19.7 flop/B): bench.py prices it against HBM
+    assert f / b < 19.7
+
+
 def test_unpriced_kernels():
     w = I.WORKLOADS[2]
     assert bench.kernel_work(w, "fwd_reduce", 1, w.n_train, 1) is None
