@@ -21,6 +21,8 @@
  *    from pnn_last_error (per handle; a NULL handle gives the message of the last failed
  *    pnn_init on the calling thread).  No exception or abort crosses the interface.
  *  - One handle must not be used from two host threads at once.
+ *  - Input rows x_dev are read with 16-byte vector loads: x_dev must be 16-byte aligned
+ *    (PNN_EINVAL otherwise); sizes[0] is a multiple of 8, so every row then is too.
  *
  * Parameter layout (host side, get/set): one network is P = pnn_param_count(cfg) floats,
  * W1, b1, W2, b2, ..., W_l row-major [sizes[l]][sizes[l-1]], b_l [sizes[l]].

@@ -704,6 +704,9 @@ void free_all(pnn_net* n) {
     for (auto e : n->free_events) (void)hipEventDestroy(e);
 }
 
+// the kernels read input rows with 16-byte vector loads
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
 // a persistent launch that gave up waiting leaves its abort flag set
 pnn_status check_abort(pnn_net* n) {
     if (!(n->persistent || n->mbp) || !n->flags) return PNN_OK;
@@ -935,6 +938,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
 pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev, int64_t N, void* hip_stream) {
     TRY(usable(n));
     if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
+    if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
     if (N < n->cfg.replicas) return fail(n, PNN_ESHAPE, "N = %lld < K = %d leaves a slice empty", (long long)N, n->cfg.replicas);
     hipStream_t s = (hipStream_t)hip_stream;
     if (n->psgd) return psgd_epoch(n, x_dev, y_dev, N, s);
@@ -951,6 +955,7 @@ pnn_status pnn_train_epoch_order(pnn_net* n, const float* x_dev, const int32_t* 
                                  const int32_t* order_dev, void* hip_stream) {
     TRY(usable(n));
     if (!x_dev || !y_dev || !order_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev / order_dev is NULL");
+    if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
     if (N < n->cfg.replicas) return fail(n, PNN_ESHAPE, "N = %lld < K = %d leaves a slice empty", (long long)N, n->cfg.replicas);
     if (N > INT32_MAX) return fail(n, PNN_ESHAPE, "N = %lld does not fit the int32 order", (long long)N);
     hipStream_t s = (hipStream_t)hip_stream;
@@ -1085,6 +1090,7 @@ pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrow
         return PNN_OK;
     }
     if (!x_dev || !pred_dev) return fail(n, PNN_EINVAL, "x_dev / pred_dev is NULL");
+    if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
     hipStream_t s = (hipStream_t)hip_stream;
     const bool count = correct_host && y_dev;
     TRY(run_inference(n, which, x_dev, nrows, pred_dev, out_dev, count, y_dev, nullptr, s));
@@ -1108,6 +1114,7 @@ pnn_status pnn_eval(pnn_net* n, int32_t which, const float* x_dev, const int32_t
         return PNN_OK;
     }
     if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
+    if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
     hipStream_t s = (hipStream_t)hip_stream;
     if (cost_host && nrows > n->cost_rows) {
         HIP_TRY(n, hipStreamSynchronize(s));

@@ -201,6 +201,28 @@ def test_epochs_launch_plan(over, N, epochs, monkeypatch):
     net.close()
 
 
+def test_misaligned_input_rows_are_rejected():
+    """x_dev must be 16-byte aligned (rows are read with 16-byte loads): a view one float into a
+    buffer is refused by every call that reads rows, before any device work."""
+    w = I.WORKLOADS[2].scaled(replicas=2)
+    X, y = I.train_set(w, 2 * 40)
+    net = make_net(w, I.init_params(w))
+    xb = torch.zeros(X.size + 4, dtype=torch.float32, device="cuda")
+    xv = xb[1:1 + X.size].view(X.shape)
+    assert xv.data_ptr() % 16 == 4
+    yd = dev(y)
+    for call in (lambda: net.train_epoch(xv, yd),
+                 lambda: net.train_epoch_order(xv, yd, dev(np.arange(len(y), dtype=np.int32))),
+                 lambda: net.infer(xv, torch.empty(len(y), dtype=torch.int32, device="cuda")),
+                 lambda: net.evaluate(xv, yd)):
+        with pytest.raises(B.PnnError) as ei:
+            call()
+        assert ei.value.status == B.PNN_EINVAL and "aligned" in str(ei.value)
+    net.train_epoch(dev(X), yd)  # the handle stays usable
+    net.get_params(0)
+    net.close()
+
+
 def test_mini_batch_kernel_abort_path(monkeypatch):
     """Failure handling forced from the host: the persistent mini-batch kernel's readers wait for
     share tags that are never written, reach a small poll bound, raise the abort flag and every
