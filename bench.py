@@ -11,8 +11,9 @@ Printed: one JSON line with samples/s over all CNs (N * epochs / step time), the
 position of the dominant kernel (measured with HIP events around every launch in an extra,
 untimed step), and the CPU oracle timed on the host cores as a baseline.
 
-Default workload: 784-128-10 sigmoid MLP, K = 4 CNs, per-sample SGD, 60,000 samples,
-1 epoch + merge (workload index 1).  --workload selects another.
+Default workload: the largest one, 784-1024-10 sigmoid MLP, K = 256 CNs, mini-batch 128,
+600,000 samples, 2 epochs with a merge and broadcast after each (workload index 4).
+--workload selects another.
 
 Two further modes (not the default; one JSON line per measurement):
   --sweep-k 1,2,4,...  the time to train the workload's whole training set with K CNs for each
@@ -160,12 +161,80 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(w, X, y, th0, N):
+    """The oracle timed on the host cores: one thread per CN up to the usable cores (the paper
+    runs one goroutine per CN), on a bounded sample of the workload (the first rows of every
+    CN's slice, one epoch), repeated three times (median), plus one thread on one CN's rows."""
+    from oracle import oracle as O
+    cores = len(os.sched_getaffinity(0))
+    threads = max(1, min(w.replicas, cores))
+    o = O.Oracle.from_workload(w)
+    per = -(-N // w.replicas)
+    # about 6 s of work per repeat at ~2.5 GFLOP/s per thread
+    budget = 6.0 * threads * 2.5e9 / method_flops_per_sample(w)
+    n_s = int(min(per, max(w.batch, budget // w.replicas)))
+    idx = np.concatenate([np.arange(s, s + min(n_s, ln)) for s, ln in
+                          (o.shard(N, k) for k in range(w.replicas))])
+    Xs, ys = X[idx], y[idx]   # the sample keeps the slicing: each CN gets its own n_s rows
+    times = []
+    for _ in range(3):
+        th = o.replicate(th0)
+        t1 = time.time()
+        o.train_epoch(th, Xs, ys, threads=threads)
+        times.append(time.time() - t1)
+    dt = float(np.median(times))
+    # one thread, one CN: the first rows of CN 0's slice (about 4 s of work)
+    n1 = int(min(per, max(w.batch, 4.0 * 2.5e9 / method_flops_per_sample(w))))
+    o1 = O.Oracle.from_workload(w, replicas=1)
+    th1 = o1.replicate(th0)
+    t1 = time.time()
+    o1.train_epoch(th1, X[:n1], y[:n1], threads=1)
+    dt1 = time.time() - t1
+    return {"value": round(len(idx) / dt, 2), "unit": "samples/s", "cores": cores, "threads": threads,
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "sample": f"{len(idx)} samples ({min(n_s, per)} per CN x {w.replicas} CNs), 1 epoch, fp64, "
+                      f"{threads} threads (one CN per thread at a time), median of 3 repeats "
+                      f"{', '.join(f'{t:.2f}' for t in times)} s",
+            "one_thread": {"value": round(n1 / dt1, 2), "unit": "samples/s",
+                           "sample": f"{n1} samples of one CN, 1 thread, {dt1:.2f} s"}}
+
+
+def schedule_position(w, N, ms, prof):
+    """The whole training schedule against the roofs: the algorithmic flops and HBM bytes of
+    every profiled library kernel (kernel_work), summed, over the measured step time."""
+    if not prof:
+        return None
+    fl = by = 0.0
+    for name, (tot, n_l) in prof.items():
+        wk = kernel_work(w, name, n_l, N, w.epochs)
+        if wk is None:
+            continue
+        fl += wk[0] * n_l
+        by += wk[1] * n_l
+    s = ms / 1e3
+    mpeak = BF16_PEAK_TFLOPS if w.precision == I.BF16_MIXED else FP32_PEAK_TFLOPS
+    return {"flops": fl, "bytes": by, "tflops": round(fl / s / 1e12, 3), "mfma_frac": round(fl / s / 1e12 / mpeak, 4),
+            "gbs": round(by / s / 1e9, 1), "hbm_frac": round(by / s / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one device-to-device copy of 1 GiB (reference dispatch for HBM byte counters)")
@@ -226,18 +295,21 @@ def main():
         torch.cuda.synchronize()
         print(f"[bench] warmup step {i} done", file=sys.stderr, flush=True)
 
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # K steps bracketed by synchronisations; an event pair per step on the launch stream gives
+    # the per-step times (their median is reported beside the mean)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         step()
-    ev1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / args.steps
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    ms_median = float(np.median(per_step))
     samples = N * w.epochs
     value = samples / (ms / 1e3)
-    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (median {ms_median:.3f})", file=sys.stderr, flush=True)
 
     # evaluation (outside the step)
     pred = torch.empty(len(yt), dtype=torch.int32, device="cuda")
@@ -281,26 +353,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        from oracle import oracle as O
-        cores = len(os.sched_getaffinity(0))
-        threads = max(1, min(w.replicas, cores))
-        o = O.Oracle.from_workload(w)
-        # bounded sample: the first n_s rows of every CN's slice, one epoch, sized for about
-        # 15 s of work per thread at ~1 GFLOP/s
-        per = -(-N // w.replicas)
-        budget = 15.0 * threads * 1e9 / method_flops_per_sample(w)
-        n_s = int(min(per, max(w.batch, budget // w.replicas)))
-        idx = np.concatenate([np.arange(s, s + min(n_s, ln)) for s, ln in
-                              (o.shard(N, k) for k in range(w.replicas))])
-        th = o.replicate(th0)
-        # the sample keeps the slicing: each CN gets its own n_s rows
-        Xs, ys = X[idx], y[idx]
-        t1 = time.time()
-        o.train_epoch(th, Xs, ys, threads=threads)
-        dt = time.time() - t1
-        cpu = {"value": round(len(idx) / dt, 2), "unit": "samples/s", "cores": threads, "kind": "oracle",
-               "sample": f"{len(idx)} samples ({min(n_s, per)} per CN x {w.replicas} CNs), 1 epoch, fp64, "
-                         f"{threads} threads, {dt:.1f}s"}
+        cpu = cpu_baseline(w, X, y, th0, N)
 
     out = {
         "metric": "training samples/sec (all K replicas) + % of HBM/MFMA roofline",
@@ -310,6 +363,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_median": round(ms_median, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -319,6 +373,7 @@ def main():
                    "epochs": w.epochs, "n_train": N, "lr": w.lr,
                    "merge": "every epoch" if w.merge_every_epoch else "end"},
         "roofline": roofline,
+        "schedule": schedule_position(w, N, ms, prof),
         "cpu_baseline": cpu,
         "eval_ms": round(eval_ms, 3),
         "eval_accuracy": round(correct / len(yt), 4),

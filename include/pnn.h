@@ -15,8 +15,10 @@
  *  - The library owns the parameters and its workspace (allocated in pnn_init, released
  *    in pnn_destroy).
  *  - `hip_stream` is a hipStream_t (NULL = the default stream).  Device work is enqueued on
- *    it and the call returns once enqueued; only pnn_get_params, pnn_set_params and a
- *    pnn_infer call with correct_host != NULL wait for the device.
+ *    it and the call returns once enqueued; only pnn_get_params, pnn_set_params, pnn_eval
+ *    and a pnn_infer call with correct_host != NULL wait for the device.  After a training
+ *    epoch on a persistent plan (pnn_plan), the next call that consumes the CNs other than
+ *    pnn_train_epoch first waits for that epoch to end, to read its failure flag.
  *  - Errors are returned as a pnn_status; the message of the last failure is available
  *    from pnn_last_error (per handle; a NULL handle gives the message of the last failed
  *    pnn_init on the calling thread).  No exception or abort crosses the interface.
@@ -80,7 +82,10 @@ typedef struct {
  * softmax output; K >= 1, B >= 1, finite lr >= 0.  Returns PNN_OK or PNN_EINVAL. */
 pnn_status pnn_config_check(const pnn_config* cfg);
 
-/* P, the number of parameters of one network (0 for an invalid configuration). */
+/* P, the number of parameters of one network: every weight W_kj and every bias b_k of each
+ * layer (eq. (2): sizes[l] * sizes[l-1] weights and sizes[l] biases per layer l), which is what
+ * the combination averages (section "Implementation Details").  0 for an invalid
+ * configuration. */
 int64_t pnn_param_count(const pnn_config* cfg);
 
 /* Dataset split (section "Implementation Details": the dataset is split according to the
@@ -192,10 +197,13 @@ int32_t pnn_profile_read(pnn_net* net, const char** names, double* total_ms, int
  * The environment variable PNN_MB_PLAN=launch, read by pnn_init, selects "mini-batch"
  * where "mini-batch persistent" would apply.  The persistent plans' workgroups wait for each
  * other with bounded polls (PNN_SPIN_LIMIT, read by pnn_init, default 4194304 polls); a launch
- * that runs into the bound ends every workgroup (the CNs' parameters are then unspecified),
- * and the next pnn_get_params returns PNN_EHIP and marks the handle unusable.
- * PNN_TEST_STALL_SHARES=1 (tests of that path only) makes every wait of the persistent
- * mini-batch kernel run into the bound. */
+ * that runs into the bound ends every workgroup and leaves the CNs' parameters unspecified.
+ * The next call that consumes the CNs -- pnn_merge, pnn_merge_weighted, pnn_infer, pnn_eval,
+ * pnn_get_params, pnn_set_params (each waits for the last persistent launch to end first) or
+ * pnn_train_epoch (which does not wait: it sees the failure once that launch has ended, and a
+ * persistent launch enqueued after the failed one ends at once) -- returns PNN_EHIP and marks
+ * the handle unusable (PNN_ESTATE from then on).  PNN_TEST_STALL_WAITS=1 (tests of that path
+ * only) makes the persistent kernels' waits run into the bound. */
 const char* pnn_plan(const pnn_net* net);
 
 /* Releases the handle and everything it owns (NULL is ignored). */

@@ -1454,12 +1454,14 @@ __device__ inline float row_allsum16(float v) {
 }
 __device__ inline float readlane_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
 
-// Activations of the sequential per-sample steps, on the hardware exp2 and reciprocal
-// (about 1e-6 relative error for |z| < 10).
+// Activations of the sequential per-sample steps.  The sigmoid runs on the hardware exp2 and
+// reciprocal (relative error below |z| * 6e-8 + 2 ulp).  tanh takes the library function:
+// written as 1 - 2 / (e^{2z} + 1) it would lose its relative accuracy near z = 0 (cancellation:
+// about 1e-4 relative at z = 1e-3), which a cross-entropy output error then amplifies.
 __device__ inline float act_fast(int a, float z) {
     switch (a) {
     case ACT_SIGMOID: return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
-    case ACT_TANH: return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * z) + 1.0f);
+    case ACT_TANH: return tanhf(z);
     case ACT_RELU: return z >= 0.0f ? z + 0.0f : -0.0f;
     case ACT_LEAKY: return z >= 0.0f ? z + 0.0f : 0.01f * z;
     default: return z;
@@ -1566,8 +1568,11 @@ struct PsgdPArgs {
     int qstride;         // row stride (per neuron) within a slot
     int64_t qslot;
     float* d1;           // [2][K][H][T]  by chunk parity (transposed: one row per hidden neuron)
-    int* flags;          // qready[K], dready[K], abort
+    int* flags;          // qready[K], dready[K], abort (sticky: cleared only at allocation)
     int H, O, In, act1, act2, loss, nrb;
+    int wait_skew;       // 0; a large value makes the first wait of every sequential workgroup
+                         // wait for more tile signals than ever come (failure-handling test:
+                         // the bound is reached)
     float lr;
     long spin_limit;
 };
@@ -1966,7 +1971,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     if (tid < 12) lf[tid] = 0;
 
     // chunk 0: wait for Q_0 and stage it with the Gram block and labels
-    if (!wait_geq(qready, a.nrb, gabort, a.spin_limit)) return;
+    if (!wait_geq(qready, a.nrb + a.wait_skew, gabort, a.spin_limit)) return;
     {
         const float* Q = a.qbuf + (size_t)k * HW * TS;
         const float* G = a.gram + (size_t)k * a.nch * T * GS;
@@ -2512,6 +2517,8 @@ template <int T, int NH, int A1, int A2, int LS, int OC, int RT>
 __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
     extern __shared__ float smem[];
     const int b = blockIdx.x, K = a.k_rep;
+    // an earlier launch gave up waiting: the parameters are unspecified, train no further
+    if (__hip_atomic_load(a.flags + 2 * K, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
     if (b < K) psgd_rec<T, NH, A1, A2, LS, OC>(a, b, smem);
     else {
         const int j = b - K;
@@ -2553,7 +2560,7 @@ struct MbpArgs {
     const int32_t* y;
     int64_t n_total;
     unsigned long long* zpart;  // [2][K][nrb][MBP_TB][16] tagged output-sum shares
-    int* flags;                 // [K + 1]; flags[K]: abort
+    int* flags;                 // [K + 1]; flags[K]: abort (sticky: cleared only at allocation)
     int k_rep, H, O, In, act1, act2, loss, nrb, B;
     int xcd_map;                // 1: the tiles of a CN run on one XCD (grid a multiple of 8)
     unsigned tag0;              // tag of step 0 (>= 1)
@@ -2579,6 +2586,8 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, l16 = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // (uniform: keeps the block tests scalar)
     const int H = a.H, O = a.O, In = a.In, K = a.k_rep, nrb = a.nrb;
+    // an earlier launch gave up waiting: the parameters are unspecified, train no further
+    if (__hip_atomic_load(a.flags + K, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
     // workgroups go to the 8 XCDs in turn by id: with xcd_map, ids x, x + 8, x + 16, ... hold
     // consecutive tiles, so that a CN's tiles share one L2
     int lin = blockIdx.x;
@@ -2657,7 +2666,6 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
     bool ok = true;
     for (int c = 0; c < nsteps; ++c) {
         const int tc = (int)min<int64_t>(a.B, nz - (int64_t)c * a.B);
-        const int64_t xb = xs + (int64_t)c * a.B;
         const float scale = a.lr / (float)tc;
         const unsigned long long tag = (unsigned long long)(a.tag0 + (unsigned)c) << 32;
         int yc[ZS / 256];

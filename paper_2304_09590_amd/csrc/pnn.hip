@@ -101,9 +101,15 @@ struct pnn_net {
     size_t zpart_elems = 0;
     unsigned mbp_tag = 1;                 // tag of the next launch's first batch step
     // bounded waits of the persistent kernels: polls before giving up; and a test hook that
-    // makes the mini-batch kernel's readers wait for share tags that are never written
+    // makes their waits run into that bound (the mini-batch kernel's readers wait for share
+    // tags that are never written, the per-sample kernel's for more tiles than exist)
     long spin_limit = 0;
     unsigned tag_skew = 0;
+    int wait_skew = 0;
+    // the abort flag of the last persistent launch has not been read yet; abort_ev follows
+    // that launch on its stream
+    bool abort_pending = false;
+    hipEvent_t abort_ev = nullptr;
 
     // profiling
     bool prof = false;
@@ -479,6 +485,14 @@ const void* persistent_fn(const pnn_net* n) { return n->prt == 2 ? persistent_fn
 // width of the live wave's neuron set (input-sum rows are padded to it)
 int live_width(int H) { return H <= 64 ? 64 : 128; }
 
+// after a persistent launch: its abort flag is read by the next call that consumes the CNs
+pnn_status note_persistent_launch(pnn_net* n, hipStream_t s) {
+    if (!n->abort_ev) HIP_TRY(n, hipEventCreateWithFlags(&n->abort_ev, hipEventDisableTiming));
+    HIP_TRY(n, hipEventRecord(n->abort_ev, s));
+    n->abort_pending = true;
+    return PNN_OK;
+}
+
 pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
     const int K = n->cfg.replicas, H = n->sizes[1], In = n->sizes[0];
     const int64_t nmax = shard_len(N, K, 0);
@@ -514,8 +528,9 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
         TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K * (nch - 1), "psgd_gram")));
     }
     {
+        // (the abort slot flags[2K] is sticky: a launch after an abort ends at once)
         Launch l(n, s, "zero_flags");
-        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, 2 * K + 1);
+        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, 2 * K);
         TRY(l.done());
     }
     PsgdPArgs a;
@@ -528,6 +543,7 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
     a.d1 = n->d1; a.flags = n->flags;
     a.H = H; a.O = n->sizes[2]; a.In = In; a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
     a.nrb = n->nrb;
+    a.wait_skew = n->wait_skew;
     a.lr = n->cfg.lr;
     a.spin_limit = n->spin_limit;
     void* params[] = {&a};
@@ -540,7 +556,8 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
         n->broken = true;
         return fail(n, PNN_EHIP, "cooperative launch of the per-sample kernel failed: %s", hipGetErrorString(e));
     }
-    return l.done();
+    TRY(l.done());
+    return note_persistent_launch(n, s);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -560,8 +577,9 @@ pnn_status mbp_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hi
         n->mbp_tag = 1;
     }
     {
+        // (the abort slot flags[K] is sticky: a launch after an abort ends at once)
         Launch l(n, s, "zero_flags");
-        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, K + 1);
+        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, K);
         TRY(l.done());
     }
     MbpArgs a;
@@ -589,7 +607,8 @@ pnn_status mbp_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hi
         n->broken = true;
         return fail(n, PNN_EHIP, "cooperative launch of the mini-batch kernel failed: %s", hipGetErrorString(e));
     }
-    return l.done();
+    TRY(l.done());
+    return note_persistent_launch(n, s);
 }
 
 pnn_status psgd_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hipStream_t s) {
@@ -700,6 +719,7 @@ void free_all(pnn_net* n) {
     f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
     for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
     f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ord_x); f(n->ord_y); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx); f(n->zpart);
+    if (n->abort_ev) (void)hipEventDestroy(n->abort_ev);
     for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : n->free_events) (void)hipEventDestroy(e);
 }
@@ -707,12 +727,26 @@ void free_all(pnn_net* n) {
 // the kernels read input rows with 16-byte vector loads
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-// a persistent launch that gave up waiting leaves its abort flag set
-pnn_status check_abort(pnn_net* n) {
-    if (!(n->persistent || n->mbp) || !n->flags) return PNN_OK;
+// A persistent launch that gave up waiting leaves its (sticky) abort flag set and the CNs'
+// parameters unspecified.  Every call that consumes the CNs reads the flag of the last such
+// launch first: `wait` waits for that launch to end; without it the flag is read only if the
+// launch has already ended (a later launch of the same kernel ends at once on a set flag).
+pnn_status check_abort(pnn_net* n, bool wait) {
+    if (!n->abort_pending) return PNN_OK;
+    if (!wait) {
+        const hipError_t q = hipEventQuery(n->abort_ev);
+        if (q == hipErrorNotReady) return PNN_OK;
+        if (q != hipSuccess) {
+            n->broken = true;
+            return fail(n, PNN_EHIP, "hipEventQuery failed: %s", hipGetErrorString(q));
+        }
+    } else {
+        HIP_TRY(n, hipEventSynchronize(n->abort_ev));
+    }
     int ab = 0;
     const int at = n->persistent ? 2 * n->cfg.replicas : n->cfg.replicas;
     HIP_TRY(n, hipMemcpy(&ab, n->flags + at, sizeof(int), hipMemcpyDeviceToHost));
+    n->abort_pending = false;
     if (ab) {
         n->broken = true;
         return fail(n, PNN_EHIP, "the %s training kernel timed out waiting for a peer workgroup",
@@ -781,13 +815,17 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
     };
     if (hipGetDevice(&n->device) != hipSuccess) return bail(fail(n, PNN_EHIP, "no HIP device"));
     // failure-handling tests: PNN_SPIN_LIMIT bounds the persistent kernels' waits (polls);
-    // PNN_TEST_STALL_SHARES=1 makes every wait of the mini-batch kernel run into that bound
+    // PNN_TEST_STALL_WAITS=1 makes the persistent kernels' waits run into that bound
     n->spin_limit = SPIN_LIMIT;
     if (const char* e = getenv("PNN_SPIN_LIMIT")) {
         const long v = strtol(e, nullptr, 10);
         if (v > 0) n->spin_limit = v;
     }
-    if (const char* e = getenv("PNN_TEST_STALL_SHARES")) n->tag_skew = strcmp(e, "1") == 0 ? 1u : 0u;
+    if (const char* e = getenv("PNN_TEST_STALL_WAITS")) {
+        const bool on = strcmp(e, "1") == 0;
+        n->tag_skew = on ? 1u : 0u;
+        n->wait_skew = on ? (1 << 29) : 0;  // (the tiles count up to nrb per chunk, and run a chunk ahead)
+    }
     const int K = cfg->replicas, B = cfg->batch;
     pnn_status st;
     if ((st = dev_alloc(n, &n->theta, (size_t)K * n->pstride)) != PNN_OK) return bail(st);
@@ -940,6 +978,7 @@ pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev,
     if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
     if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
     if (N < n->cfg.replicas) return fail(n, PNN_ESHAPE, "N = %lld < K = %d leaves a slice empty", (long long)N, n->cfg.replicas);
+    TRY(check_abort(n, false));
     hipStream_t s = (hipStream_t)hip_stream;
     if (n->psgd) return psgd_epoch(n, x_dev, y_dev, N, s);
     if (n->mbp) return mbp_epoch(n, x_dev, y_dev, N, s);
@@ -992,6 +1031,7 @@ static pnn_status launch_merge(pnn_net* n, int32_t broadcast, const double* w_de
 
 pnn_status pnn_merge(pnn_net* n, int32_t broadcast, void* hip_stream) {
     TRY(usable(n));
+    TRY(check_abort(n, true));
     return launch_merge(n, broadcast, nullptr, (double)n->cfg.replicas, (hipStream_t)hip_stream);
 }
 
@@ -1006,6 +1046,7 @@ pnn_status pnn_merge_weighted(pnn_net* n, const double* weights_host, int32_t br
         ws += v;
     }
     if (!(ws > 0.0) || !std::isfinite(ws)) return fail(n, PNN_EINVAL, "the weights sum to %g (must be positive)", ws);
+    TRY(check_abort(n, true));
     hipStream_t s = (hipStream_t)hip_stream;
     // the weights travel with the launch's stream order (the copy waits for earlier work)
     HIP_TRY(n, hipMemcpyAsync(n->d_mw, weights_host, sizeof(double) * K, hipMemcpyHostToDevice, s));
@@ -1091,6 +1132,7 @@ pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrow
     }
     if (!x_dev || !pred_dev) return fail(n, PNN_EINVAL, "x_dev / pred_dev is NULL");
     if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
+    TRY(check_abort(n, true));
     hipStream_t s = (hipStream_t)hip_stream;
     const bool count = correct_host && y_dev;
     TRY(run_inference(n, which, x_dev, nrows, pred_dev, out_dev, count, y_dev, nullptr, s));
@@ -1115,6 +1157,7 @@ pnn_status pnn_eval(pnn_net* n, int32_t which, const float* x_dev, const int32_t
     }
     if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
     if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
+    TRY(check_abort(n, true));
     hipStream_t s = (hipStream_t)hip_stream;
     if (cost_host && nrows > n->cost_rows) {
         HIP_TRY(n, hipStreamSynchronize(s));
@@ -1152,7 +1195,7 @@ pnn_status pnn_get_params(pnn_net* n, int32_t which, float* host_out) {
     if (!host_out) return fail(n, PNN_EINVAL, "host_out is NULL");
     if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
     HIP_TRY(n, hipDeviceSynchronize());
-    TRY(check_abort(n));
+    TRY(check_abort(n, true));
     std::vector<float> padded(n->pstride);
     const float* src = which < 0 ? n->merged : n->theta + (size_t)which * n->pstride;
     HIP_TRY(n, hipMemcpy(padded.data(), src, n->pstride * sizeof(float), hipMemcpyDeviceToHost));
@@ -1165,6 +1208,7 @@ pnn_status pnn_set_params(pnn_net* n, int32_t which, const float* host_in) {
     if (!host_in) return fail(n, PNN_EINVAL, "host_in is NULL");
     if (which < -2 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
     HIP_TRY(n, hipDeviceSynchronize());
+    TRY(check_abort(n, true));
     std::vector<float> padded(n->pstride);
     unpack(n, host_in, padded.data());
     const size_t bytes = n->pstride * sizeof(float);

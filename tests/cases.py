@@ -1,0 +1,69 @@
+"""Parity cases shared by the GPU parity tests and the CPU test of the oracle's own sensitivity
+to rounding (which shows, for each case, that its comparison bar measures the implementation and
+not the amplification of rounding differences)."""
+import pnn_inputs as I
+
+# ------------------------------------------------------------------------------------
+# full epochs at reduced sizes: ragged last batches / chunks, uneven slices, merges
+# (workload, overrides, N, epochs)
+
+EPOCH_CASES = [
+    # workload, overrides, N, epochs
+    (0, {}, 2000, 1),                                         # workload 0 at full size
+    (1, {}, 4 * 300 + 3, 1),                                  # per-sample chunks with a ragged tail
+    (1, dict(replicas=3), 3 * 140 + 1, 2),                    # uneven slices, two epochs
+    (2, {}, 16 * 100 + 5, 2),                                 # batches 32,32,32,4/5
+    (3, dict(replicas=8), 8 * 150 + 3, 2),                    # bf16, merge + broadcast each epoch
+    (4, dict(replicas=16), 16 * 260 + 7, 2),                  # batches 128,128,4/5, merge each epoch
+    (2, dict(sizes=(784, 64, 32, 10), acts=(I.RELU, I.TANH, I.SOFTMAX), loss=I.LOSS_XENT, batch=16,
+             replicas=2, merge_every_epoch=True), 2 * 90 + 1, 2),   # deeper fp32 net
+    (0, dict(sizes=(784, 32, 16, 10), acts=(I.TANH, I.SIGMOID, I.SIGMOID), replicas=2), 2 * 40, 1),  # B=1, L=3
+    (1, dict(acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, replicas=2), 2 * 150, 1),  # per-sample softmax/xent
+    # variants of the paper's first experiment: other activations, a large learning rate,
+    # full-batch gradient descent (a batch as large as the slice)
+    (1, dict(acts=(I.LEAKY_RELU, I.SOFTMAX), loss=I.LOSS_XENT, replicas=2), 2 * 150, 1),  # per-sample leaky ReLU
+    (1, dict(sizes=(784, 64, 10), acts=(I.TANH, I.SIGMOID), replicas=3), 3 * 100 + 2, 1),  # per-sample tanh
+    (1, dict(sizes=(784, 64, 10), acts=(I.TANH, I.SIGMOID), loss=I.LOSS_XENT, replicas=3), 3 * 100 + 2, 1),
+    (1, dict(lr=0.6, replicas=2), 2 * 120, 1),                # sigmoid, eta 0.6
+    (2, dict(sizes=(784, 96, 10), acts=(I.LEAKY_RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=8, replicas=4),
+     4 * 40 + 3, 2),                                          # mini-batch leaky ReLU / softmax
+    (2, dict(batch=101, replicas=4), 4 * 100 + 3, 3),         # full batch: one step per slice and epoch
+    # per-sample with more CNs than 16-row tile workgroups fit: 32-row tiles
+    (1, dict(replicas=32), 32 * 70 + 5, 1),
+    (1, dict(sizes=(784, 64, 10), replicas=60), 60 * 40 + 7, 1),
+    # persistent mini-batch plan: a hidden width that leaves the last 16-neuron tile half
+    # empty, batches of 7 and a grid that is no multiple of 8; 32-neuron tiles (20 CNs of 256
+    # neurons); batches of 2 with ReLU / softmax
+    (2, dict(sizes=(784, 56, 10), acts=(I.SIGMOID, I.SIGMOID), batch=7, replicas=5), 5 * 40 + 3, 2),
+    (2, dict(replicas=20), 20 * 40 + 3, 1),
+    (2, dict(acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=2, replicas=3), 3 * 30 + 2, 1),
+]
+
+
+# ------------------------------------------------------------------------------------
+# the per-sample chunked plan (B = 1, one hidden layer, where the persistent per-sample kernel
+# does not fit): overrides of the 784-128-10 per-sample workload and N, one epoch
+
+CHUNKED_CASES = [
+    # overrides of the 784-128-10 per-sample workload, N; chunk length T = 64 / 128 / 16 / 32
+    (dict(sizes=(784, 256, 10), replicas=2), 2 * 300 + 1),             # 4 full chunks + 44/45
+    (dict(replicas=64), 64 * 200 + 5),                                 # 64 CNs: 1 chunk + 72/73
+    (dict(sizes=(784, 1024, 10), replicas=2), 2 * 50 + 1),             # 3 chunks + 2/3
+    (dict(sizes=(784, 384, 10), acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, replicas=3), 3 * 90 + 2),
+]
+
+
+# ------------------------------------------------------------------------------------
+# bf16-mixed epochs: the weight tensors held elementwise after each epoch (all tensors are also
+# held normwise per layer).  A tensor is left out where the oracle's own divergence under a
+# one-ulp change of its start reaches half the bar (tests/test_sensitivity.py asserts both
+# sides); at full size (59 steps per epoch) every tensor is normwise only.
+# key: (workload, overrides as sorted items, N, epochs) -> {epoch: tensors}
+
+def case_key(idx, over, N, epochs):
+    return (idx, tuple(sorted(over.items())), N, epochs)
+
+
+BF16_ELEMENTWISE = {
+    case_key(3, dict(replicas=8), 8 * 150 + 3, 2): {0: ("W1", "W3"), 1: ("W3",)},
+}
