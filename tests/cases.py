@@ -23,7 +23,6 @@ EPOCH_CASES = [
     # full-batch gradient descent (a batch as large as the slice)
     (1, dict(acts=(I.LEAKY_RELU, I.SOFTMAX), loss=I.LOSS_XENT, replicas=2), 2 * 150, 1),  # per-sample leaky ReLU
     (1, dict(sizes=(784, 64, 10), acts=(I.TANH, I.SIGMOID), replicas=3), 3 * 100 + 2, 1),  # per-sample tanh
-    (1, dict(sizes=(784, 64, 10), acts=(I.TANH, I.SIGMOID), loss=I.LOSS_XENT, replicas=3), 3 * 100 + 2, 1),
     (1, dict(lr=0.6, replicas=2), 2 * 120, 1),                # sigmoid, eta 0.6
     (2, dict(sizes=(784, 96, 10), acts=(I.LEAKY_RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=8, replicas=4),
      4 * 40 + 3, 2),                                          # mini-batch leaky ReLU / softmax
@@ -39,6 +38,14 @@ EPOCH_CASES = [
     (2, dict(acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=2, replicas=3), 3 * 30 + 2, 1),
 ]
 
+# fp32 epoch cases where the method amplifies rounding differences to the size of the epoch bar
+# (tests/test_sensitivity.py: a one-ulp change of the oracle's own start moves some elements by
+# half the bar or more, while every layer stays below a tenth of it normwise).  On the GPU they
+# are held normwise per layer after the epoch, and elementwise step by step.
+SENSITIVE_FP32_CASES = [
+    # tanh hidden layer, sigmoid outputs with the cross-entropy error (per-sample)
+    (1, dict(sizes=(784, 64, 10), acts=(I.TANH, I.SIGMOID), loss=I.LOSS_XENT, replicas=3), 3 * 100 + 2, 1),
+]
 
 # ------------------------------------------------------------------------------------
 # the per-sample chunked plan (B = 1, one hidden layer, where the persistent per-sample kernel
@@ -65,5 +72,5 @@ def case_key(idx, over, N, epochs):
 
 
 BF16_ELEMENTWISE = {
-    case_key(3, dict(replicas=8), 8 * 150 + 3, 2): {0: ("W1", "W3"), 1: ("W3",)},
+    case_key(3, dict(replicas=8), 8 * 150 + 3, 2): {0: ("W1", "W3", "b3"), 1: ("W3",)},
 }

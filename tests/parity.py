@@ -7,13 +7,16 @@ The rms floor keeps near-zero entries (biases start at 0) from turning rounding 
 large relative errors.  Bars: 1e-5 after one training step and 1e-3 after full epochs in
 fp32; 2e-2 per step in bf16-mixed precision.
 
-bf16-mixed training over many steps is chaotic at the level of single rounding decisions:
-moving the oracle's own start by one fp32 ulp changes its hidden-layer biases by ~20% per
-element (~2-3% in norm) after one epoch, while the weights move by ~3e-4 in norm.  Over whole
-epochs in bf16 the comparison is therefore normwise per layer, with W_l and b_l together:
-    err(l) = ||gpu_l - ref_l||_2 / ||ref_l||_2 <= 2e-2,
-and every single step is held to the elementwise 2e-2 bar by a separate test that restarts
-the oracle from the GPU's state before each step.
+Where the method amplifies rounding differences to the size of a bar, that bar would measure
+the amplification rather than the implementation; tests/test_sensitivity.py measures, for every
+parity case, how far the oracle moves from its own run when its start moves by one fp32 ulp.
+Where that reaches half a bar for some tensor (bf16-mixed training over several steps; fp32
+nets with a tanh hidden layer under sigmoid outputs with the cross-entropy error), whole epochs
+are compared normwise per layer, W_l and b_l together:
+    err(l) = ||gpu_l - ref_l||_2 / ||ref_l||_2,
+the tensors that stay below half the bar elementwise (tests/cases.py) are still compared
+elementwise, and every single step of those nets is held elementwise by tests that restart the
+oracle from the GPU's state before each step.
 """
 from __future__ import annotations
 

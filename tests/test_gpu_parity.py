@@ -13,7 +13,7 @@ import pytest
 
 import pnn_inputs as I
 from oracle import oracle as O
-from tests.cases import BF16_ELEMENTWISE, CHUNKED_CASES, EPOCH_CASES, case_key
+from tests.cases import BF16_ELEMENTWISE, CHUNKED_CASES, EPOCH_CASES, SENSITIVE_FP32_CASES, case_key
 from tests.parity import (BF16_TOL, EPOCH_TOL, STEP_TOL, argmax_agrees, assert_close, log, oracle_replicas,
                           rel_err)
 
@@ -574,9 +574,26 @@ def test_eval_accuracy_and_cost(idx):
 
 
 # ------------------------------------------------------------------------------------
-# per-sample steps of a net whose training amplifies rounding (tanh hidden layer, sigmoid
-# outputs with the cross-entropy error; the whole epoch is also an epoch case above): every
-# step compared, the oracle restarting from the GPU's state.
+# nets whose training amplifies rounding differences to the size of the epoch bar (tanh hidden
+# layer, sigmoid outputs with the cross-entropy error; tests/test_sensitivity.py): whole epochs
+# normwise per layer, and every step elementwise with the oracle restarting from the GPU's state
+
+
+@pytest.mark.parametrize("idx,over,N,epochs", SENSITIVE_FP32_CASES)
+def test_sensitive_epochs_normwise(idx, over, N, epochs):
+    w = I.WORKLOADS[idx].scaled(**over)
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    for e in range(epochs):
+        net.train_epoch(dev(X), dev(y))
+        o.train_epoch(ref, X, y, threads=8)
+        for k in range(w.replicas):
+            assert_close(w.sizes, net.get_params(k), ref[k], EPOCH_TOL, f"epoch {e} replica {k}", layerwise=True)
+    net.close()
+
 
 
 def test_per_sample_stepwise_tanh_xent():

@@ -9,7 +9,8 @@ a wrong split or merge) fails at least one of them:
 * torch.autograd in float64 (a library routine computing the same derivative),
 * invariants of the method: shard partition, merge identities, mini-batch averaging,
   eta = 0, K = 1, replica independence, softmax normalisation,
-* bf16 rounding against torch's float32 -> bfloat16 conversion.
+* bf16 rounding against torch's float32 -> bfloat16 conversion, and a hand-derived bf16-mixed
+  step in which every rounding point of the mixed-precision reading changes the result.
 """
 import json
 import os
@@ -371,6 +372,34 @@ def test_bf16_rounding_matches_torch():
     ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
     got = np.array([O.round_bf16(float(a)) for a in v])
     np.testing.assert_array_equal(got, ref)
+
+
+def test_worked_2_2_2_sigmoid_softmax_bf16_step():
+    """One bf16-mixed step against a hand derivation (tests/golden/derive_bf16_step.py) in which
+    every rounding point of the reading changes the result: the oracle matches the derived
+    intermediates and updated parameters to 1e-12, and each variant with one rounding point moved
+    or dropped (x, operand weights, a1, d2, d1 unrounded; d1 rounded before the derivative
+    product; the derivative taken from the unrounded a1) is at least 5e-5 away from it."""
+    g = _load("worked_2_2_2_sigmoid_softmax_bf16.json")
+    o = O.Oracle(g["sizes"], [ACT[a] for a in g["acts"]], O.LOSS_XENT, precision=O.BF16, lr=g["lr"])
+    th = _flat(g)
+    x = np.array(g["x"], dtype=np.float32)
+    assert np.array_equal(x.astype(np.float64), g["x"])  # (the inputs are float32 values)
+    (z1, a1, d1), (z2, a2, d2) = o.trace(th, x, g["label"])
+    np.testing.assert_allclose(z1, g["z1"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(a1, g["a1b"], rtol=0, atol=0)       # hidden activation stored in bf16
+    np.testing.assert_allclose(z2, g["z2"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(a2, g["a2"], rtol=0, atol=1e-12)    # softmax output not rounded
+    np.testing.assert_allclose(d2, g["d2b"], rtol=0, atol=0)
+    np.testing.assert_allclose(d1, g["d1b"], rtol=0, atol=0)
+    theta = th[None, :].copy()
+    o.train_epoch(theta, x[None, :], np.array([g["label"]], np.int32))
+    got = theta[0]
+    want = _flat({"W1": g["W1_new"], "b1": g["b1_new"], "W2": g["W2_new"], "b2": g["b2_new"]})
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+    for name, v in g["variants"].items():
+        alt = _flat({"W1": v["W1_new"], "b1": v["b1_new"], "W2": v["W2_new"], "b2": v["b2_new"]})
+        assert np.max(np.abs(alt - want)) >= 5e-5, name
 
 
 def test_bf16_mode_equals_exact_mode_when_nothing_needs_rounding():
