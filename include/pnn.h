@@ -161,6 +161,20 @@ pnn_status pnn_infer(pnn_net* net, int32_t which, const float* x_dev, int64_t n,
 pnn_status pnn_eval(pnn_net* net, int32_t which, const float* x_dev, const int32_t* y_dev, int64_t n,
                     int64_t* correct_host, double* cost_host, void* hip_stream);
 
+/* pnn_eval without any device allocation, for callers that cannot allocate device memory
+ * (code that must not call hipMalloc: tight evaluation loops in serving or training, harnesses
+ * that forbid allocation).  Same arguments, results and errors as pnn_eval, computed by the same
+ * kernels; its workspace (a count, a sum, one 8,192-row chunk's hidden activations and, when
+ * cost_host is given, n per-row costs) lives in a fixed 64 MiB device array that the library
+ * holds on every GPU it runs on until the process ends, instead of in buffers grown with
+ * hipMalloc.  A call that needs more workspace than that returns PNN_ESHAPE and launches
+ * nothing (with cost_host: n <= 8,388,576 - 1,024 A up to alignment, A the bytes of hidden
+ * activations of one row: 4 per hidden neuron, 2 in bf16-mixed precision).  Every call on one GPU shares that GPU's array, which keeps the last call's contents:
+ * calls that overlap in time on one GPU (other host threads, other streams) race and must be
+ * serialised by the caller. */
+pnn_status pnn_eval_noalloc(pnn_net* net, int32_t which, const float* x_dev, const int32_t* y_dev, int64_t n,
+                            int64_t* correct_host, double* cost_host, void* hip_stream);
+
 /* Copies one network's parameters (which = -1 merged, 0..K-1 a CN) to host_out (P floats)
  * in the layout above.  Waits for the device. */
 pnn_status pnn_get_params(pnn_net* net, int32_t which, float* host_out);

@@ -24,6 +24,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -32,9 +33,27 @@
 
 using namespace pnn;
 
+// Fixed workspace of pnn_eval_noalloc, for callers that cannot allocate device memory: one
+// copy per GPU, held until the process ends.  In host code `scratch` names a host-side stand-in
+// of the array, not its device address: host code reaches the memory only through the address
+// that hipGetSymbolAddress gives for the current device (scratch_setup, scratch_ptr).
+constexpr size_t SCRATCH_BYTES = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_init_error;
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[MAX_DEVICES] = {nullptr};
+
+// device address of the workspace on `dev` (NULL before scratch_setup ran there)
+void* scratch_ptr(int dev) {
+    if (dev < 0 || dev >= MAX_DEVICES) return nullptr;
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    return g_scratch_addr[dev];
+}
 
 struct ProfRec {
     const char* name;
@@ -814,6 +833,18 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         return st;
     };
     if (hipGetDevice(&n->device) != hipSuccess) return bail(fail(n, PNN_EHIP, "no HIP device"));
+    {
+        // the device address of the fixed workspace, once per device (this device is current)
+        if (n->device >= MAX_DEVICES) return bail(fail(n, PNN_EINVAL, "device %d: at most %d devices", n->device, MAX_DEVICES));
+        std::lock_guard<std::mutex> g(g_scratch_mu);
+        if (!g_scratch_addr[n->device]) {
+            void* p = nullptr;
+            const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess || !p)
+                return bail(fail(n, PNN_EHIP, "hipGetSymbolAddress of the workspace failed: %s", hipGetErrorString(e)));
+            g_scratch_addr[n->device] = p;
+        }
+    }
     // failure-handling tests: PNN_SPIN_LIMIT bounds the persistent kernels' waits (polls);
     // PNN_TEST_STALL_WAITS=1 makes the persistent kernels' waits run into that bound
     n->spin_limit = SPIN_LIMIT;
@@ -1054,15 +1085,24 @@ pnn_status pnn_merge_weighted(pnn_net* n, const double* weights_host, int32_t br
     return launch_merge(n, broadcast, n->d_mw, ws, s);
 }
 
-// forward pass of one network over nrows data-set rows in chunks, then the output layer:
-// predictions (pred, nullable), outputs (out, nullable), the correct count into d_correct
-// (count), per-row costs into cost (nullable; needs y)
-static pnn_status run_inference(pnn_net* n, int32_t which, const float* x_dev, int64_t nrows, int32_t* pred_dev,
-                                float* out_dev, bool count, const int32_t* y_dev, double* cost, hipStream_t s) {
-    if (count) zero_ints_kernel<<<1, 256, 0, s>>>((int*)n->d_correct, 2);
+// rows of one inference chunk
+constexpr int INFER_CHUNK = 8192;
+
+// workspace bytes of an allocation-free evaluation of nrows rows: counters, one chunk's hidden
+// activations, per-row costs (when the cost is asked for)
+static int64_t noalloc_eval_bytes(const pnn_net* n, int64_t nrows, bool cost) {
+    const int rows = (int)std::min<int64_t>(nrows, INFER_CHUNK);
+    const int64_t el = n->bf16 ? 2 : 4;
+    int64_t b = 256;
+    for (int l = 1; l < n->L; ++l) b += round_up((int64_t)rows * n->sizes[l] * el, 256);
+    if (cost) b += nrows * (int64_t)sizeof(double);
+    return b;
+}
+
+// the handle's inference workspace for min(nrows, INFER_CHUNK) rows (grown with hipMalloc)
+static pnn_status grow_inference_ws(pnn_net* n, int64_t nrows, hipStream_t s) {
     const int L = n->L;
-    const int CH = 8192;
-    const int rows = (int)std::min<int64_t>(nrows, CH);
+    const int rows = (int)std::min<int64_t>(nrows, INFER_CHUNK);
     if (L > 1 && rows > n->inf_rows) {
         HIP_TRY(n, hipStreamSynchronize(s));
         const size_t el = n->bf16 ? 2 : 4;
@@ -1073,6 +1113,19 @@ static pnn_status run_inference(pnn_net* n, int32_t which, const float* x_dev, i
         }
         n->inf_rows = rows;
     }
+    return PNN_OK;
+}
+
+// forward pass of one network over nrows data-set rows in chunks of INFER_CHUNK, then the
+// output layer: predictions (pred, nullable), outputs (out, nullable), the correct count into
+// *correct (count; zeroed first), per-row costs into cost (nullable; needs y).  ws[l] holds
+// the activations of hidden layer l for a chunk.
+static pnn_status run_inference(pnn_net* n, int32_t which, const float* x_dev, int64_t nrows, int32_t* pred_dev,
+                                float* out_dev, bool count, const int32_t* y_dev, double* cost, void* const* ws,
+                                unsigned long long* correct, hipStream_t s) {
+    if (count) zero_ints_kernel<<<1, 256, 0, s>>>((int*)correct, 2);
+    const int L = n->L;
+    const int CH = INFER_CHUNK;
     const float* th = which < 0 ? n->merged : n->theta + (size_t)which * n->pstride;
     const bf16_t* sh = !n->bf16 ? nullptr : (which < 0 ? n->mshadow : n->shadow + (size_t)which * n->pstride);
     for (int64_t r0 = 0; r0 < nrows; r0 += CH) {
@@ -1081,8 +1134,8 @@ static pnn_status run_inference(pnn_net* n, int32_t which, const float* x_dev, i
             GemmArgs g = gemm_base(n, CH, n->sizes[l], n->sizes[l - 1], nrows, r0, CH, 1);
             g.k_rep = 1;
             if (l == 1) g.a = opnd(x_dev, 0, n->sizes[0], 1);
-            else g.a = opnd(n->inf_ws[l - 1], 0, n->sizes[l - 1], 0);
-            g.c = n->inf_ws[l]; g.c_z = 0; g.c_ld = n->sizes[l];
+            else g.a = opnd(ws[l - 1], 0, n->sizes[l - 1], 0);
+            g.c = ws[l]; g.c_z = 0; g.c_ld = n->sizes[l];
             g.bias = th + n->off_b[l - 1]; g.bias_z = 0;
             g.act = n->act[l - 1];
             g.M = std::min<int64_t>(CH, nrows - r0);
@@ -1099,11 +1152,11 @@ static pnn_status run_inference(pnn_net* n, int32_t which, const float* x_dev, i
         RowArgs a;
         memset(&a, 0, sizeof a);
         if (L == 1) { a.x = x_dev; a.x_xrows = 1; a.x_ld = n->sizes[0]; }
-        else { a.x = n->inf_ws[L - 1]; a.x_z = 0; a.x_ld = n->sizes[L - 1]; }
+        else { a.x = ws[L - 1]; a.x_z = 0; a.x_ld = n->sizes[L - 1]; }
         a.bias = th + n->off_b[L - 1];
         a.H = n->sizes[L - 1]; a.O = n->sizes[L]; a.act = n->act[L - 1]; a.loss = n->cfg.loss;
         a.n_total = nrows; a.k_rep = 1; a.r0 = r0; a.step_rows = CH;
-        a.y = y_dev; a.out = out_dev; a.pred = pred_dev; a.correct = count ? n->d_correct : nullptr;
+        a.y = y_dev; a.out = out_dev; a.pred = pred_dev; a.correct = count ? correct : nullptr;
         a.cost = cost;
         const int rws = (int)std::min<int64_t>(CH, nrows - r0);
         dim3 grid((rws + 3) / 4, 1, 1);
@@ -1121,6 +1174,28 @@ static pnn_status run_inference(pnn_net* n, int32_t which, const float* x_dev, i
     return PNN_OK;
 }
 
+// the evaluation of pnn_eval on a given workspace: correct count into *correct, per-row costs
+// into cost[nrows] summed in a fixed order into *cost_sum; waits for the device
+static pnn_status eval_run(pnn_net* n, int32_t which, const float* x_dev, const int32_t* y_dev, int64_t nrows,
+                           int64_t* correct_host, double* cost_host, void* const* ws, unsigned long long* correct,
+                           double* cost, double* cost_sum, hipStream_t s) {
+    TRY(run_inference(n, which, x_dev, nrows, nullptr, nullptr, correct_host != nullptr, y_dev,
+                      cost_host ? cost : nullptr, ws, correct, s));
+    if (cost_host) {
+        Launch lc(n, s, "eval_cost_sum");
+        sum_f64_kernel<<<1, 256, 0, s>>>(cost, nrows, cost_sum);
+        TRY(lc.done());
+    }
+    unsigned long long c = 0;
+    double cs = 0.0;
+    if (correct_host) HIP_TRY(n, hipMemcpyAsync(&c, correct, sizeof c, hipMemcpyDeviceToHost, s));
+    if (cost_host) HIP_TRY(n, hipMemcpyAsync(&cs, cost_sum, sizeof cs, hipMemcpyDeviceToHost, s));
+    HIP_TRY(n, hipStreamSynchronize(s));
+    if (correct_host) *correct_host = (int64_t)c;
+    if (cost_host) *cost_host = cs / (double)nrows;
+    return PNN_OK;
+}
+
 pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrows, int32_t* pred_dev, float* out_dev,
                      int64_t* correct_host, const int32_t* y_dev, void* hip_stream) {
     TRY(usable(n));
@@ -1135,7 +1210,8 @@ pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrow
     TRY(check_abort(n, true));
     hipStream_t s = (hipStream_t)hip_stream;
     const bool count = correct_host && y_dev;
-    TRY(run_inference(n, which, x_dev, nrows, pred_dev, out_dev, count, y_dev, nullptr, s));
+    TRY(grow_inference_ws(n, nrows, s));
+    TRY(run_inference(n, which, x_dev, nrows, pred_dev, out_dev, count, y_dev, nullptr, n->inf_ws, n->d_correct, s));
     if (count) {
         unsigned long long c = 0;
         HIP_TRY(n, hipMemcpyAsync(&c, n->d_correct, sizeof c, hipMemcpyDeviceToHost, s));
@@ -1167,21 +1243,45 @@ pnn_status pnn_eval(pnn_net* n, int32_t which, const float* x_dev, const int32_t
         TRY(dev_alloc(n, &n->d_cost, (size_t)nrows));
         n->cost_rows = nrows;
     }
-    TRY(run_inference(n, which, x_dev, nrows, nullptr, nullptr, correct_host != nullptr, y_dev,
-                      cost_host ? n->d_cost : nullptr, s));
-    if (cost_host) {
-        Launch lc(n, s, "eval_cost_sum");
-        sum_f64_kernel<<<1, 256, 0, s>>>(n->d_cost, nrows, n->d_cost_sum);
-        TRY(lc.done());
+    TRY(grow_inference_ws(n, nrows, s));
+    return eval_run(n, which, x_dev, y_dev, nrows, correct_host, cost_host, n->inf_ws, n->d_correct, n->d_cost,
+                    n->d_cost_sum, s);
+}
+
+pnn_status pnn_eval_noalloc(pnn_net* n, int32_t which, const float* x_dev, const int32_t* y_dev, int64_t nrows,
+                            int64_t* correct_host, double* cost_host, void* hip_stream) {
+    TRY(usable(n));
+    if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
+    if (nrows < 0) return fail(n, PNN_ESHAPE, "n < 0");
+    if (nrows == 0) {
+        if (correct_host) *correct_host = 0;
+        if (cost_host) *cost_host = 0.0;
+        return PNN_OK;
     }
-    unsigned long long c = 0;
-    double cs = 0.0;
-    if (correct_host) HIP_TRY(n, hipMemcpyAsync(&c, n->d_correct, sizeof c, hipMemcpyDeviceToHost, s));
-    if (cost_host) HIP_TRY(n, hipMemcpyAsync(&cs, n->d_cost_sum, sizeof cs, hipMemcpyDeviceToHost, s));
-    HIP_TRY(n, hipStreamSynchronize(s));
-    if (correct_host) *correct_host = (int64_t)c;
-    if (cost_host) *cost_host = cs / (double)nrows;
-    return PNN_OK;
+    if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
+    if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
+    char* base = (char*)scratch_ptr(n->device);
+    if (!base) return fail(n, PNN_ESTATE, "no workspace address for device %d", n->device);
+    // workspace layout: [correct count, cost sum] | hidden activations of a chunk, layer by
+    // layer | per-row costs
+    const int64_t need = noalloc_eval_bytes(n, nrows, cost_host != nullptr);
+    if (need > (int64_t)SCRATCH_BYTES)
+        return fail(n, PNN_ESHAPE, "evaluating %lld rows needs %lld bytes of workspace; the fixed workspace has %lld",
+                    (long long)nrows, (long long)need, (long long)SCRATCH_BYTES);
+    TRY(check_abort(n, true));
+    hipStream_t s = (hipStream_t)hip_stream;
+    unsigned long long* correct = (unsigned long long*)base;
+    double* cost_sum = (double*)(base + 8);
+    void* ws[9] = {nullptr};
+    int64_t o = 256;
+    const int rows = (int)std::min<int64_t>(nrows, INFER_CHUNK);
+    const int64_t el = n->bf16 ? 2 : 4;
+    for (int l = 1; l < n->L; ++l) {
+        ws[l] = base + o;
+        o += round_up((int64_t)rows * n->sizes[l] * el, 256);
+    }
+    double* cost = cost_host ? (double*)(base + o) : nullptr;
+    return eval_run(n, which, x_dev, y_dev, nrows, correct_host, cost_host, ws, correct, cost, cost_sum, s);
 }
 
 const char* pnn_plan(const pnn_net* n) {

@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
         L.pnn_infer.argtypes = [vp, i32, vp, i64, vp, vp, P(i64), vp, vp]
         L.pnn_infer.restype = i32
         L.pnn_eval.argtypes = [vp, i32, vp, vp, i64, P(i64), P(ctypes.c_double), vp]
+        L.pnn_eval_noalloc.argtypes = [vp, i32, vp, vp, i64, P(i64), P(ctypes.c_double), vp]
+        L.pnn_eval_noalloc.restype = i32
         L.pnn_merge_weighted.argtypes = [vp, P(ctypes.c_double), i32, vp]
         L.pnn_train_epoch_order.argtypes = [vp, vp, vp, i64, vp, vp]
         L.pnn_train_epoch_order.restype = i32
@@ -204,6 +206,16 @@ class PNN:
         self._check(self._lib.pnn_eval(self.h, which, _dev_ptr(x, "torch.float32"), _dev_ptr(y, "torch.int32"),
                                        x.shape[0], ctypes.byref(c), ctypes.byref(cost), _stream_handle(stream)),
                     "pnn_eval")
+        return c.value, cost.value
+
+    def evaluate_noalloc(self, x, y, which: int = -1, stream=None):
+        """(correct count, mean cost) as evaluate, on the library's fixed workspace
+        (pnn_eval_noalloc: no device allocation)."""
+        c = ctypes.c_int64(-1)
+        cost = ctypes.c_double(float("nan"))
+        self._check(self._lib.pnn_eval_noalloc(self.h, which, _dev_ptr(x, "torch.float32"),
+                                               _dev_ptr(y, "torch.int32"), x.shape[0], ctypes.byref(c),
+                                               ctypes.byref(cost), _stream_handle(stream)), "pnn_eval_noalloc")
         return c.value, cost.value
 
     def get_params(self, which: int = -1) -> np.ndarray:
