@@ -733,6 +733,507 @@ __global__ __launch_bounds__(256) void gemm128_kernel(GemmArgs g) {
 }
 
 // ------------------------------------------------------------------------------------
+// fp32 GEMM on the bf16 matrix cores, 128 x 128 tiles.
+//
+// An fp32 value a is the exact sum of three bf16 parts, a = a_h + a_m + a_l: a_h = RNE(a), the
+// remainder a - a_h (exact in fp32, at most 16 significant bits) gives a_m = RNE of it, and the
+// second remainder (at most 8 significant bits) is a_l exactly.  The product a b is the sum of
+// the nine part products; the six kept (hh, hm, mh, hl, lh, mm) leave out terms below
+// 2^-23 |a b| together, and each part product is exact in the fp32 accumulator's input.  A
+// 32-deep k-tile thus takes six v_mfma_f32_16x16x32_bf16 (16 cycles each) per 16 x 16 output
+// block instead of eight v_mfma_f32_16x16x4_f32 (32 cycles each): the matrix cores run bf16 at
+// sixteen times their fp32 rate on this chip.  The sum carries rounding errors of the same size
+// as the plain fp32 matrix instruction's (one fp32 rounding per instruction and output; the
+// small terms go first).
+//
+// Eight waves of 64 x 32 (4 x 2 blocks of 16 x 16), two per SIMD, one workgroup per CU (120 KiB
+// of dynamic LDS: two stages of both operands' three bf16 planes [t][k], row stride 40, which
+// the 16-byte fragment reads cover without bank conflicts).  The fp32 operands are loaded two
+// k-tiles ahead into registers through bounds-checked buffer loads; while the matrix
+// instructions of k-tile k run, the wave splits k-tile k+1 (v_cvt_pk_bf16_f32, round to nearest
+// even) into the other stage.  KC operands (rows = t) load a float4 of 4 k per thread and row;
+// NC operands (rows = k) a 2 k x 4 t block, whose pairs of k pack into the 4-byte stores of the
+// transpose.  The weight update (EPI_UPD) loads its targets before the contraction.  Epilogues
+// as in gemm128_kernel (fp32 outputs).
+
+constexpr int B3_THREADS = 512;
+constexpr int B3_BK = 32, B3_LDK = 40, B3_PLANE = 128 * B3_LDK;   // bf16 elements
+constexpr int B3_STAGE = 2 * 3 * B3_PLANE;                         // A and B, three planes each
+__host__ __device__ constexpr size_t b3_lds_bytes() { return (size_t)2 * B3_STAGE * sizeof(bf16_t); }
+
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+// two floats to packed bf16 (one v_cvt_pk_bf16_f32), x in the low half
+__device__ inline uint32_t cvt_pk_bf16(float x, float y) {
+    const bf2v p = {(__bf16)x, (__bf16)y};
+    return __builtin_bit_cast(uint32_t, p);
+}
+// the fp32 value of the low bf16 of a packed pair (a byte permute: written as a shift, the
+// compiler re-derives it with a second conversion)
+__device__ inline float bf_lo(uint32_t p) { return __uint_as_float(__builtin_amdgcn_perm(0u, p, 0x01000c0cu)); }
+__device__ inline float bf_hi(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
+// split two floats into their three packed bf16 parts
+__device__ inline void split3_pk(float x, float y, uint32_t& h, uint32_t& m, uint32_t& l) {
+    h = cvt_pk_bf16(x, y);
+    const float rx = x - bf_lo(h), ry = y - bf_hi(h);
+    m = cvt_pk_bf16(rx, ry);
+    l = cvt_pk_bf16(rx - bf_lo(m), ry - bf_hi(m));
+}
+
+// one operand's k-tile (128 t x 32 k), as loaded by thread tid: KC v[u] = row kc_row(tid, u),
+// k 4 (tid & 7) .. + 3; NC v[e] = k 2 (tid & 15) + e, columns 4 (tid >> 4) .. + 3
+struct B3Raw { float4 v[2]; };
+
+// KC rows: a wave's part u covers rows {0, 4, 8, 12} (lanes 0-31) and {1, 5, 9, 13} (lanes
+// 32-63) of a 16-row block (or those + 2), so that the 64-byte pieces its lanes store fall on
+// disjoint LDS banks at the 80-byte row stride
+__device__ inline int kc_row(int tid, int u) {
+    const int L = tid & 63, b = 2 * (tid >> 6) + u;  // b: 16 blocks of 8 rows
+    return 16 * (b >> 1) + 2 * (b & 1) + 4 * ((L >> 3) & 3) + (L >> 5);
+}
+
+// Branch-free loads through a buffer descriptor: an element outside the tile's valid rows lies
+// past the descriptor's range, one past the valid contraction gets an offset beyond it, and both
+// read as zero, so the wait counters stay exact across the pipeline.  KC: the descriptor starts
+// at the tile's first row (t0) and spans its valid rows; NC: it starts at the tile's first
+// column (t0) of contraction row 0 and ends with the last valid contraction row.
+struct B3Src {
+    uint64_t base;  // first byte (the same in every lane)
+    int nbytes;     // bytes in range
+    uint32_t ld4;   // row stride in bytes
+};
+
+template <bool KC>
+__device__ inline B3Src b3_src(const Operand& o, int z, int cn, int64_t xbase, int t0, int t_valid, int k_valid) {
+    B3Src r;
+    r.ld4 = (uint32_t)(o.ld * 4);
+    const int rows = KC ? t_valid - t0 : k_valid;
+    const char* base = KC ? operand_row(o, 4, z, cn, xbase, t0) : operand_row(o, 4, z, cn, xbase, 0) + (size_t)t0 * 4;
+    int64_t bytes = (int64_t)rows * o.ld * 4 - (KC ? 0 : (int64_t)t0 * 4);
+    if (rows <= 0 || bytes < 0) bytes = 0;
+    r.base = (uint64_t)base;
+    r.nbytes = (int)bytes;
+    return r;
+}
+
+// the descriptor, built where it is used from values made scalar explicitly (they are the same
+// in every lane; otherwise every buffer load would loop over the lanes' descriptors)
+__device__ inline __amdgpu_buffer_rsrc_t b3_rsrc(const B3Src& src) {
+    const uint64_t a = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(src.base >> 32)) << 32) |
+                       (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)src.base);
+    return __builtin_amdgcn_make_buffer_rsrc((void*)a, (short)0, __builtin_amdgcn_readfirstlane(src.nbytes), 0x00020000);
+}
+
+template <bool KC>
+__device__ inline void b3_load(B3Raw& r, const B3Src& src, int t_valid_rel, int k0, int k_valid, int tid) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        int t, k;
+        if (KC) { t = kc_row(tid, u); k = (tid & 7) * 4; }
+        else { t = (tid >> 4) * 4; k = 2 * (tid & 15) + u; }
+        // the offset, with its top bit set (past any range) when the element is invalid
+        // (arithmetic, not a select: the compiler would turn a select into branches)
+        const uint32_t inv = KC ? (uint32_t)(k_valid - 1 - (k0 + k)) >> 31 : (uint32_t)(t_valid_rel - 1 - t) >> 31;
+        const uint32_t off = (KC ? (uint32_t)t * src.ld4 + (uint32_t)(k0 + k) * 4u
+                                 : (uint32_t)(k0 + k) * src.ld4 + (uint32_t)t * 4u) | (inv << 31);
+        r.v[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(src), off, 0, 0));
+    }
+}
+
+// split and store part u (0, 1) of a loaded k-tile into the three planes
+template <bool KC>
+__device__ inline void b3_store_part(bf16_t* lds, const B3Raw& r, int u, int tid) {
+    if (KC) {
+        const int t = kc_row(tid, u), k = (tid & 7) * 4;
+        uint32_t h0, m0, l0, h1, m1, l1;
+        split3_pk(r.v[u].x, r.v[u].y, h0, m0, l0);
+        split3_pk(r.v[u].z, r.v[u].w, h1, m1, l1);
+        bf16_t* d = lds + t * B3_LDK + k;
+        *(uint2*)d = make_uint2(h0, h1);
+        *(uint2*)(d + B3_PLANE) = make_uint2(m0, m1);
+        *(uint2*)(d + 2 * B3_PLANE) = make_uint2(l0, l1);
+    } else {
+        // columns t + 2 u, t + 2 u + 1 of rows k, k + 1
+        const int t = (tid >> 4) * 4 + 2 * u, k = 2 * (tid & 15);
+        const float a0 = u ? r.v[0].z : r.v[0].x, a1 = u ? r.v[0].w : r.v[0].y;
+        const float c0 = u ? r.v[1].z : r.v[1].x, c1 = u ? r.v[1].w : r.v[1].y;
+        uint32_t h, m, l;
+        bf16_t* d = lds + t * B3_LDK + k;
+        split3_pk(a0, c0, h, m, l);
+        *(uint32_t*)d = h; *(uint32_t*)(d + B3_PLANE) = m; *(uint32_t*)(d + 2 * B3_PLANE) = l;
+        split3_pk(a1, c1, h, m, l);
+        d += B3_LDK;
+        *(uint32_t*)d = h; *(uint32_t*)(d + B3_PLANE) = m; *(uint32_t*)(d + 2 * B3_PLANE) = l;
+    }
+}
+
+template <bool A_KC, bool B_KC, int EPI>
+__global__ __launch_bounds__(B3_THREADS) void gemm128x3_kernel(GemmArgs g) {
+    extern __shared__ __attribute__((aligned(16))) bf16_t b3s[];  // [2 stages][A 3 planes, B 3 planes]
+    __shared__ float rowsum[128];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 2, wn = wave & 3;  // wave tile: rows 64 wm .., columns 32 wn ..
+    int bx, by, bz;
+    gemm_tile(bx, by, bz);
+    const int zz = bz / g.ksplit, slice = bz % g.ksplit;
+    int cn, valid;
+    int64_t r0;
+    gemm_zinfo(g, zz, cn, r0, valid);
+    const int Mv = (g.sample_dims & 1) ? valid : g.M;
+    const int Nv = (g.sample_dims & 2) ? valid : g.N;
+    const int Kv = (g.sample_dims & 4) ? valid : g.Kd;
+    const int m0 = by * 128, n0 = bx * 128;
+    if (m0 >= Mv || n0 >= Nv) return;
+    const int kbeg = slice * g.kchunk;
+    const int kend = min(Kv, kbeg + g.kchunk);
+    const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
+    const bool do_rowsum = (EPI == EPI_UPD) && g.ubias != nullptr && bx == 0;
+    if (do_rowsum && tid < 128) rowsum[tid] = 0.f;
+    const bool vec = ((g.c_ld | g.c_z | g.c_split | g.bias_z) & 3) == 0;
+    // (operands enter swapped: lane holds row m0 + 64 wm + 16 i + (lane & 15), columns
+    // n .. n+3 with n = n0 + 32 wn + 16 j + 4 (lane >> 4))
+    auto coord = [&](int i, int j, int& m, int& n) {
+        m = m0 + wm * 64 + i * 16 + (lane & 15);
+        n = n0 + wn * 32 + j * 16 + (lane >> 4) * 4;
+    };
+
+    // the update's targets, read before the contraction (their latency behind it)
+    float4 wpre[4][2];
+    if constexpr (EPI == EPI_UPD) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                int m, n;
+                coord(i, j, m, n);
+                const float* W = (const float*)g.c + (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+                wpre[i][j] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (m < Mv && n < Nv) {
+                    if (vec && n + 3 < Nv) wpre[i][j] = *(const float4*)W;
+                    else {
+                        wpre[i][j].x = W[0];
+                        if (n + 1 < Nv) wpre[i][j].y = W[1];
+                        if (n + 2 < Nv) wpre[i][j].z = W[2];
+                    }
+                }
+            }
+    }
+
+    f4 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    B3Raw ra, rb, na, nb;  // k-tiles in flight: the one split during the current tile, the one after
+    const B3Src sa = b3_src<A_KC>(g.a, zz, cn, xbase, m0, Mv, kend);
+    const B3Src sb = b3_src<B_KC>(g.b, zz, cn, xbase, n0, Nv, kend);
+    auto load = [&](B3Raw& xa, B3Raw& xb, int k0) {  // (zeros past kend)
+        b3_load<A_KC>(xa, sa, Mv - m0, k0, kend, tid);
+        b3_load<B_KC>(xb, sb, Nv - n0, k0, kend, tid);
+    };
+    load(ra, rb, kbeg);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        b3_store_part<A_KC>(b3s, ra, u, tid);
+        b3_store_part<B_KC>(b3s + 3 * B3_PLANE, rb, u, tid);
+    }
+    load(ra, rb, kbeg + B3_BK);
+    __syncthreads();
+    int buf = 0;
+    const int rl = lane & 15, kg = lane >> 4;
+    // one k-tile: the loads of the tile two ahead into (ya, yb), the tile's matrix instructions
+    // from stage buf, the next tile (xa, xb) split into the other stage between them
+    auto step = [&](int k0, const B3Raw& xa, const B3Raw& xb, B3Raw& ya, B3Raw& yb) {
+        // (the loads and the split run on past kend, on zeros: no branch in the pipeline)
+        load(ya, yb, k0 + 2 * B3_BK);
+        const bf16_t* A = b3s + buf * B3_STAGE;
+        const bf16_t* Bt = A + 3 * B3_PLANE;
+        bf16_t* An = b3s + (buf ^ 1) * B3_STAGE;
+        if (do_rowsum && tid < 128) {
+            // the bias gradient: the tile's rows of A summed over k (h + m + l is a exactly)
+            float sr = 0.f;
+#pragma unroll
+            for (int k = 0; k < B3_BK; ++k) {
+                const int o = tid * B3_LDK + k;
+                sr += (bf2f(A[o]) + bf2f(A[o + B3_PLANE])) + bf2f(A[o + 2 * B3_PLANE]);
+            }
+            rowsum[tid] += sr;
+        }
+        bf8v av[3][4], bv[3][2];
+#pragma unroll
+        for (int p = 0; p < 3; ++p) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                av[p][i] = *(const bf8v*)(A + p * B3_PLANE + (wm * 64 + i * 16 + rl) * B3_LDK + kg * 8);
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                bv[p][j] = *(const bf8v*)(Bt + p * B3_PLANE + (wn * 32 + j * 16 + rl) * B3_LDK + kg * 8);
+        }
+        // six groups of 8 matrix instructions, small terms first: (a part, b part) = lh, hl, mm,
+        // mh, hm, hh; the next k-tile's split and store in between
+        constexpr int PA[6] = {2, 0, 1, 1, 0, 0}, PB[6] = {0, 2, 1, 0, 1, 0};
+#pragma unroll
+        for (int t = 0; t < 6; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[PB[t]][j], av[PA[t]][i], acc[i][j], 0, 0, 0);
+            if (t == 0 || t == 1) b3_store_part<A_KC>(An, xa, t, tid);
+            if (t == 2 || t == 3) b3_store_part<B_KC>(An + 3 * B3_PLANE, xb, t - 2, tid);
+        }
+        __syncthreads();
+        buf ^= 1;
+    };
+    // two k-tiles per trip, the register sets alternating (no copy between them)
+    for (int k0 = kbeg; k0 < kend; k0 += 2 * B3_BK) {
+        step(k0, ra, rb, na, nb);
+        if (k0 + B3_BK >= kend) break;
+        step(k0 + B3_BK, na, nb, ra, rb);
+    }
+
+    float scale = g.lr;
+    if (EPI == EPI_UPD && g.scale_per_batch) scale = valid > 0 ? g.lr / (float)valid : 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            int m, n;
+            coord(i, j, m, n);
+            if (m >= Mv || n >= Nv) continue;
+            const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+            const f4 v = acc[i][j];
+            if (vec && n + 3 < Nv) {
+                const float4 c4 = make_float4(v[0], v[1], v[2], v[3]);
+                if constexpr (EPI == EPI_STORE) {
+                    *(float4*)((float*)g.c + ci + (size_t)slice * g.c_split) = c4;
+                } else if constexpr (EPI == EPI_FWD) {
+                    const float4 bb = *(const float4*)(g.bias + (size_t)cn * g.bias_z + n);
+                    *(float4*)((float*)g.c + ci) = make_float4(act_fn(g.act, c4.x + bb.x), act_fn(g.act, c4.y + bb.y),
+                                                               act_fn(g.act, c4.z + bb.z), act_fn(g.act, c4.w + bb.w));
+                } else if constexpr (EPI == EPI_BWD) {
+                    const float4 x = *(const float4*)((const float*)g.aux + ci);
+                    *(float4*)((float*)g.c + ci) = make_float4(c4.x * act_deriv(g.act, x.x), c4.y * act_deriv(g.act, x.y),
+                                                               c4.z * act_deriv(g.act, x.z), c4.w * act_deriv(g.act, x.w));
+                } else {  // EPI_UPD: in-place W -= scale * acc
+                    float4 w = wpre[i][j];
+                    w.x -= scale * c4.x; w.y -= scale * c4.y; w.z -= scale * c4.z; w.w -= scale * c4.w;
+                    *(float4*)((float*)g.c + ci) = w;
+                }
+            } else {
+                const float wp[4] = {wpre[i][j].x, wpre[i][j].y, wpre[i][j].z, wpre[i][j].w};
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if (n + r >= Nv) continue;
+                    const size_t cr = ci + r;
+                    if constexpr (EPI == EPI_STORE) {
+                        ((float*)g.c)[cr + (size_t)slice * g.c_split] = v[r];
+                    } else if constexpr (EPI == EPI_FWD) {
+                        const float zv = v[r] + g.bias[(size_t)cn * g.bias_z + n + r];
+                        ((float*)g.c)[cr] = act_fn(g.act, zv);
+                    } else if constexpr (EPI == EPI_BWD) {
+                        const float x = ((const float*)g.aux)[cr];
+                        ((float*)g.c)[cr] = v[r] * act_deriv(g.act, x);
+                    } else {
+                        ((float*)g.c)[cr] = wp[r] - scale * v[r];
+                    }
+                }
+            }
+        }
+    if (do_rowsum && tid < 128 && m0 + tid < Mv) {
+        float* b = g.ubias + (size_t)cn * g.bias_z;
+        b[m0 + tid] -= scale * rowsum[tid];
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Weight update W -= eta / B_t * delta^T x on the bf16 matrix cores (fp32 operands split in
+// three bf16 parts, as in gemm128x3_kernel), for a contraction over at most 128 samples.
+//
+// One workgroup (eight waves, one per CU) owns a 128-row strip of W (rows m0 .. m0 + 127, all
+// N columns) of one CN: it splits the strip's errors delta[s][m0 ..] for every sample s once
+// into LDS (three planes [m][s], 128 samples, 16-byte chunks XOR-swizzled by the row so that
+// neither the transposing stores nor the fragment reads meet bank conflicts), subtracts the
+// bias gradient eta / B_t sum_s delta[s][m], and then walks the strip's 128-column tiles: the
+// samples' input columns x[s][n0 ..] stream through two LDS stages in k-chunks of 32 samples
+// (loaded two chunks ahead, across tile boundaries), and each finished tile's targets, loaded
+// one tile ahead, take their update and go back.  A: NC operand (rows = samples), B: NC.
+
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+constexpr int U3_KMAX = 128;   // samples of one update
+constexpr int U3_DPLANE = 128 * U3_KMAX;
+__host__ __device__ constexpr size_t u3_lds_bytes() {
+    return (size_t)3 * U3_DPLANE * sizeof(bf16_t) + (size_t)2 * 3 * B3_PLANE * sizeof(bf16_t);
+}
+// element offset of (row m, sample k) in a plane of the errors (16-byte chunks swizzled)
+__device__ inline int u3_off(int m, int k) { return m * U3_KMAX + ((((k >> 3) ^ (m & 15))) << 3) + (k & 7); }
+
+__global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
+    extern __shared__ __attribute__((aligned(16))) bf16_t u3s[];
+    bf16_t* dpl = u3s;                   // [3][128 m][128 k] errors, swizzled
+    bf16_t* xst = u3s + 3 * U3_DPLANE;   // [2 stages][3 planes][128 n][40] inputs
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 2, wn = wave & 3;
+    const int rl = lane & 15, kg = lane >> 4;
+    int bx, by, bz;
+    gemm_tile(bx, by, bz);
+    const int zz = bz;
+    int cn, valid;
+    int64_t r0;
+    gemm_zinfo(g, zz, cn, r0, valid);
+    const int Mv = g.M, Nv = g.N;
+    const int Kv = (g.sample_dims & 4) ? valid : g.Kd;   // samples of this step (<= 128)
+    const int m0 = by * 128;
+    if (m0 >= Mv || Kv <= 0) return;
+    const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
+    const int nkc = (Kv + B3_BK - 1) / B3_BK;          // k-chunks per tile
+    const int ntile = (Nv + 127) / 128;
+    const int nsteps = ntile * nkc;
+    const float scale = g.scale_per_batch ? g.lr / (float)Kv : g.lr;
+    float* Wz = (float*)g.c + (size_t)zz * g.c_z;
+
+    // the strip's targets through a buffer descriptor (rows past M and columns past N out of
+    // range: loads give zero, stores are dropped; no branch, exact wait counters).  N and the
+    // row stride are multiples of 4, so a valid float4 never crosses N.
+    B3Src wsrc;
+    {
+        wsrc.base = (uint64_t)(Wz + (size_t)m0 * g.c_ld);
+        wsrc.nbytes = (int)((int64_t)min(128, Mv - m0) * g.c_ld * 4);
+        wsrc.ld4 = (uint32_t)(g.c_ld * 4);
+    }
+    auto woff = [&](int n0, int i, int j) {
+        const int n = n0 + wn * 32 + j * 16 + kg * 4;
+        const uint32_t inv = (uint32_t)(Nv - 1 - n) >> 31;
+        return ((uint32_t)(wm * 64 + i * 16 + rl) * wsrc.ld4 + (uint32_t)n * 4u) | (inv << 31);
+    };
+    auto load_w = [&](float4 (&w)[4][2], int n0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                w[i][j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(wsrc), woff(n0, i, j), 0, 0));
+    };
+    float4 wcur[4][2], wnext[4][2];
+    load_w(wcur, 0);
+
+    // the input stream: step q = (tile q / nkc, k-chunk q % nkc); zeros past the last step
+    auto xsrc = [&](int q) {
+        const int n0 = min(q / nkc, ntile - 1) * 128;
+        return b3_src<false>(g.b, zz, cn, xbase, n0, Nv, Kv);
+    };
+    auto xload = [&](B3Raw& r, int q) {
+        const int kc = q % nkc;
+        b3_load<false>(r, xsrc(q), q < nsteps ? Nv - min(q / nkc, ntile - 1) * 128 : 0, kc * B3_BK, Kv, tid);
+    };
+    B3Raw ra, na;
+    xload(ra, 0);
+
+    // the strip's errors: 2 samples x 4 rows per thread and pass, split into the planes
+    {
+        const B3Src ds = b3_src<false>(g.a, zz, cn, xbase, m0, Mv, Kv);
+#pragma unroll
+        for (int pass = 0; pass < U3_KMAX * 128 / (8 * B3_THREADS); ++pass) {
+            const int kpair = (tid & 15) + 16 * (pass & 3), mq = (tid >> 4) * 4;  // samples 2 kpair, +1; rows mq ..
+            B3Raw v;
+            b3_load<false>(v, ds, Mv - m0, 2 * kpair - 2 * (tid & 15), Kv, tid);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float a0 = j == 0 ? v.v[0].x : j == 1 ? v.v[0].y : j == 2 ? v.v[0].z : v.v[0].w;
+                const float a1 = j == 0 ? v.v[1].x : j == 1 ? v.v[1].y : j == 2 ? v.v[1].z : v.v[1].w;
+                uint32_t h, m, l;
+                split3_pk(a0, a1, h, m, l);
+                const int o = u3_off(mq + j, 2 * kpair);
+                *(uint32_t*)(dpl + o) = h;
+                *(uint32_t*)(dpl + U3_DPLANE + o) = m;
+                *(uint32_t*)(dpl + 2 * U3_DPLANE + o) = l;
+            }
+        }
+    }
+    xload(na, 1);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) b3_store_part<false>(xst, ra, u, tid);
+    xload(ra, 2);
+    __syncthreads();
+    // the bias gradient (h + m + l is delta exactly)
+    if (g.ubias != nullptr && tid < 128) {
+        float sr = 0.f;
+        for (int k = 0; k < U3_KMAX; ++k) {
+            const int o = u3_off(tid, k);
+            sr += (bf2f(dpl[o]) + bf2f(dpl[U3_DPLANE + o])) + bf2f(dpl[2 * U3_DPLANE + o]);
+        }
+        if (m0 + tid < Mv) g.ubias[(size_t)cn * g.bias_z + m0 + tid] -= scale * sr;
+    }
+
+    f4 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    int buf = 0;
+    constexpr int PA[6] = {2, 0, 1, 1, 0, 0}, PB[6] = {0, 2, 1, 0, 1, 0};
+    // step q: chunk q's matrix instructions from stage buf, chunk q+1 (xa) split into the other
+    // stage, chunk q+3 loaded into ya
+    auto step = [&](int q, const B3Raw& xa, B3Raw& ya) {
+        xload(ya, q + 3);
+        const int kc = q % nkc;
+        const bf16_t* Bt = xst + buf * 3 * B3_PLANE;
+        bf16_t* Bn = xst + (buf ^ 1) * 3 * B3_PLANE;
+        if (kc == 0) {
+            // a new tile: its targets were loaded one tile ahead; the next tile's now
+            const int tn = q / nkc;
+            if (tn + 1 < ntile) load_w(wnext, (tn + 1) * 128);
+        }
+        bf8v av[3][4], bv[3][2];
+#pragma unroll
+        for (int p = 0; p < 3; ++p) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                av[p][i] = *(const bf8v*)(dpl + p * U3_DPLANE + u3_off(wm * 64 + i * 16 + rl, kc * B3_BK + kg * 8));
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                bv[p][j] = *(const bf8v*)(Bt + p * B3_PLANE + (wn * 32 + j * 16 + rl) * B3_LDK + kg * 8);
+        }
+#pragma unroll
+        for (int t = 0; t < 6; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[PB[t]][j], av[PA[t]][i], acc[i][j], 0, 0, 0);
+            if (t == 1 || t == 3) b3_store_part<false>(Bn, xa, t >> 1, tid);
+        }
+        if (kc == nkc - 1) {
+            // the tile is complete: W -= scale * acc
+            const int n0 = (q / nkc) * 128;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const f4 v = acc[i][j];
+                    float4 w = wcur[i][j];
+                    w.x -= scale * v[0]; w.y -= scale * v[1]; w.z -= scale * v[2]; w.w -= scale * v[3];
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), b3_rsrc(wsrc), woff(n0, i, j), 0, 0);
+                    acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+                    wcur[i][j] = wnext[i][j];
+                }
+        }
+        __syncthreads();
+        buf ^= 1;
+    };
+    // three input register sets in rotation: chunk q+1 (split now), q+2, q+3 (in flight)
+    B3Raw rc;
+    for (int q = 0; q < nsteps; q += 3) {
+        step(q, na, rc);
+        if (q + 1 >= nsteps) break;
+        step(q + 1, ra, na);
+        if (q + 2 >= nsteps) break;
+        step(q + 2, rc, ra);
+    }
+}
+
+// ------------------------------------------------------------------------------------
 // Output layer, one wavefront per sample row: z = W x + b over <= 16 outputs, the output
 // activation (eq. (3), softmax eq. (5)), then either the output error (training, eq. (9)
 // or (10)) or the predicted class and the correct count (inference).

@@ -119,6 +119,9 @@ struct pnn_net {
     unsigned long long* zpart = nullptr;  // [2][K][nrb][32][16] tagged output-sum shares
     size_t zpart_elems = 0;
     unsigned mbp_tag = 1;                 // tag of the next launch's first batch step
+    // fp32 products of the large GEMMs on the bf16 matrix cores (three-part split); false:
+    // fp32 matrix instructions throughout (PNN_GEMM=fp32, read by pnn_init)
+    bool gemm_x3 = true;
     // bounded waits of the persistent kernels: polls before giving up; and a test hook that
     // makes their waits run into that bound (the mini-batch kernel's readers wait for share
     // tags that are never written, the per-sample kernel's for more tiles than exist)
@@ -310,11 +313,38 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
     if (grid.x == 0 || grid.y == 0 || grid.z == 0 || grid.y > 65535 || grid.z > 65535)
         return fail(n, PNN_EINVAL, "%s: bad grid %u x %u x %u", name, grid.x, grid.y, grid.z);
     if constexpr (!BF) {
-        // large fp32 shapes with both operands along k (forward, inference): 128 x 128 tiles.
-        // (The weight update, short contraction and a read-modify-write epilogue, keeps the
-        // 64 x 64 tiles: more workgroups in flight to cover its epilogue.)
+        const dim3 g128((g.N + 127) / 128, (g.M + 127) / 128, (unsigned)(Z * g.ksplit));
+        // the weight update over at most 128 samples of a layer of >= 128 neurons: strips of 128
+        // rows of W on the bf16 matrix cores (upd128x3_kernel)
+        if constexpr (EPI == EPI_UPD && !A_KC && !B_KC) {
+            const int kmax = (g.sample_dims & 4) ? g.step_rows : g.Kd;
+            if (n->gemm_x3 && g.M >= 128 && g.N >= 128 && kmax <= U3_KMAX && g.ksplit == 1 && g.shadow == nullptr &&
+                g.N % 4 == 0 && g.c_ld % 4 == 0) {
+                static const hipError_t attr = hipFuncSetAttribute((const void*)upd128x3_kernel,
+                                                                   hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                                   (int)u3_lds_bytes());
+                if (attr != hipSuccess) return fail(n, PNN_EHIP, "%s: hipFuncSetAttribute: %s", name, hipGetErrorString(attr));
+                Launch l(n, s, name);
+                upd128x3_kernel<<<dim3(1, (g.M + 127) / 128, (unsigned)Z), B3_THREADS, u3_lds_bytes(), s>>>(g);
+                return l.done();
+            }
+        }
+        // large fp32 shapes: 128 x 128 tiles on the bf16 matrix cores, each fp32 operand split
+        // into three bf16 parts (gemm128x3_kernel)
+        if (n->gemm_x3 && g.M >= 128 && g.N >= 128 && g.shadow == nullptr && (g.ksplit == 1 || g.kchunk % B3_BK == 0)) {
+            static const hipError_t attr = hipFuncSetAttribute((const void*)gemm128x3_kernel<A_KC, B_KC, EPI>,
+                                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                               (int)b3_lds_bytes());
+            if (attr != hipSuccess) return fail(n, PNN_EHIP, "%s: hipFuncSetAttribute: %s", name, hipGetErrorString(attr));
+            Launch l(n, s, name);
+            gemm128x3_kernel<A_KC, B_KC, EPI><<<g128, B3_THREADS, b3_lds_bytes(), s>>>(g);
+            return l.done();
+        }
+        // otherwise, with both operands along k (forward, inference): 128 x 128 tiles on the
+        // fp32 matrix instructions.  (The weight update, short contraction and a
+        // read-modify-write epilogue, keeps the 64 x 64 tiles: more workgroups in flight to
+        // cover its epilogue.)
         if (A_KC && B_KC && g.M >= 128 && g.N >= 128 && g.shadow == nullptr) {
-            dim3 g128((g.N + 127) / 128, (g.M + 127) / 128, (unsigned)(Z * g.ksplit));
             Launch l(n, s, name);
             gemm128_kernel<A_KC, B_KC, EPI><<<g128, 256, 0, s>>>(g);
             return l.done();
@@ -847,6 +877,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
     }
     // failure-handling tests: PNN_SPIN_LIMIT bounds the persistent kernels' waits (polls);
     // PNN_TEST_STALL_WAITS=1 makes the persistent kernels' waits run into that bound
+    if (const char* e = getenv("PNN_GEMM")) n->gemm_x3 = strcmp(e, "fp32") != 0;
     n->spin_limit = SPIN_LIMIT;
     if (const char* e = getenv("PNN_SPIN_LIMIT")) {
         const long v = strtol(e, nullptr, 10);
