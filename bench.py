@@ -43,6 +43,9 @@ import pnn_inputs as I  # noqa: E402
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 (vector with packed FMA, and matrix)
 BF16_PEAK_TFLOPS = 2500.0      # MI355X bf16 dense matrix
+# fp32 products on the bf16 matrix cores (kernels named *_x3): six bf16 part products per fp32
+# product, so their compute roof is the bf16 peak over six, in fp32 flops
+X3_PEAK_TFLOPS = BF16_PEAK_TFLOPS / 6.0
 
 
 def method_flops_per_sample(w) -> float:
@@ -83,6 +86,8 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
                                  rows (2 H a + 4)
     merge: reads K*P floats and writes P (and K*P with broadcast).
     """
+    if name.endswith("_x3"):
+        name = name[:-3]
     s = w.sizes
     K = w.replicas
     L = len(s) - 1
@@ -225,8 +230,9 @@ def schedule_position(w, N, ms, prof):
         by += wk[1] * n_l
     s = ms / 1e3
     mpeak = BF16_PEAK_TFLOPS if w.precision == I.BF16_MIXED else FP32_PEAK_TFLOPS
-    return {"flops": fl, "bytes": by, "tflops": round(fl / s / 1e12, 3), "mfma_frac": round(fl / s / 1e12 / mpeak, 4),
-            "gbs": round(by / s / 1e9, 1), "hbm_frac": round(by / s / 1e9 / HBM_PEAK_GBS, 4)}
+    return {"flops": fl, "bytes": by, "tflops": round(fl / s / 1e12, 3), "mfma_peak_tflops": mpeak,
+            "mfma_frac": round(fl / s / 1e12 / mpeak, 4), "gbs": round(by / s / 1e9, 1),
+            "hbm_frac": round(by / s / 1e9 / HBM_PEAK_GBS, 4)}
 
 
 def main():
@@ -338,8 +344,11 @@ def main():
         if wk is not None:
             flops, byts = wk
             # the bound is the roof the kernel's arithmetic intensity reaches first: the matrix
-            # peak of its operand type against HBM (ridge 19.7 flop/B in fp32, 312 in bf16)
+            # peak of its operand type against HBM (ridge 19.7 flop/B in fp32, 312 in bf16,
+            # 52 for fp32 products on the bf16 matrix cores)
             mpeak = BF16_PEAK_TFLOPS if w.precision == I.BF16_MIXED else FP32_PEAK_TFLOPS
+            if dom.endswith("_x3"):
+                mpeak = X3_PEAK_TFLOPS
             ridge = mpeak * 1e12 / (HBM_PEAK_GBS * 1e9)
             if dom == "psgd_persistent" or flops < ridge * byts:
                 bound, ach, peak, unit = "hbm", byts / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"

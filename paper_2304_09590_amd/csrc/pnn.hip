@@ -295,6 +295,17 @@ GemmArgs gemm_base(const pnn_net* n, int M, int N, int Kd, int64_t n_total, int6
     return g;
 }
 
+// profiling name of a launch on the split-bf16 path ("<name>_x3")
+const char* x3_name(const char* name) {
+    static const char* const names[][2] = {{"fwd_gemm", "fwd_gemm_x3"}, {"upd_gemm", "upd_gemm_x3"},
+                                           {"bwd_gemm", "bwd_gemm_x3"}, {"infer_fwd_gemm", "infer_fwd_gemm_x3"},
+                                           {"psgd_upd", "psgd_upd_x3"},  {"psgd_p", "psgd_p_x3"},
+                                           {"psgd_gram", "psgd_gram_x3"}};
+    for (const auto& e : names)
+        if (strcmp(e[0], name) == 0) return e[1];
+    return name;
+}
+
 template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO>
 pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const char* name) {
     // shapes the kernel assumes: 16-byte loads along contiguous dimensions
@@ -324,7 +335,7 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
                                                                    hipFuncAttributeMaxDynamicSharedMemorySize,
                                                                    (int)u3_lds_bytes());
                 if (attr != hipSuccess) return fail(n, PNN_EHIP, "%s: hipFuncSetAttribute: %s", name, hipGetErrorString(attr));
-                Launch l(n, s, name);
+                Launch l(n, s, x3_name(name));
                 upd128x3_kernel<<<dim3(1, (g.M + 127) / 128, (unsigned)Z), B3_THREADS, u3_lds_bytes(), s>>>(g);
                 return l.done();
             }
@@ -336,7 +347,7 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
                                                                hipFuncAttributeMaxDynamicSharedMemorySize,
                                                                (int)b3_lds_bytes());
             if (attr != hipSuccess) return fail(n, PNN_EHIP, "%s: hipFuncSetAttribute: %s", name, hipGetErrorString(attr));
-            Launch l(n, s, name);
+            Launch l(n, s, x3_name(name));
             gemm128x3_kernel<A_KC, B_KC, EPI><<<g128, B3_THREADS, b3_lds_bytes(), s>>>(g);
             return l.done();
         }
