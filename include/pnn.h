@@ -200,13 +200,14 @@ int32_t pnn_profile_read(pnn_net* net, const char** names, double* total_ms, int
 /* Name of the training plan that pnn_init chose for the handle (a static string; "" for
  * a NULL handle).  All plans compute the update of pnn_train_epoch and differ only in the
  * order of fp32 roundings:
- *  "per-sample persistent"  B = 1, one hidden layer of <= 128 neurons, every CN's
- *                           workgroups co-resident on the device: one launch per epoch;
+ *  "per-sample persistent"  B = 1, one hidden layer of <= 128 neurons, sizes[0] <= 832: one
+ *                           launch per epoch for each group of CNs whose workgroups fit the
+ *                           device at once (all K CNs in one group where they fit);
  *  "per-sample chunked"     B = 1 otherwise;
  *  "mini-batch persistent"  fp32, one hidden layer, 2 <= B <= 32, <= 16 outputs,
- *                           sizes[0] % 16 == 0 and <= 832, H <= 512, every CN's
- *                           ceil(H / 16) (else ceil(H / 32)) tile workgroups co-resident:
- *                           one launch per epoch;
+ *                           sizes[0] % 16 == 0 and <= 832, H <= 512: one launch per epoch for
+ *                           each group of CNs whose ceil(H / 16) (or ceil(H / 32)) tile
+ *                           workgroups fit the device at once;
  *  "mini-batch"             kernel launches per layer and batch step.
  * The environment variable PNN_MB_PLAN=launch, read by pnn_init, selects "mini-batch"
  * where "mini-batch persistent" would apply.  The persistent plans' workgroups wait for each

@@ -2043,12 +2043,14 @@ __device__ inline void signal_set(int* flag, int v) {
 // first-layer errors only up to chunk c-2, and is computed while chunk c-1 runs.
 //
 // Grid (cooperative, all workgroups co-resident, 256 threads each):
-//   blockIdx < K: the sequential workgroup of CN k.  Waves 0..HW/64-1 own one hidden
+// (One launch trains CNs cn0 .. cn0 + KL - 1; where all K CNs' workgroups do not fit the CUs
+// at once, the CNs go in groups, one launch each.)
+//   blockIdx < KL: the sequential workgroup of CN cn0 + blockIdx.  Waves 0..HW/64-1 own one hidden
 //     neuron per lane (W2 column and b1 in registers); the other "helper" waves compute,
 //     one step ahead, the already-known part (s <= t-2) of the next step's in-chunk
 //     correction.  At chunk start all four waves compute the previous-chunk correction on
 //     the matrix cores.
-//   blockIdx >= K: tile workgroups.  Tile (k, rb) keeps W1[16 rows][all inputs] of CN k in
+//   blockIdx >= KL: tile workgroups.  Tile (k, rb) keeps W1[16 rows][all inputs] of CN k in
 //     registers for the epoch, laid out as the B operand of v_mfma_f32_16x16x4_f32 (lane l:
 //     row 16 rb + l % 16, inputs 16 ib + 4 (l / 16) + q).  It publishes Q_0 and Q_1, then for
 //     each later chunk waits for the previous chunk's errors, applies
@@ -2071,6 +2073,7 @@ struct PsgdPArgs {
     float* d1;           // [2][K][H][T]  by chunk parity (transposed: one row per hidden neuron)
     int* flags;          // qready[K], dready[K], abort (sticky: cleared only at allocation)
     int H, O, In, act1, act2, loss, nrb;
+    int cn0, k_launch;   // this launch trains CNs cn0 .. cn0 + k_launch - 1 (all K share the flags)
     int wait_skew;       // 0; a large value makes the first wait of every sequential workgroup
                          // wait for more tile signals than ever come (failure-handling test:
                          // the bound is reached)
@@ -3017,13 +3020,13 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
 template <int T, int NH, int A1, int A2, int LS, int OC, int RT>
 __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
     extern __shared__ float smem[];
-    const int b = blockIdx.x, K = a.k_rep;
+    const int b = blockIdx.x, K = a.k_rep, KL = a.k_launch;
     // an earlier launch gave up waiting: the parameters are unspecified, train no further
     if (__hip_atomic_load(a.flags + 2 * K, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
-    if (b < K) psgd_rec<T, NH, A1, A2, LS, OC>(a, b, smem);
+    if (b < KL) psgd_rec<T, NH, A1, A2, LS, OC>(a, a.cn0 + b, smem);
     else {
-        const int j = b - K;
-        psgd_tile<T, RT>(a, j / a.nrb, j % a.nrb, smem);
+        const int j = b - KL;
+        psgd_tile<T, RT>(a, a.cn0 + j / a.nrb, j % a.nrb, smem);
     }
 }
 
@@ -3063,6 +3066,7 @@ struct MbpArgs {
     unsigned long long* zpart;  // [2][K][nrb][MBP_TB][16] tagged output-sum shares
     int* flags;                 // [K + 1]; flags[K]: abort (sticky: cleared only at allocation)
     int k_rep, H, O, In, act1, act2, loss, nrb, B;
+    int cn0;                    // this launch trains CNs cn0 .. cn0 + gridDim.x / nrb - 1
     int xcd_map;                // 1: the tiles of a CN run on one XCD (grid a multiple of 8)
     unsigned tag0;              // tag of step 0 (>= 1)
     unsigned tag_skew;          // 0; > 0 makes the readers wait for tags never written (abort test)
@@ -3093,7 +3097,7 @@ __global__ __launch_bounds__(256) void mbp_kernel(MbpArgs a) {
     // consecutive tiles, so that a CN's tiles share one L2
     int lin = blockIdx.x;
     if (a.xcd_map) lin = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
-    const int k = lin / nrb, rb = lin - k * nrb;
+    const int k = a.cn0 + lin / nrb, rb = lin % nrb;
     const int hb = rb * NR;
     const int nib = (In + 15) / 16;
     float* xsm = smem;                       // [64 MAX_IB][XT] the batch's rows transposed: [input][row]

@@ -106,6 +106,7 @@ struct pnn_net {
     bool persistent = false;
     bool pspecial = false;   // sigmoid / sigmoid / quadratic loss / 10 outputs
     int nrb = 0;             // tile workgroups per CN
+    int kgroup = 0;          // CNs per launch of a persistent plan (all K, or groups that fit the CUs)
     int prt = 1;             // 16-row sub-tiles per tile workgroup
     int* flags = nullptr;    // qready[K], dready[K], abort
     float* qbuf = nullptr;   // [2][K][T][H]
@@ -607,16 +608,24 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
     a.lr = n->cfg.lr;
     a.spin_limit = n->spin_limit;
     void* params[] = {&a};
-    const dim3 grid((unsigned)(K * (1 + n->nrb)));
-    Launch l(n, s, "psgd_persistent");
     const void* fn = persistent_fn(n);
-    hipError_t e = hipLaunchCooperativeKernel(fn, grid, dim3(256), params, (unsigned)n->psmem, s);
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        n->broken = true;
-        return fail(n, PNN_EHIP, "cooperative launch of the per-sample kernel failed: %s", hipGetErrorString(e));
+    // the CNs in groups of at most kgroup (balanced), one launch each
+    const int G = (K + n->kgroup - 1) / n->kgroup;
+    for (int gi = 0, c0 = 0; gi < G; ++gi) {
+        const int kl = (K - c0) / (G - gi);
+        a.cn0 = c0;
+        a.k_launch = kl;
+        const dim3 grid((unsigned)(kl * (1 + n->nrb)));
+        Launch l(n, s, "psgd_persistent");
+        hipError_t e = hipLaunchCooperativeKernel(fn, grid, dim3(256), params, (unsigned)n->psmem, s);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            n->broken = true;
+            return fail(n, PNN_EHIP, "cooperative launch of the per-sample kernel failed: %s", hipGetErrorString(e));
+        }
+        TRY(l.done());
+        c0 += kl;
     }
-    TRY(l.done());
     return note_persistent_launch(n, s);
 }
 
@@ -651,23 +660,31 @@ pnn_status mbp_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hi
     a.k_rep = K; a.H = n->sizes[1]; a.O = n->sizes[2]; a.In = n->sizes[0];
     a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
     a.nrb = n->nrb; a.B = n->cfg.batch;
-    const int grid = K * n->nrb;
-    a.xcd_map = grid % 8 == 0;
     a.tag0 = n->mbp_tag;
     a.tag_skew = n->tag_skew;
     n->mbp_tag += (unsigned)nsteps;
     a.lr = n->cfg.lr;
     a.spin_limit = n->spin_limit;
     void* params[] = {&a};
-    Launch l(n, s, "mb_persistent");
-    hipError_t e = hipLaunchCooperativeKernel(mbp_fn(n->mrt), dim3((unsigned)grid), dim3(256), params,
-                                              (unsigned)n->psmem, s);
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        n->broken = true;
-        return fail(n, PNN_EHIP, "cooperative launch of the mini-batch kernel failed: %s", hipGetErrorString(e));
+    // the CNs in groups of at most kgroup (balanced), one launch each (every CN has its own
+    // share slots, so the groups' launches share the step tags)
+    const int G = (K + n->kgroup - 1) / n->kgroup;
+    for (int gi = 0, c0 = 0; gi < G; ++gi) {
+        const int kl = (K - c0) / (G - gi);
+        const int grid = kl * n->nrb;
+        a.cn0 = c0;
+        a.xcd_map = grid % 8 == 0;
+        Launch l(n, s, "mb_persistent");
+        hipError_t e = hipLaunchCooperativeKernel(mbp_fn(n->mrt), dim3((unsigned)grid), dim3(256), params,
+                                                  (unsigned)n->psmem, s);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            n->broken = true;
+            return fail(n, PNN_EHIP, "cooperative launch of the mini-batch kernel failed: %s", hipGetErrorString(e));
+        }
+        TRY(l.done());
+        c0 += kl;
     }
-    TRY(l.done());
     return note_persistent_launch(n, s);
 }
 
@@ -918,8 +935,20 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, n->device) != hipSuccess) cus = 0;
         const int H = n->sizes[1], In = n->sizes[0], O = n->sizes[2];
         const int HW = live_width(H);
-        // tile workgroups of 16 rows of W1 each, or of 32 when the 16-row tiles do not fit
-        const int rt = (int64_t)K * (1 + (H + 15) / 16) <= cus ? 1 : 2;
+        // tile workgroups of 16 rows of W1 (rt = 1) or 32 (rt = 2); the CNs go in groups whose
+        // workgroups fit the CUs, one launch each.  Of the two, the one with the least estimated
+        // time: launches x the relative time of a step (1 with 16-row tiles, 1.8 with 32-row
+        // tiles, whose tiles do twice the work per chunk; 1.5 to 1.9 measured with 784-128-10
+        // nets, growing with the CNs in flight)
+        int rt = 1, kg = 0;
+        double best = 1e30;
+        for (int r = 1; r <= 2; ++r) {
+            const int nb = (H + 16 * r - 1) / (16 * r);
+            const int g = std::min(K, cus / (1 + nb));
+            if (g < 1) continue;
+            const double cost = (double)((K + g - 1) / g) * (r == 1 ? 1.0 : 1.8);
+            if (cost < best) { best = cost; rt = r; kg = g; }
+        }
         const int nrb = (H + 16 * rt - 1) / (16 * rt);
         n->prt = rt;
         // input sums [HW][T+4], errors [HW][T+4], Gram blocks 3 x [T][T+4], window
@@ -931,15 +960,16 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
         n->pspecial = n->act[0] == PNN_SIGMOID && n->act[1] == PNN_SIGMOID && cfg->loss == PNN_LOSS_MSE && O == 10;
         const void* fn = persistent_fn(n);
         int per_cu = 0;
-        bool fits = H <= 128 && In <= 4 * MAX_IB * 16 && (int64_t)K * (1 + nrb) <= cus;
+        bool fits = H <= 128 && In <= 4 * MAX_IB * 16 && kg >= 1;
         if (fits && hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)n->psmem) != hipSuccess)
             fits = false;
         if (fits && hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, n->psmem) != hipSuccess) fits = false;
-        if (fits && (int64_t)per_cu * cus < (int64_t)K * (1 + nrb)) fits = false;
+        if (fits && (int64_t)per_cu * cus < (int64_t)kg * (1 + nrb)) fits = false;
         (void)hipGetLastError();
         if (fits) {
             n->persistent = true;
             n->nrb = nrb;
+            n->kgroup = kg;
             const size_t qn = (size_t)2 * K * HW * (PT + 4);
             if ((st = dev_alloc(n, &n->qbuf, qn)) != PNN_OK) return bail(st);
             // padding neurons and rows of the input sums are never written by the kernel: zero them
@@ -996,9 +1026,20 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
             int cus = 0;
             if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, n->device) != hipSuccess) cus = 0;
             const int H = n->sizes[1];
-            int rt = 0;
-            if ((H + 15) / 16 <= MBP_NRB && (int64_t)K * ((H + 15) / 16) <= cus) rt = 1;
-            else if ((H + 31) / 32 <= MBP_NRB && (int64_t)K * ((H + 31) / 32) <= cus) rt = 2;
+            // tile workgroups of 16 neurons (rt = 1) or 32 (rt = 2); the CNs in groups whose tiles
+            // fit the CUs, one launch each; the one with the least estimated time (launches x the
+            // relative time of a batch step: 1 with 16-neuron tiles, 1.45 with 32, as measured
+            // with 784-256-10 nets)
+            int rt = 0, kg = 0;
+            double best = 1e30;
+            for (int r = 1; r <= 2; ++r) {
+                const int nb = (H + 16 * r - 1) / (16 * r);
+                if (nb > MBP_NRB) continue;
+                const int g = std::min(K, cus / nb);
+                if (g < 1) continue;
+                const double cost = (double)((K + g - 1) / g) * (r == 1 ? 1.0 : 1.45);
+                if (cost < best) { best = cost; rt = r; kg = g; }
+            }
             if (rt > 0) {
                 const int nrb = (H + 16 * rt - 1) / (16 * rt);
                 const size_t smem = (size_t)mbp_lds_floats(rt) * sizeof(float);
@@ -1006,12 +1047,13 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
                 int per_cu = 0;
                 bool fits = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem) == hipSuccess;
                 if (fits && hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, smem) != hipSuccess) fits = false;
-                if (fits && (int64_t)per_cu * cus < (int64_t)K * nrb) fits = false;
+                if (fits && (int64_t)per_cu * cus < (int64_t)kg * nrb) fits = false;
                 (void)hipGetLastError();
                 if (fits) {
                     n->mbp = true;
                     n->mrt = rt;
                     n->nrb = nrb;
+                    n->kgroup = kg;
                     n->psmem = smem;
                     n->zpart_elems = (size_t)2 * K * nrb * MBP_TB * 16;
                     // (zeroed: a share is valid only with its step's tag, which is >= 1)

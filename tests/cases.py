@@ -30,12 +30,20 @@ EPOCH_CASES = [
     # per-sample with more CNs than 16-row tile workgroups fit: 32-row tiles
     (1, dict(replicas=32), 32 * 70 + 5, 1),
     (1, dict(sizes=(784, 64, 10), replicas=60), 60 * 40 + 7, 1),
+    # per-sample with more CNs than fit the device at once: 64 CNs of 16-row tiles in 3
+    # launches of 21/21/22; 96 CNs of 32-row tiles in 2 launches of 48
+    (1, dict(replicas=64), 64 * 40 + 5, 1),
+    (1, dict(replicas=96), 96 * 30 + 5, 1),
     # persistent mini-batch plan: a hidden width that leaves the last 16-neuron tile half
     # empty, batches of 7 and a grid that is no multiple of 8; 32-neuron tiles (20 CNs of 256
     # neurons); batches of 2 with ReLU / softmax
     (2, dict(sizes=(784, 56, 10), acts=(I.SIGMOID, I.SIGMOID), batch=7, replicas=5), 5 * 40 + 3, 2),
     (2, dict(replicas=20), 20 * 40 + 3, 1),
     (2, dict(acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=2, replicas=3), 3 * 30 + 2, 1),
+    # persistent mini-batch plan in CN groups (32-neuron tiles): 80 CNs in 3 launches of
+    # 26/27/27; 64 CNs in 2 launches of 32, merge + broadcast each epoch
+    (2, dict(replicas=80), 80 * 40 + 3, 1),
+    (2, dict(replicas=64, merge_every_epoch=True), 64 * 40 + 3, 2),
 ]
 
 # fp32 epoch cases where the method amplifies rounding differences to the size of the epoch bar
@@ -54,7 +62,7 @@ SENSITIVE_FP32_CASES = [
 CHUNKED_CASES = [
     # overrides of the 784-128-10 per-sample workload, N; chunk length T = 64 / 128 / 16 / 32
     (dict(sizes=(784, 256, 10), replicas=2), 2 * 300 + 1),             # 4 full chunks + 44/45
-    (dict(replicas=64), 64 * 200 + 5),                                 # 64 CNs: 1 chunk + 72/73
+    (dict(sizes=(784, 160, 10), replicas=48), 48 * 200 + 5),           # 48 CNs: 1 chunk + 72/73
     (dict(sizes=(784, 1024, 10), replicas=2), 2 * 50 + 1),             # 3 chunks + 2/3
     (dict(sizes=(784, 384, 10), acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, replicas=3), 3 * 90 + 2),
 ]

@@ -202,10 +202,12 @@ def test_chunked_plan_epoch(over, N):
 PLAN_CASES = [
     # workload, overrides, plan chosen at init
     (1, {}, "per-sample persistent"),
+    (1, dict(replicas=64), "per-sample persistent"),          # 3 launches of 21/21/22 CNs
     (1, dict(sizes=(784, 256, 10)), "per-sample chunked"),
     (2, {}, "mini-batch persistent"),                          # 16 CNs x 16 tiles of 16 neurons
     (2, dict(replicas=20), "mini-batch persistent"),          # 32-neuron tiles
-    (2, dict(replicas=40), "mini-batch"),                     # 40 x 8 tiles do not fit
+    (2, dict(replicas=40), "mini-batch persistent"),          # 2 launches of 20 CNs
+    (2, dict(sizes=(784, 1024, 10)), "mini-batch"),           # 64 tiles of 16 neurons per CN
     (2, dict(batch=33), "mini-batch"),
     (3, dict(replicas=8), "mini-batch"),                      # bf16, two hidden layers
     (4, dict(replicas=4), "mini-batch"),
