@@ -747,8 +747,7 @@ __global__ __launch_bounds__(256) void gemm128_kernel(GemmArgs g) {
 // small terms go first).
 //
 // Eight waves of 64 x 32 (4 x 2 blocks of 16 x 16), two per SIMD, one workgroup per CU (120 KiB
-// of dynamic LDS: two stages of both operands' three bf16 planes [t][k], row stride 40, which
-// the 16-byte fragment reads cover without bank conflicts).  The fp32 operands are loaded two
+// of dynamic LDS: two stages of both operands' three bf16 planes [t][k], laid out by b3_off).  The fp32 operands are loaded two
 // k-tiles ahead into registers through bounds-checked buffer loads; while the matrix
 // instructions of k-tile k run, the wave splits k-tile k+1 (v_cvt_pk_bf16_f32, round to nearest
 // even) into the other stage.  KC operands (rows = t) load a float4 of 4 k per thread and row;
@@ -783,12 +782,19 @@ __device__ inline void split3_pk(float x, float y, uint32_t& h, uint32_t& m, uin
 // k 4 (tid & 7) .. + 3; NC v[e] = k 2 (tid & 15) + e, columns 4 (tid >> 4) .. + 3
 struct B3Raw { float4 v[2]; };
 
-// KC rows: a wave's part u covers rows {0, 4, 8, 12} (lanes 0-31) and {1, 5, 9, 13} (lanes
-// 32-63) of a 16-row block (or those + 2), so that the 64-byte pieces its lanes store fall on
-// disjoint LDS banks at the 80-byte row stride
-__device__ inline int kc_row(int tid, int u) {
-    const int L = tid & 63, b = 2 * (tid >> 6) + u;  // b: 16 blocks of 8 rows
-    return 16 * (b >> 1) + 2 * (b & 1) + 4 * ((L >> 3) & 3) + (L >> 5);
+// KC rows: eight threads per row (128 contiguous bytes of the operand), a wave's part u eight
+// consecutive rows
+__device__ inline int kc_row(int tid, int u) { return (tid >> 3) + 64 * u; }
+
+// element offset of (row t, k) in a plane.  KC operands (stored by rows): rows of 32 k (64
+// bytes), the four 16-byte chunks of a row permuted by XOR with bits 1-2 of the row; NC
+// operands (stored by columns, 4 bytes at a time): rows of 40 (80 bytes).  Neither the stores
+// nor the 16-byte fragment reads of a KC plane meet bank conflicts; an NC plane's stores meet
+// none, its fragment reads some (both measured with the LDS bank-conflict counter).
+template <bool KC>
+__device__ inline int b3_off(int t, int k) {
+    if (KC) return t * B3_BK + ((((k >> 3) ^ ((t >> 1) & 3))) << 3) + (k & 7);
+    return t * B3_LDK + k;
 }
 
 // Branch-free loads through a buffer descriptor: an element outside the tile's valid rows lies
@@ -847,7 +853,7 @@ __device__ inline void b3_store_part(bf16_t* lds, const B3Raw& r, int u, int tid
         uint32_t h0, m0, l0, h1, m1, l1;
         split3_pk(r.v[u].x, r.v[u].y, h0, m0, l0);
         split3_pk(r.v[u].z, r.v[u].w, h1, m1, l1);
-        bf16_t* d = lds + t * B3_LDK + k;
+        bf16_t* d = lds + b3_off<true>(t, k);
         *(uint2*)d = make_uint2(h0, h1);
         *(uint2*)(d + B3_PLANE) = make_uint2(m0, m1);
         *(uint2*)(d + 2 * B3_PLANE) = make_uint2(l0, l1);
@@ -857,11 +863,11 @@ __device__ inline void b3_store_part(bf16_t* lds, const B3Raw& r, int u, int tid
         const float a0 = u ? r.v[0].z : r.v[0].x, a1 = u ? r.v[0].w : r.v[0].y;
         const float c0 = u ? r.v[1].z : r.v[1].x, c1 = u ? r.v[1].w : r.v[1].y;
         uint32_t h, m, l;
-        bf16_t* d = lds + t * B3_LDK + k;
+        bf16_t* d = lds + b3_off<false>(t, k);
         split3_pk(a0, c0, h, m, l);
         *(uint32_t*)d = h; *(uint32_t*)(d + B3_PLANE) = m; *(uint32_t*)(d + 2 * B3_PLANE) = l;
         split3_pk(a1, c1, h, m, l);
-        d += B3_LDK;
+        d = lds + b3_off<false>(t + 1, k);
         *(uint32_t*)d = h; *(uint32_t*)(d + B3_PLANE) = m; *(uint32_t*)(d + 2 * B3_PLANE) = l;
     }
 }
@@ -955,7 +961,7 @@ __global__ __launch_bounds__(B3_THREADS) void gemm128x3_kernel(GemmArgs g) {
             float sr = 0.f;
 #pragma unroll
             for (int k = 0; k < B3_BK; ++k) {
-                const int o = tid * B3_LDK + k;
+                const int o = b3_off<A_KC>(tid, k);
                 sr += (bf2f(A[o]) + bf2f(A[o + B3_PLANE])) + bf2f(A[o + 2 * B3_PLANE]);
             }
             rowsum[tid] += sr;
@@ -965,10 +971,10 @@ __global__ __launch_bounds__(B3_THREADS) void gemm128x3_kernel(GemmArgs g) {
         for (int p = 0; p < 3; ++p) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                av[p][i] = *(const bf8v*)(A + p * B3_PLANE + (wm * 64 + i * 16 + rl) * B3_LDK + kg * 8);
+                av[p][i] = *(const bf8v*)(A + p * B3_PLANE + b3_off<A_KC>(wm * 64 + i * 16 + rl, kg * 8));
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                bv[p][j] = *(const bf8v*)(Bt + p * B3_PLANE + (wn * 32 + j * 16 + rl) * B3_LDK + kg * 8);
+                bv[p][j] = *(const bf8v*)(Bt + p * B3_PLANE + b3_off<B_KC>(wn * 32 + j * 16 + rl, kg * 8));
         }
         // six groups of 8 matrix instructions, small terms first: (a part, b part) = lh, hl, mm,
         // mh, hm, hh; the next k-tile's split and store in between
@@ -1193,7 +1199,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                 av[p][i] = *(const bf8v*)(dpl + p * U3_DPLANE + u3_off(wm * 64 + i * 16 + rl, kc * B3_BK + kg * 8));
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                bv[p][j] = *(const bf8v*)(Bt + p * B3_PLANE + (wn * 32 + j * 16 + rl) * B3_LDK + kg * 8);
+                bv[p][j] = *(const bf8v*)(Bt + p * B3_PLANE + b3_off<false>(wn * 32 + j * 16 + rl, kg * 8));
         }
 #pragma unroll
         for (int t = 0; t < 6; ++t) {
