@@ -40,6 +40,13 @@ __device__ inline bf16_t f2bf(float f) {
 }
 __device__ inline float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+// two floats to packed bf16 (one v_cvt_pk_bf16_f32, round to nearest even), x in the low half
+__device__ inline uint32_t cvt_pk_bf16(float x, float y) {
+    const bf2v p = {(__bf16)x, (__bf16)y};
+    return __builtin_bit_cast(uint32_t, p);
+}
+
 template <typename T> __device__ inline float to_f(T v);
 template <> __device__ inline float to_f<float>(float v) { return v; }
 template <> __device__ inline float to_f<bf16_t>(bf16_t v) { return bf2f(v); }
@@ -189,6 +196,39 @@ __device__ inline const char* operand_row(const Operand& o, int elem, int z, int
     return p + (size_t)(z * o.zstride + r * o.ld) * elem;
 }
 
+// Branch-free loads through a buffer descriptor: an element outside the tile's valid rows lies
+// past the descriptor's range, one past the valid contraction gets an offset beyond it, and both
+// read as zero, so the wait counters stay exact across the pipeline.  KC: the descriptor starts
+// at the tile's first row (t0) and spans its valid rows; NC: it starts at the tile's first
+// column (t0) of contraction row 0 and ends with the last valid contraction row.
+struct B3Src {
+    uint64_t base;  // first byte (the same in every lane)
+    int nbytes;     // bytes in range
+    uint32_t ld4;   // row stride in bytes
+};
+
+template <bool KC, int ES = 4>
+__device__ inline B3Src b3_src(const Operand& o, int z, int cn, int64_t xbase, int t0, int t_valid, int k_valid) {
+    B3Src r;
+    r.ld4 = (uint32_t)(o.ld * ES);
+    const int rows = KC ? t_valid - t0 : k_valid;
+    const char* base = KC ? operand_row(o, ES, z, cn, xbase, t0) : operand_row(o, ES, z, cn, xbase, 0) + (size_t)t0 * ES;
+    int64_t bytes = (int64_t)rows * o.ld * ES - (KC ? 0 : (int64_t)t0 * ES);
+    if (rows <= 0 || bytes < 0) bytes = 0;
+    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
+    r.base = (uint64_t)base;
+    r.nbytes = (int)bytes;
+    return r;
+}
+
+// the descriptor, built where it is used from values made scalar explicitly (they are the same
+// in every lane; otherwise every buffer load would loop over the lanes' descriptors)
+__device__ inline __amdgpu_buffer_rsrc_t b3_rsrc(const B3Src& src) {
+    const uint64_t a = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(src.base >> 32)) << 32) |
+                       (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)src.base);
+    return __builtin_amdgcn_make_buffer_rsrc((void*)a, (short)0, __builtin_amdgcn_readfirstlane(src.nbytes), 0x00020000);
+}
+
 // bf16 tiles, 64 rows or columns x 32 k, stored as lds[t][k] (row stride 40 bf16), loaded into
 // registers first (up to 32 bytes per thread; fp32 sources are rounded to bf16 on the way in).
 //   KC (rows = t): fp32 two float4 of 4 k, bf16 one 16-byte load of 8 k;
@@ -268,6 +308,48 @@ __device__ inline void bf_store_nc(bf16_t* lds, const BfRaw& v, int tid) {
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) *(uint32_t*)(lds + (cq + j) * LDK + k) = e[0][j] | (e[1][j] << 16);
+}
+
+// The same tiles through a buffer descriptor (b3_src with the source's element size): rows
+// past the tile's valid rows and contraction steps past k_valid read as zero, with no branch,
+// so that several k-tiles can be in flight with exact wait counters.
+template <typename TS, bool KC>
+__device__ inline BfRaw bf_bload(const B3Src& src, int t_valid_rel, int k0, int k_valid, int tid) {
+    constexpr uint32_t ES = sizeof(TS);
+    BfRaw v;
+    v.r[0] = v.r[1] = make_uint4(0, 0, 0, 0);
+    if constexpr (KC) {
+        if constexpr (ES == 4) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int idx = tid + h * 256, r = idx >> 3, kq = (idx & 7) * 4;
+                const uint32_t inv = (uint32_t)(k_valid - 1 - (k0 + kq)) >> 31;
+                const uint32_t off = ((uint32_t)r * src.ld4 + (uint32_t)(k0 + kq) * ES) | (inv << 31);
+                v.r[h] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(src), off, 0, 0));
+            }
+        } else {
+            const int r = tid >> 2, kq = (tid & 3) * 8;
+            const uint32_t inv = (uint32_t)(k_valid - 1 - (k0 + kq)) >> 31;
+            const uint32_t off = ((uint32_t)r * src.ld4 + (uint32_t)(k0 + kq) * ES) | (inv << 31);
+            v.r[0] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(src), off, 0, 0));
+        }
+    } else {
+        const int k = (tid & 15) * 2, cq = (tid >> 4) * 4;
+        const uint32_t inv = (uint32_t)(t_valid_rel - 1 - cq) >> 31;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t off = ((uint32_t)(k0 + k + h) * src.ld4 + (uint32_t)cq * ES) | (inv << 31);
+            if constexpr (ES == 4) {
+                v.r[h] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(src), off, 0, 0));
+            } else {
+                typedef unsigned int u2v_t __attribute__((ext_vector_type(2)));
+                const u2v_t q = __builtin_bit_cast(u2v_t, __builtin_amdgcn_raw_buffer_load_b64(b3_rsrc(src), off, 0, 0));
+                v.r[h].x = q.x;
+                v.r[h].y = q.y;
+            }
+        }
+    }
+    return v;
 }
 
 // fp32 tiles of an operand whose rows are the contraction index ("NC" layout) stay as they
@@ -423,30 +505,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             buf ^= 1;
         }
     } else {
-        BfRaw ra, rb;
-        auto load = [&](int k0) {
-            if constexpr (A_KC) ra = bf_load_kc<TA>(g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
-            else ra = bf_load_nc<TA>(g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
-            if constexpr (B_KC) rb = bf_load_kc<TB>(g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
-            else rb = bf_load_nc<TB>(g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
-        };
-        auto store = [&](int buf) {
-            if constexpr (A_KC) bf_store_kc<TA>(As + buf * ASZ, ra, tid);
-            else bf_store_nc<TA>(As + buf * ASZ, ra, tid);
-            if constexpr (B_KC) bf_store_kc<TB>(Bs + buf * BSZ, rb, tid);
-            else bf_store_nc<TB>(Bs + buf * BSZ, rb, tid);
-        };
-        if (kbeg < kend) {
-            load(kbeg);
-            store(0);
-        }
-        __syncthreads();
-        int buf = 0;
-        for (int k0 = kbeg; k0 < kend; k0 += BK) {
-            const bool more = k0 + BK < kend;
-            if (more) load(k0 + BK);
-            const LT* A = As + buf * ASZ;
-            const LT* Bt = Bs + buf * BSZ;
+        // the bf16 tiles of the contraction: the steps of the weight update (a short contraction
+        // over the batch) as they come, one k-tile ahead; the others through the deeper pipeline
+        // below
+        auto compute_tile = [&](const LT* A, const LT* Bt) {
             if (do_rowsum && tid < 64) {
                 float s = 0.f;
 #pragma unroll
@@ -464,9 +526,76 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = SW ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[j], av[i], acc[i][j], 0, 0, 0)
                                    : __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-            if (more) store(buf ^ 1);
+        };
+        if constexpr (EPI == EPI_UPD) {
+            BfRaw ra, rb;
+            auto load = [&](int k0) {
+                if constexpr (A_KC) ra = bf_load_kc<TA>(g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+                else ra = bf_load_nc<TA>(g.a, zz, cn, xbase, m0, Mv, k0, kend, tid);
+                if constexpr (B_KC) rb = bf_load_kc<TB>(g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+                else rb = bf_load_nc<TB>(g.b, zz, cn, xbase, n0, Nv, k0, kend, tid);
+            };
+            auto store = [&](int buf) {
+                if constexpr (A_KC) bf_store_kc<TA>(As + buf * ASZ, ra, tid);
+                else bf_store_nc<TA>(As + buf * ASZ, ra, tid);
+                if constexpr (B_KC) bf_store_kc<TB>(Bs + buf * BSZ, rb, tid);
+                else bf_store_nc<TB>(Bs + buf * BSZ, rb, tid);
+            };
+            if (kbeg < kend) {
+                load(kbeg);
+                store(0);
+            }
             __syncthreads();
-            buf ^= 1;
+            int buf = 0;
+            for (int k0 = kbeg; k0 < kend; k0 += BK) {
+                const bool more = k0 + BK < kend;
+                if (more) load(k0 + BK);
+                compute_tile(As + buf * ASZ, Bs + buf * BSZ);
+                if (more) store(buf ^ 1);
+                __syncthreads();
+                buf ^= 1;
+            }
+        } else {
+            // k-tile i is loaded into register set i % BF_PD, BF_PD tiles ahead of its use, through
+            // buffer descriptors (no branch: exact wait counters); it goes to LDS buffer i & 1 one
+            // tile ahead.  (The contraction of these layers is long and each tile's matrix work
+            // short: the loop is bound by memory latency, which the tiles in flight cover.)
+            constexpr int BF_PD = 2;
+            BfRaw ra[BF_PD], rb[BF_PD];
+            const B3Src sa = b3_src<A_KC, sizeof(TA)>(g.a, zz, cn, xbase, m0, Mv, kend);
+            const B3Src sb = b3_src<B_KC, sizeof(TB)>(g.b, zz, cn, xbase, n0, Nv, kend);
+            auto load = [&](BfRaw& xa, BfRaw& xb, int k0) {
+                xa = bf_bload<TA, A_KC>(sa, Mv - m0, k0, kend, tid);
+                xb = bf_bload<TB, B_KC>(sb, Nv - n0, k0, kend, tid);
+            };
+            auto store = [&](int buf, const BfRaw& xa, const BfRaw& xb) {
+                if constexpr (A_KC) bf_store_kc<TA>(As + buf * ASZ, xa, tid);
+                else bf_store_nc<TA>(As + buf * ASZ, xa, tid);
+                if constexpr (B_KC) bf_store_kc<TB>(Bs + buf * BSZ, xb, tid);
+                else bf_store_nc<TB>(Bs + buf * BSZ, xb, tid);
+            };
+            const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+#pragma unroll
+            for (int p = 0; p < BF_PD; ++p)
+                if (p < nk) load(ra[p], rb[p], kbeg + p * BK);
+            // tile 0 to LDS; its register set takes tile BF_PD
+            if (nk > 0) store(0, ra[0], rb[0]);
+            if (BF_PD < nk) load(ra[0], rb[0], kbeg + BF_PD * BK);
+            __syncthreads();
+            // tile i = i0 + p (register set p); after its matrix instructions, tile i + 1 (set
+            // (p + 1) % BF_PD) goes to the other buffer and that set takes tile i + 1 + BF_PD
+            for (int i0 = 0; i0 < nk; i0 += BF_PD)
+#pragma unroll
+            for (int p = 0; p < BF_PD; ++p) {
+                const int i = i0 + p;
+                if (i >= nk) break;
+                const int buf = i & 1;
+                compute_tile(As + buf * ASZ, Bs + buf * BSZ);
+                const int pn = (p + 1) % BF_PD;
+                if (i + 1 < nk) store(buf ^ 1, ra[pn], rb[pn]);
+                if (i + 1 + BF_PD < nk) load(ra[pn], rb[pn], kbeg + (i + 1 + BF_PD) * BK);
+                __syncthreads();
+            }
         }
     }
 
@@ -527,6 +656,124 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     if (do_rowsum && tid < 64 && m0 + tid < Mv) {
         float* b = g.ubias + (size_t)cn * g.bias_z;
         b[m0 + tid] -= scale * rowsum[tid];
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// bf16 forward product of at most 64 rows (one training step's batch) with both operands
+// along k, C[64 x 64 tile] = A[64 x K] B[64 x K]^T with gemm_kernel's forward epilogue.  The
+// four waves split the contraction (wave w takes the 32-deep steps w, w + 4, ...) and read
+// their fragments straight from global memory in the matrix instruction's layout (A rows
+// 16 i + lane % 16, B rows 16 j + lane % 16, k 8 (lane / 16) .. + 7 of the step; fp32 A rounded
+// to bf16 on the way), KW_PD steps ahead through buffer descriptors (steps past K read zero):
+// no LDS staging and no barrier in the loop, which in the staged kernel is bound by latency on
+// these long, narrow contractions.  The partial tiles meet in LDS and are added in wave order;
+// wave w then finishes rows 16 w .. 16 w + 15 of the tile.
+
+constexpr int KW_PD = 2;
+
+template <typename TA, typename TO>
+__global__ __launch_bounds__(256) void gemm_kw_kernel(GemmArgs g) {
+    __shared__ __attribute__((aligned(16))) float red[4 * 64 * 64];  // [wave][i][j][lane][4]
+    constexpr int AV = sizeof(TA) / 2;  // 16-byte loads per A fragment
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, rl = lane & 15, kg = lane >> 4;
+    int bx, by, bz;
+    gemm_tile(bx, by, bz);
+    const int zz = bz;
+    int cn, valid;
+    int64_t r0;
+    gemm_zinfo(g, zz, cn, r0, valid);
+    const int Mv = (g.sample_dims & 1) ? valid : g.M;
+    const int Nv = (g.sample_dims & 2) ? valid : g.N;
+    const int Kv = g.Kd;
+    const int m0 = by * 64, n0 = bx * 64;
+    if (m0 >= Mv || n0 >= Nv) return;
+    const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
+    const B3Src sa = b3_src<true, sizeof(TA)>(g.a, zz, cn, xbase, m0, Mv, Kv);
+    const B3Src sb = b3_src<true, 2>(g.b, zz, cn, xbase, n0, Nv, Kv);
+
+    f4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    uint4 fa[KW_PD][4][AV], fb[KW_PD][4];
+    auto load = [&](int p, int s) {
+        const int k = 32 * s + 8 * kg;
+        const uint32_t inv = (uint32_t)(Kv - 1 - k) >> 31;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t o = ((uint32_t)(16 * i + rl) * sa.ld4 + (uint32_t)k * (uint32_t)sizeof(TA)) | (inv << 31);
+#pragma unroll
+            for (int v = 0; v < AV; ++v)
+                fa[p][i][v] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(sa), o + 16u * v, 0, 0));
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t o = ((uint32_t)(16 * j + rl) * sb.ld4 + (uint32_t)k * 2u) | (inv << 31);
+            fb[p][j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(sb), o, 0, 0));
+        }
+    };
+    auto mma = [&](int p) {
+        bf8v av[4], bv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (AV == 2) {
+                const uint4 x0 = fa[p][i][0], x1 = fa[p][i][1];
+                const uint4 q = make_uint4(cvt_pk_bf16(__uint_as_float(x0.x), __uint_as_float(x0.y)),
+                                           cvt_pk_bf16(__uint_as_float(x0.z), __uint_as_float(x0.w)),
+                                           cvt_pk_bf16(__uint_as_float(x1.x), __uint_as_float(x1.y)),
+                                           cvt_pk_bf16(__uint_as_float(x1.z), __uint_as_float(x1.w)));
+                av[i] = __builtin_bit_cast(bf8v, q);
+            } else {
+                av[i] = __builtin_bit_cast(bf8v, fa[p][i][0]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bv[j] = __builtin_bit_cast(bf8v, fb[p][j]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[j], av[i], acc[i][j], 0, 0, 0);
+    };
+    // the wave's steps q = 0, 1, ... are the contraction steps wave + 4 q; register set q % KW_PD
+    const int nsteps = (Kv + 31) / 32;
+    const int nq = nsteps > wave ? (nsteps - wave + 3) / 4 : 0;
+#pragma unroll
+    for (int p = 0; p < KW_PD; ++p) load(p, wave + 4 * p);
+    for (int q0 = 0; q0 < nq; q0 += KW_PD)
+#pragma unroll
+        for (int p = 0; p < KW_PD; ++p) {
+            if (q0 + p >= nq) break;
+            mma(p);
+            load(p, wave + 4 * (q0 + p + KW_PD));  // (past the contraction: zeros, unused)
+        }
+
+    // the four partial tiles, added in wave order; wave w finishes block row i = w
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *(f4*)(red + (((wave * 4 + i) * 4 + j) * 64 + lane) * 4) = acc[i][j];
+    __syncthreads();
+    const int i = wave;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        f4 v = *(const f4*)(red + (((0 * 4 + i) * 4 + j) * 64 + lane) * 4);
+#pragma unroll
+        for (int w = 1; w < 4; ++w) v += *(const f4*)(red + (((w * 4 + i) * 4 + j) * 64 + lane) * 4);
+        const int m = m0 + 16 * i + rl, n = n0 + 16 * j + 4 * kg;
+        if (m >= Mv || n >= Nv) continue;
+        const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+        const float* bb = g.bias + (size_t)cn * g.bias_z + n;
+        if (n + 3 < Nv && ((g.c_ld | g.c_z | g.bias_z) & 3) == 0) {
+            const float4 b4 = *(const float4*)bb;
+            store4<TO>((TO*)g.c + ci, make_float4(act_fn(g.act, v[0] + b4.x), act_fn(g.act, v[1] + b4.y),
+                                                  act_fn(g.act, v[2] + b4.z), act_fn(g.act, v[3] + b4.w)));
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                if (n + r < Nv) ((TO*)g.c)[ci + r] = from_f<TO>(act_fn(g.act, v[r] + bb[r]));
+        }
     }
 }
 
@@ -760,12 +1007,6 @@ constexpr int B3_BK = 32, B3_LDK = 40, B3_PLANE = 128 * B3_LDK;   // bf16 elemen
 constexpr int B3_STAGE = 2 * 3 * B3_PLANE;                         // A and B, three planes each
 __host__ __device__ constexpr size_t b3_lds_bytes() { return (size_t)2 * B3_STAGE * sizeof(bf16_t); }
 
-typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
-// two floats to packed bf16 (one v_cvt_pk_bf16_f32), x in the low half
-__device__ inline uint32_t cvt_pk_bf16(float x, float y) {
-    const bf2v p = {(__bf16)x, (__bf16)y};
-    return __builtin_bit_cast(uint32_t, p);
-}
 // the fp32 value of the low bf16 of a packed pair (a byte permute: written as a shift, the
 // compiler re-derives it with a second conversion)
 __device__ inline float bf_lo(uint32_t p) { return __uint_as_float(__builtin_amdgcn_perm(0u, p, 0x01000c0cu)); }
@@ -795,38 +1036,6 @@ template <bool KC>
 __device__ inline int b3_off(int t, int k) {
     if (KC) return t * B3_BK + ((((k >> 3) ^ ((t >> 1) & 3))) << 3) + (k & 7);
     return t * B3_LDK + k;
-}
-
-// Branch-free loads through a buffer descriptor: an element outside the tile's valid rows lies
-// past the descriptor's range, one past the valid contraction gets an offset beyond it, and both
-// read as zero, so the wait counters stay exact across the pipeline.  KC: the descriptor starts
-// at the tile's first row (t0) and spans its valid rows; NC: it starts at the tile's first
-// column (t0) of contraction row 0 and ends with the last valid contraction row.
-struct B3Src {
-    uint64_t base;  // first byte (the same in every lane)
-    int nbytes;     // bytes in range
-    uint32_t ld4;   // row stride in bytes
-};
-
-template <bool KC>
-__device__ inline B3Src b3_src(const Operand& o, int z, int cn, int64_t xbase, int t0, int t_valid, int k_valid) {
-    B3Src r;
-    r.ld4 = (uint32_t)(o.ld * 4);
-    const int rows = KC ? t_valid - t0 : k_valid;
-    const char* base = KC ? operand_row(o, 4, z, cn, xbase, t0) : operand_row(o, 4, z, cn, xbase, 0) + (size_t)t0 * 4;
-    int64_t bytes = (int64_t)rows * o.ld * 4 - (KC ? 0 : (int64_t)t0 * 4);
-    if (rows <= 0 || bytes < 0) bytes = 0;
-    r.base = (uint64_t)base;
-    r.nbytes = (int)bytes;
-    return r;
-}
-
-// the descriptor, built where it is used from values made scalar explicitly (they are the same
-// in every lane; otherwise every buffer load would loop over the lanes' descriptors)
-__device__ inline __amdgpu_buffer_rsrc_t b3_rsrc(const B3Src& src) {
-    const uint64_t a = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(src.base >> 32)) << 32) |
-                       (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)src.base);
-    return __builtin_amdgcn_make_buffer_rsrc((void*)a, (short)0, __builtin_amdgcn_readfirstlane(src.nbytes), 0x00020000);
 }
 
 template <bool KC>

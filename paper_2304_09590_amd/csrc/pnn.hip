@@ -362,6 +362,15 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
             return l.done();
         }
     }
+    // the bf16 forward product of a training step's batch (at most 64 rows): the waves of a
+    // tile split the contraction (gemm_kw_kernel)
+    if constexpr (BF && A_KC && B_KC && EPI == EPI_FWD && sizeof(TB) == 2) {
+        if (g.M <= 64 && g.ksplit == 1 && g.Kd % 8 == 0 && !(g.sample_dims & 4)) {
+            Launch l(n, s, name);
+            gemm_kw_kernel<TA, TO><<<grid, 256, 0, s>>>(g);
+            return l.done();
+        }
+    }
     Launch l(n, s, name);
     if (EPI == EPI_UPD && g.Kd <= 64) gemm_kernel<BF, TA, TB, A_KC, B_KC, EPI, TO, EPI == EPI_UPD><<<grid, 256, 0, s>>>(g);
     else gemm_kernel<BF, TA, TB, A_KC, B_KC, EPI, TO><<<grid, 256, 0, s>>>(g);
