@@ -199,6 +199,41 @@ def test_chunked_plan_epoch(over, N):
     net.close()
 
 
+# ------------------------------------------------------------------------------------
+# the fp32 products on the fp32 matrix instructions (PNN_GEMM=fp32: gemm128_kernel for the
+# forward, gemm_kernel for the update) instead of the split-bf16 kernels
+
+
+@pytest.mark.parametrize("idx,over,N,epochs", [
+    (4, dict(replicas=16), 16 * 260 + 7, 2),
+    (2, dict(sizes=(784, 192, 10), replicas=4), 4 * 100 + 5, 1),
+])
+def test_epochs_fp32_matrix_path(idx, over, N, epochs, monkeypatch):
+    monkeypatch.setenv("PNN_GEMM", "fp32")
+    monkeypatch.setenv("PNN_MB_PLAN", "launch")
+    w = I.WORKLOADS[idx].scaled(**over)
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    assert net.plan == "mini-batch"
+    log(f"fp32 matrix path: {w.name} {over} N={N}")
+    xd, yd = dev(X), dev(y)
+    net.profile(True)
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    for e in range(epochs):
+        net.train_epoch(xd, yd)
+        o.train_epoch(ref, X, y, threads=8)
+        for k in range(w.replicas):
+            close_epoch(w, net.get_params(k), ref[k], f"epoch {e} replica {k}")
+        if w.merge_every_epoch:
+            net.merge(broadcast=True)
+            ref[:] = o.merge(ref)[None, :]
+    names = set(net.profile_read())
+    assert names and not any(n.endswith("_x3") for n in names), names
+    net.close()
+
+
 PLAN_CASES = [
     # workload, overrides, plan chosen at init
     (1, {}, "per-sample persistent"),
