@@ -40,6 +40,19 @@ EPOCH_CASES = [
     (2, dict(sizes=(784, 56, 10), acts=(I.SIGMOID, I.SIGMOID), batch=7, replicas=5), 5 * 40 + 3, 2),
     (2, dict(replicas=20), 20 * 40 + 3, 1),
     (2, dict(acts=(I.RELU, I.SOFTMAX), loss=I.LOSS_XENT, batch=2, replicas=3), 3 * 30 + 2, 1),
+    # edge shapes: the most weight layers (8, mini-batch, every activation); four layers with
+    # B = 1 (the generic per-sample path); one weight layer (logistic regression); the widest
+    # output layer (16, softmax); a single sigmoid output; a hidden width that leaves the
+    # per-sample kernel's last 16-row tile half empty; bf16-mixed with B = 1
+    (2, dict(sizes=(784, 64, 56, 48, 40, 32, 24, 16, 10),
+             acts=(I.RELU, I.TANH, I.LEAKY_RELU, I.SIGMOID, I.RELU, I.TANH, I.SIGMOID, I.SOFTMAX),
+             loss=I.LOSS_XENT, batch=8, replicas=3), 3 * 50 + 2, 1),
+    (0, dict(sizes=(784, 40, 24, 16, 10), acts=(I.RELU, I.TANH, I.SIGMOID, I.SIGMOID), replicas=2), 2 * 40 + 1, 1),
+    (2, dict(sizes=(784, 10), acts=(I.SOFTMAX,), loss=I.LOSS_XENT, batch=8, replicas=4), 4 * 40 + 3, 2),
+    (2, dict(sizes=(784, 64, 16), acts=(I.SIGMOID, I.SOFTMAX), loss=I.LOSS_XENT, batch=16, replicas=4), 4 * 60 + 1, 1),
+    (2, dict(sizes=(784, 32, 1), acts=(I.SIGMOID, I.SIGMOID), batch=4, replicas=2), 2 * 40 + 1, 1),
+    (1, dict(sizes=(784, 40, 10), replicas=3), 3 * 70 + 1, 1),
+    (3, dict(sizes=(784, 64, 10), acts=(I.RELU, I.SOFTMAX), batch=1, replicas=2, merge_every_epoch=False), 2 * 40, 1),
     # persistent mini-batch plan in CN groups (32-neuron tiles): 80 CNs in 3 launches of
     # 26/27/27; 64 CNs in 2 launches of 32, merge + broadcast each epoch
     (2, dict(replicas=80), 80 * 40 + 3, 1),

@@ -103,7 +103,11 @@ def oracle_replicas(o: O.Oracle, thetas: np.ndarray, ids: Sequence[int], X, y, t
 
 def argmax_agrees(out_ref: np.ndarray, pred_gpu: np.ndarray, margin: float = 1e-5):
     """GPU predictions equal the oracle's argmax except where the oracle's top two outputs are
-    within `margin` (then either of the tied classes is accepted)."""
+    within `margin` (then either of the tied classes is accepted).  With a single output the
+    prediction is that output's index, 0."""
+    if out_ref.shape[1] < 2:
+        assert (pred_gpu == 0).all(), "a single-output network predicts class 0"
+        return 0
     top = np.argmax(out_ref, axis=1)
     srt = np.sort(out_ref, axis=1)
     gap = srt[:, -1] - srt[:, -2]
