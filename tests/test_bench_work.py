@@ -64,3 +64,15 @@ def test_persistent_minibatch_effective_bytes():
 def test_unpriced_kernels():
     w = I.WORKLOADS[2]
     assert bench.kernel_work(w, "fwd_reduce", 1, w.n_train, 1) is None
+
+
+def test_more_than_one_gpu_is_refused():
+    # one GPU only: bench.py --gpus N with N > 1 exits with a message before touching a device
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
