@@ -473,16 +473,18 @@ def test_full_workload1_all_replicas():
     _full(w, list(range(w.replicas)), threads=4)
 
 
-def test_full_workload2_sampled():
-    _full(I.WORKLOADS[2], [0, 15])
+def test_full_workload2_all_replicas():
+    w = I.WORKLOADS[2]
+    _full(w, list(range(w.replicas)))
 
 
 def test_full_workload3_sampled():
-    _full(I.WORKLOADS[3], [0, 63])
+    _full(I.WORKLOADS[3], [0, 9, 18, 27, 36, 45, 54, 63])
 
 
 def test_full_workload4_sampled():
-    _full(I.WORKLOADS[4], [0, 191, 192, 255])
+    # every sixteenth CN and both sides of the slice-length boundary (CNs 191 / 192)
+    _full(I.WORKLOADS[4], sorted(set(range(0, 256, 16)) | {191, 192, 255}))
 
 
 # ------------------------------------------------------------------------------------
