@@ -9,7 +9,7 @@ import pnn_inputs as I
 
 EPOCH_CASES = [
     # workload, overrides, N, epochs
-    (0, {}, 2000, 1),                                         # workload 0 at full size
+    (0, {}, 2000, 1),                                         # 784-16-10, K = 1, at full size
     (1, {}, 4 * 300 + 3, 1),                                  # per-sample chunks with a ragged tail
     (1, dict(replicas=3), 3 * 140 + 1, 2),                    # uneven slices, two epochs
     (2, {}, 16 * 100 + 5, 2),                                 # batches 32,32,32,4/5
