@@ -6,6 +6,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <type_traits>
 
 namespace pnn {
 
@@ -1263,6 +1264,143 @@ __global__ __launch_bounds__(B3_THREADS) void gemm128x3_kernel(GemmArgs g) {
 }
 
 // ------------------------------------------------------------------------------------
+// fp32 GEMM on the bf16 matrix cores, 128 x 256 tiles, both operands along k (forward):
+// the three-part split of gemm128x3_kernel with twice the matrix work per split value.
+//
+// Eight waves of 64 x 64 (4 x 4 blocks), two per SIMD, one workgroup per CU (144 KiB of dynamic
+// LDS: two stages of A's three planes, 128 rows, and B's, 256 rows, laid out by b3_off<true>).
+// Per 32-deep k-tile a wave issues 96 matrix instructions against 12 splits of two values (48
+// against 8 in the 128 x 128 kernel): a quarter fewer of the split's vector instructions, which
+// the matrix cores do not overlap, per matrix instruction.  B's fragments stay in registers for
+// the k-tile and A's are read one plane at a time (l, m, h), which keeps the wave within the 256
+// registers of two waves per SIMD (a few spill).
+constexpr int G2_PA = 128 * B3_BK, G2_PB = 256 * B3_BK;       // plane sizes (64-byte rows)
+constexpr int G2_STAGE = 3 * G2_PA + 3 * G2_PB;
+__host__ __device__ constexpr size_t g2_lds_bytes() { return (size_t)2 * G2_STAGE * sizeof(bf16_t); }
+
+// split and store part u of a KC k-tile into three planes pstride apart, rows + row_off
+__device__ inline void g2_store(bf16_t* plane0, int pstride, const B3Raw& r, int u, int tid, int row_off) {
+    const int t = kc_row(tid, u) + row_off, k = (tid & 7) * 4;
+    uint32_t h0, m0, l0, h1, m1, l1;
+    split3_pk(r.v[u].x, r.v[u].y, h0, m0, l0);
+    split3_pk(r.v[u].z, r.v[u].w, h1, m1, l1);
+    bf16_t* d = plane0 + b3_off<true>(t, k);
+    *(uint2*)d = make_uint2(h0, h1);
+    *(uint2*)(d + pstride) = make_uint2(m0, m1);
+    *(uint2*)(d + 2 * pstride) = make_uint2(l0, l1);
+}
+
+template <int EPI>
+__global__ __launch_bounds__(B3_THREADS) void gemm256x3_kernel(GemmArgs g) {
+    extern __shared__ __attribute__((aligned(16))) bf16_t g2s[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 2, wn = wave & 3;  // wave tile: rows 64 wm, columns 64 wn
+    int bx, by, bz;
+    gemm_tile(bx, by, bz);
+    const int zz = bz;
+    int cn, valid;
+    int64_t r0;
+    gemm_zinfo(g, zz, cn, r0, valid);
+    const int Mv = (g.sample_dims & 1) ? valid : g.M;
+    const int Nv = (g.sample_dims & 2) ? valid : g.N;
+    const int Kv = g.Kd;
+    const int m0 = by * 128, n0 = bx * 256;
+    if (m0 >= Mv || n0 >= Nv) return;
+    const int kend = Kv;
+    const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
+    f4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    const B3Src sa = b3_src<true>(g.a, zz, cn, xbase, m0, Mv, kend);
+    const B3Src sb0 = b3_src<true>(g.b, zz, cn, xbase, n0, Nv, kend);
+    const B3Src sb1 = b3_src<true>(g.b, zz, cn, xbase, min(n0 + 128, Nv), Nv, kend);
+    B3Raw ra, rb0, rb1, na, nb0, nb1;
+    auto load = [&](B3Raw& xa, B3Raw& xb0, B3Raw& xb1, int k0) {
+        b3_load<true>(xa, sa, Mv - m0, k0, kend, tid);
+        b3_load<true>(xb0, sb0, Nv - n0, k0, kend, tid);
+        b3_load<true>(xb1, sb1, Nv - n0 - 128, k0, kend, tid);
+    };
+    auto store_all = [&](bf16_t* st, const B3Raw& xa, const B3Raw& xb0, const B3Raw& xb1) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            g2_store(st, G2_PA, xa, u, tid, 0);
+            g2_store(st + 3 * G2_PA, G2_PB, xb0, u, tid, 0);
+            g2_store(st + 3 * G2_PA, G2_PB, xb1, u, tid, 128);
+        }
+    };
+    load(ra, rb0, rb1, 0);
+    store_all(g2s, ra, rb0, rb1);
+    load(ra, rb0, rb1, B3_BK);
+    __syncthreads();
+    int buf = 0;
+    const int rl = lane & 15, kg = lane >> 4;
+    auto step = [&](int k0, const B3Raw& xa, const B3Raw& xb0, const B3Raw& xb1, B3Raw& ya, B3Raw& yb0, B3Raw& yb1) {
+        load(ya, yb0, yb1, k0 + 2 * B3_BK);
+        const bf16_t* A = g2s + buf * G2_STAGE;
+        const bf16_t* Bt = A + 3 * G2_PA;
+        bf16_t* An = g2s + (buf ^ 1) * G2_STAGE;
+        bf8v bv[3][4];
+#pragma unroll
+        for (int p = 0; p < 3; ++p)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                bv[p][j] = *(const bf8v*)(Bt + p * G2_PB + b3_off<true>(wn * 64 + j * 16 + rl, kg * 8));
+        // A planes l, m, h in turn: l.h, then m.m, m.h, then h.l, h.m, h.h
+        int t = 0;
+#pragma unroll
+        for (int pa = 2; pa >= 0; --pa) {
+            bf8v av[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) av[i] = *(const bf8v*)(A + pa * G2_PA + b3_off<true>(wm * 64 + i * 16 + rl, kg * 8));
+#pragma unroll
+            for (int pb = 2 - pa; pb >= 0; --pb, ++t) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[pb][j], av[i], acc[i][j], 0, 0, 0);
+                if (t == 0 || t == 1) g2_store(An, G2_PA, xa, t, tid, 0);
+                if (t == 2 || t == 3) g2_store(An + 3 * G2_PA, G2_PB, xb0, t - 2, tid, 0);
+                if (t == 4 || t == 5) g2_store(An + 3 * G2_PA, G2_PB, xb1, t - 4, tid, 128);
+            }
+        }
+        __syncthreads();
+        buf ^= 1;
+    };
+    for (int k0 = 0; k0 < kend; k0 += 2 * B3_BK) {
+        step(k0, ra, rb0, rb1, na, nb0, nb1);
+        if (k0 + B3_BK >= kend) break;
+        step(k0 + B3_BK, na, nb0, nb1, ra, rb0, rb1);
+    }
+    const bool vec = ((g.c_ld | g.c_z | g.bias_z) & 3) == 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + wm * 64 + i * 16 + rl, n = n0 + wn * 64 + j * 16 + kg * 4;
+            if (m >= Mv || n >= Nv) continue;
+            const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+            const f4 v = acc[i][j];
+            if constexpr (EPI == EPI_FWD) {
+                const float* bb = g.bias + (size_t)cn * g.bias_z + n;
+                if (vec && n + 3 < Nv) {
+                    const float4 b4 = *(const float4*)bb;
+                    *(float4*)((float*)g.c + ci) = make_float4(act_fn(g.act, v[0] + b4.x), act_fn(g.act, v[1] + b4.y),
+                                                               act_fn(g.act, v[2] + b4.z), act_fn(g.act, v[3] + b4.w));
+                } else {
+                    for (int r = 0; r < 4; ++r)
+                        if (n + r < Nv) ((float*)g.c)[ci + r] = act_fn(g.act, v[r] + bb[r]);
+                }
+            } else {
+                for (int r = 0; r < 4; ++r)
+                    if (n + r < Nv) ((float*)g.c)[ci + r] = v[r];
+            }
+        }
+}
+
+// ------------------------------------------------------------------------------------
 // Weight update W -= eta / B_t * delta^T x on the bf16 matrix cores (fp32 operands split in
 // three bf16 parts, as in gemm128x3_kernel), for a contraction over at most 128 samples.
 //
@@ -1274,6 +1412,7 @@ __global__ __launch_bounds__(B3_THREADS) void gemm128x3_kernel(GemmArgs g) {
 // samples' input columns x[s][n0 ..] stream through two LDS stages in k-chunks of 32 samples
 // (loaded two chunks ahead, across tile boundaries), and each finished tile's targets, loaded
 // one tile ahead, take their update and go back.  A: NC operand (rows = samples), B: NC.
+// FULL: updates over 97 .. 128 samples, four k-chunks per tile (zero padded).
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 constexpr int U3_KMAX = 128;   // samples of one update
@@ -1284,6 +1423,7 @@ __host__ __device__ constexpr size_t u3_lds_bytes() {
 // element offset of (row m, sample k) in a plane of the errors (16-byte chunks swizzled)
 __device__ inline int u3_off(int m, int k) { return m * U3_KMAX + ((((k >> 3) ^ (m & 15))) << 3) + (k & 7); }
 
+template <bool FULL>
 __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     extern __shared__ __attribute__((aligned(16))) bf16_t u3s[];
     bf16_t* dpl = u3s;                   // [3][128 m][128 k] errors, swizzled
@@ -1303,7 +1443,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     const int m0 = by * 128;
     if (m0 >= Mv || Kv <= 0) return;
     const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
-    const int nkc = (Kv + B3_BK - 1) / B3_BK;          // k-chunks per tile
+    const int nkc = FULL ? 4 : (Kv + B3_BK - 1) / B3_BK;   // k-chunks per tile
     const int ntile = (Nv + 127) / 128;
     const int nsteps = ntile * nkc;
     const float scale = g.scale_per_batch ? g.lr / (float)Kv : g.lr;
@@ -1437,14 +1577,80 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
         __syncthreads();
         buf ^= 1;
     };
-    // three input register sets in rotation: chunk q+1 (split now), q+2, q+3 (in flight)
-    B3Raw rc;
-    for (int q = 0; q < nsteps; q += 3) {
-        step(q, na, rc);
-        if (q + 1 >= nsteps) break;
-        step(q + 1, ra, na);
-        if (q + 2 >= nsteps) break;
-        step(q + 2, rc, ra);
+    if constexpr (FULL) {
+        // four k-chunks per tile (chunks past the CN's samples load as zeros and add exact
+        // zeros): every step's place in the tile is fixed at compile time (stage, input register
+        // set, the targets' loads and the epilogue), two tiles per trip with the targets'
+        // register sets alternating.  Input chunk c lives in set c % 4.  (With the tile's place
+        // known, the compiler's wait counts stay exact: the generic loop below, whose tile ends
+        // are data-dependent, waits for every outstanding memory operation at some steps.)
+        B3Raw xs0, xs1 = na, xs2 = ra, xs3;   // chunks 1, 2 (in flight)
+        float4 (&wa)[4][2] = wcur;
+        float4 (&wb)[4][2] = wnext;
+        auto fstep = [&](auto KC, int tn, float4 (&wc)[4][2], float4 (&wx)[4][2]) __attribute__((always_inline)) {
+            constexpr int kc = decltype(KC)::value;
+            const int q = tn * 4 + kc;
+            B3Raw& xl = kc == 0 ? xs3 : kc == 1 ? xs0 : kc == 2 ? xs1 : xs2;   // chunk q + 3
+            const B3Raw& xa = kc == 0 ? xs1 : kc == 1 ? xs2 : kc == 2 ? xs3 : xs0;  // chunk q + 1
+            xload(xl, q + 3);
+            if (kc == 0 && tn + 1 < ntile) load_w(wx, (tn + 1) * 128);
+            const bf16_t* Bt = xst + (kc & 1) * 3 * B3_PLANE;
+            bf16_t* Bn = xst + ((kc & 1) ^ 1) * 3 * B3_PLANE;
+            bf8v av[3][4], bv[3][2];
+#pragma unroll
+            for (int p = 0; p < 3; ++p) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    av[p][i] = *(const bf8v*)(dpl + p * U3_DPLANE + u3_off(wm * 64 + i * 16 + rl, kc * B3_BK + kg * 8));
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    bv[p][j] = *(const bf8v*)(Bt + p * B3_PLANE + b3_off<false>(wn * 32 + j * 16 + rl, kg * 8));
+            }
+#pragma unroll
+            for (int t = 0; t < 6; ++t) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[PB[t]][j], av[PA[t]][i], acc[i][j], 0, 0, 0);
+                if (t == 1 || t == 3) b3_store_part<false>(Bn, xa, t >> 1, tid);
+            }
+            if (kc == 3) {
+                const int n0 = tn * 128;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) {
+                        const f4 v = acc[i][j];
+                        float4 w = wc[i][j];
+                        w.x -= scale * v[0]; w.y -= scale * v[1]; w.z -= scale * v[2]; w.w -= scale * v[3];
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), b3_rsrc(wsrc), woff(n0, i, j), 0, 0);
+                        acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+                    }
+            }
+            __syncthreads();
+        };
+        auto ftile = [&](int tn, float4 (&wc)[4][2], float4 (&wx)[4][2]) __attribute__((always_inline)) {
+            fstep(std::integral_constant<int, 0>{}, tn, wc, wx);
+            fstep(std::integral_constant<int, 1>{}, tn, wc, wx);
+            fstep(std::integral_constant<int, 2>{}, tn, wc, wx);
+            fstep(std::integral_constant<int, 3>{}, tn, wc, wx);
+        };
+        for (int tn = 0; tn < ntile; tn += 2) {
+            ftile(tn, wa, wb);
+            if (tn + 1 >= ntile) break;
+            ftile(tn + 1, wb, wa);
+        }
+    } else {
+        // three input register sets in rotation: chunk q+1 (split now), q+2, q+3 (in flight)
+        B3Raw rc;
+        for (int q = 0; q < nsteps; q += 3) {
+            step(q, na, rc);
+            if (q + 1 >= nsteps) break;
+            step(q + 1, ra, na);
+            if (q + 2 >= nsteps) break;
+            step(q + 2, rc, ra);
+        }
     }
 }
 

@@ -332,17 +332,38 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
             const int kmax = (g.sample_dims & 4) ? g.step_rows : g.Kd;
             if (n->gemm_x3 && g.M >= 128 && g.N >= 128 && kmax <= U3_KMAX && g.ksplit == 1 && g.shadow == nullptr &&
                 g.N % 4 == 0 && g.c_ld % 4 == 0) {
-                static const hipError_t attr = hipFuncSetAttribute((const void*)upd128x3_kernel,
-                                                                   hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                                   (int)u3_lds_bytes());
-                if (attr != hipSuccess) return fail(n, PNN_EHIP, "%s: hipFuncSetAttribute: %s", name, hipGetErrorString(attr));
+                static const hipError_t attr =
+                    hipFuncSetAttribute((const void*)upd128x3_kernel<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)u3_lds_bytes());
+                static const hipError_t attr_full =
+                    hipFuncSetAttribute((const void*)upd128x3_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)u3_lds_bytes());
+                if (attr != hipSuccess || attr_full != hipSuccess)
+                    return fail(n, PNN_EHIP, "%s: hipFuncSetAttribute: %s", name,
+                                hipGetErrorString(attr != hipSuccess ? attr : attr_full));
+                const dim3 grid_u(1, (g.M + 127) / 128, (unsigned)Z);
                 Launch l(n, s, x3_name(name));
-                upd128x3_kernel<<<dim3(1, (g.M + 127) / 128, (unsigned)Z), B3_THREADS, u3_lds_bytes(), s>>>(g);
+                // more than 96 samples: four k-chunks per tile, the compile-time schedule
+                if (kmax > 96) upd128x3_kernel<true><<<grid_u, B3_THREADS, u3_lds_bytes(), s>>>(g);
+                else upd128x3_kernel<false><<<grid_u, B3_THREADS, u3_lds_bytes(), s>>>(g);
                 return l.done();
             }
         }
-        // large fp32 shapes: 128 x 128 tiles on the bf16 matrix cores, each fp32 operand split
-        // into three bf16 parts (gemm128x3_kernel)
+        // large fp32 shapes with both operands along k and at least 256 columns: 128 x 256 tiles
+        // (gemm256x3_kernel)
+        if constexpr (A_KC && B_KC && (EPI == EPI_FWD || EPI == EPI_STORE)) {
+            if (n->gemm_x3 && g.M >= 128 && g.N >= 256 && g.shadow == nullptr && g.ksplit == 1 && !(g.sample_dims & 4)) {
+                static const hipError_t attr = hipFuncSetAttribute((const void*)gemm256x3_kernel<EPI>,
+                                                                   hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                                   (int)g2_lds_bytes());
+                if (attr != hipSuccess) return fail(n, PNN_EHIP, "%s: hipFuncSetAttribute: %s", name, hipGetErrorString(attr));
+                Launch l(n, s, x3_name(name));
+                gemm256x3_kernel<EPI><<<dim3((g.N + 255) / 256, (g.M + 127) / 128, (unsigned)Z), B3_THREADS, g2_lds_bytes(), s>>>(g);
+                return l.done();
+            }
+        }
+        // other large fp32 shapes: 128 x 128 tiles on the bf16 matrix cores, each fp32 operand
+        // split into three bf16 parts (gemm128x3_kernel)
         if (n->gemm_x3 && g.M >= 128 && g.N >= 128 && g.shadow == nullptr && (g.ksplit == 1 || g.kchunk % B3_BK == 0)) {
             static const hipError_t attr = hipFuncSetAttribute((const void*)gemm128x3_kernel<A_KC, B_KC, EPI>,
                                                                hipFuncAttributeMaxDynamicSharedMemorySize,
