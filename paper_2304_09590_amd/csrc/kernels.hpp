@@ -1593,7 +1593,9 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             B3Raw& xl = kc == 0 ? xs3 : kc == 1 ? xs0 : kc == 2 ? xs1 : xs2;   // chunk q + 3
             const B3Raw& xa = kc == 0 ? xs1 : kc == 1 ? xs2 : kc == 2 ? xs3 : xs0;  // chunk q + 1
             xload(xl, q + 3);
-            if (kc == 0 && tn + 1 < ntile) load_w(wx, (tn + 1) * 128);
+            // (unconditional: past the last tile every column is out of range, the loads read
+            // nothing and give zeros, and the wait counts stay exact)
+            if (kc == 0) load_w(wx, (tn + 1) * 128);
             const bf16_t* Bt = xst + (kc & 1) * 3 * B3_PLANE;
             bf16_t* Bn = xst + ((kc & 1) ^ 1) * 3 * B3_PLANE;
             bf8v av[3][4], bv[3][2];
@@ -1629,6 +1631,9 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                     }
             }
             __syncthreads();
+            // no instruction crosses a step boundary: the scheduler would otherwise hoist the next
+            // step's split of a chunk loaded one step ago, and its wait with it
+            __builtin_amdgcn_sched_barrier(0);
         };
         auto ftile = [&](int tn, float4 (&wc)[4][2], float4 (&wx)[4][2]) __attribute__((always_inline)) {
             fstep(std::integral_constant<int, 0>{}, tn, wc, wx);
@@ -1636,6 +1641,10 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             fstep(std::integral_constant<int, 2>{}, tn, wc, wx);
             fstep(std::integral_constant<int, 3>{}, tn, wc, wx);
         };
+        // the prologue's loads done before the loop (s_waitcnt vmcnt(0)): the wait counts at the
+        // loop head then follow only the loop's own operations (otherwise every trip waits as if
+        // a prologue load were still the latest, for the previous tile's stores among others)
+        __builtin_amdgcn_s_waitcnt(0x0f70);
         for (int tn = 0; tn < ntile; tn += 2) {
             ftile(tn, wa, wb);
             if (tn + 1 >= ntile) break;
