@@ -59,7 +59,7 @@ def method_flops_per_sample(w) -> float:
     return 4.0 * fw + 2.0 * back + 4.0 * bias
 
 
-def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
+def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int, fused_last: bool = False):
     """Algorithmic work of one launch of a library kernel: (flops, bytes), or None.
 
     psgd_persistent: one launch trains every CN for one epoch (per-sample SGD).  Priced in
@@ -84,6 +84,12 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
       tail (fused narrow last layer: forward, output error, hidden error, update):
                                  6 rows O H; K bsteps (O H (w_op + 8 + shadow) + 8 O) +
                                  rows (2 H a + 4)
+    With the last layer fused into the split-bf16 products (plan "mini-batch fused last
+    layer", fused_last): fwd_gemm adds the last layer's forward, 2 rows O H flops and
+    K bsteps O H 4 + rows O 4 bytes; out_err (output activation and error) rows O flops and
+    rows (8 O + 4) bytes; upd_gemm adds the hidden error and the last layer's update, 4 rows O H
+    flops and K bsteps (8 O H + 8 O) + rows O 4 bytes (it reads the activations in place of the
+    errors: the same bytes).
     merge: reads K*P floats and writes P (and K*P with broadcast).
     """
     if name.endswith("_x3"):
@@ -128,8 +134,20 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int):
         O, H = s[L], s[L - 1]
         f = 6 * rows * O * H
         b = K * bsteps * (O * H * (wop + 8 + shadow) + 8 * O) + rows * (2 * H * a + 4)
+    elif name == "out_err":
+        O = s[L]
+        f = rows * O
+        b = rows * (8 * O + 4)
     else:
         return None
+    if fused_last and name in ("fwd_gemm", "upd_gemm"):
+        O, H = s[L], s[L - 1]
+        if name == "fwd_gemm":
+            f += 2 * rows * O * H
+            b += K * bsteps * O * H * 4 + rows * O * 4
+        else:
+            f += 4 * rows * O * H
+            b += K * bsteps * (8 * O * H + 8 * O) + rows * O * 4
     return f / launches, b / launches
 
 
@@ -222,8 +240,9 @@ def schedule_position(w, N, ms, prof):
     if not prof:
         return None
     fl = by = 0.0
+    fused = "out_err" in prof
     for name, (tot, n_l) in prof.items():
-        wk = kernel_work(w, name, n_l, N, w.epochs)
+        wk = kernel_work(w, name, n_l, N, w.epochs, fused)
         if wk is None:
             continue
         fl += wk[0] * n_l
@@ -340,7 +359,7 @@ def main():
     if dom is not None:
         tot, n_l = prof[dom]
         avg_s = tot / 1e3 / n_l
-        wk = kernel_work(w, dom, n_l, N, w.epochs)
+        wk = kernel_work(w, dom, n_l, N, w.epochs, "out_err" in prof)
         if wk is not None:
             flops, byts = wk
             # the bound is the roof the kernel's arithmetic intensity reaches first: the matrix

@@ -208,9 +208,15 @@ int32_t pnn_profile_read(pnn_net* net, const char** names, double* total_ms, int
  *                           sizes[0] % 16 == 0 and <= 832, H <= 512: one launch per epoch for
  *                           each group of CNs whose ceil(H / 16) (or ceil(H / 32)) tile
  *                           workgroups fit the device at once;
+ *  "mini-batch fused last layer"  fp32, one hidden layer of >= 256 neurons (a multiple of
+ *                           4), B = 128, <= 16 outputs, sizes[0] >= 128 (a multiple of 4),
+ *                           the split-bf16 products (not PNN_GEMM=fp32): kernel launches per
+ *                           batch step, with the last layer's forward in the hidden layer's
+ *                           forward and its hidden errors and update in the hidden layer's
+ *                           update (one pass less over the hidden activations);
  *  "mini-batch"             kernel launches per layer and batch step.
  * The environment variable PNN_MB_PLAN=launch, read by pnn_init, selects "mini-batch"
- * where "mini-batch persistent" would apply.  The persistent plans' workgroups wait for each
+ * where "mini-batch persistent" or "mini-batch fused last layer" would apply.  The persistent plans' workgroups wait for each
  * other with bounded polls (PNN_SPIN_LIMIT, read by pnn_init, default 4194304 polls); a launch
  * that runs into the bound ends every workgroup and leaves the CNs' parameters unspecified.
  * The next call that consumes the CNs -- pnn_merge, pnn_merge_weighted, pnn_infer, pnn_eval,

@@ -161,6 +161,17 @@ struct GemmArgs {
     float lr;
     int scale_per_batch;    // EPI_UPD: scale = lr / valid (1) or lr (0)
     bf16_t* shadow;         // EPI_UPD: bf16 copy of the updated target (+ z * c_z), nullable
+    // a narrow last layer (O2 <= 16 neurons, fp32) fused around this hidden layer's products:
+    //   forward (gemm256x3_kernel): partial output sums of each 256-column tile into zpart;
+    //   update (upd128x3_kernel): A is the hidden activations, the hidden errors are formed
+    //   from dout and the pre-update W2, and W2 / b2 take their own update.
+    float* w2;              // W2 [O2][N or M] (+ z * w2_z), fp32 master; nullable (not fused)
+    float* b2;              // b2 [O2] (+ z * bias_z)
+    int64_t w2_z;
+    float* zpart;           // [z][column tiles][M][16] partial sums of the last layer, nullable
+    const float* dout;      // [z][step rows][16] output errors, nullable
+    int o2;                 // O2
+    int act2;               // update: activation of this hidden layer (its derivative)
 };
 
 template <bool BF> struct GemmTile;
@@ -1375,29 +1386,111 @@ __global__ __launch_bounds__(B3_THREADS) void gemm256x3_kernel(GemmArgs g) {
         step(k0 + B3_BK, na, nb0, nb1, ra, rb0, rb1);
     }
     const bool vec = ((g.c_ld | g.c_z | g.bias_z) & 3) == 0;
+    if constexpr (EPI == EPI_FWD) {
+        // fused last layer: this lane's W2 values (output rl, the lane's 16 columns), loaded
+        // before the activations so that their latency hides behind them
+        float4 w2v[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) w2v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (g.zpart != nullptr && rl < g.o2) {
+            const float* w2 = g.w2 + (size_t)cn * g.w2_z + (size_t)rl * g.N;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int m = m0 + wm * 64 + i * 16 + rl, n = n0 + wn * 64 + j * 16 + kg * 4;
-            if (m >= Mv || n >= Nv) continue;
-            const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
-            const f4 v = acc[i][j];
-            if constexpr (EPI == EPI_FWD) {
+            for (int j = 0; j < 4; ++j) {
+                const int n = n0 + wn * 64 + j * 16 + kg * 4;
+                if (n + 3 < Nv) w2v[j] = *(const float4*)(w2 + n);
+                else {
+                    if (n < Nv) w2v[j].x = w2[n];
+                    if (n + 1 < Nv) w2v[j].y = w2[n + 1];
+                    if (n + 2 < Nv) w2v[j].z = w2[n + 2];
+                }
+            }
+        }
+        // the activations, in place (columns past N zero), then stored
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = n0 + wn * 64 + j * 16 + kg * 4;
                 const float* bb = g.bias + (size_t)cn * g.bias_z + n;
                 if (vec && n + 3 < Nv) {
                     const float4 b4 = *(const float4*)bb;
-                    *(float4*)((float*)g.c + ci) = make_float4(act_fn(g.act, v[0] + b4.x), act_fn(g.act, v[1] + b4.y),
-                                                               act_fn(g.act, v[2] + b4.z), act_fn(g.act, v[3] + b4.w));
+                    acc[i][j][0] = act_fn(g.act, acc[i][j][0] + b4.x);
+                    acc[i][j][1] = act_fn(g.act, acc[i][j][1] + b4.y);
+                    acc[i][j][2] = act_fn(g.act, acc[i][j][2] + b4.z);
+                    acc[i][j][3] = act_fn(g.act, acc[i][j][3] + b4.w);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[i][j][r] = n + r < Nv ? act_fn(g.act, acc[i][j][r] + bb[r]) : 0.f;
+                }
+            }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int m = m0 + wm * 64 + i * 16 + rl, n = n0 + wn * 64 + j * 16 + kg * 4;
+                if (m >= Mv || n >= Nv) continue;
+                const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+                const f4 v = acc[i][j];
+                if (vec && n + 3 < Nv) {
+                    *(float4*)((float*)g.c + ci) = make_float4(v[0], v[1], v[2], v[3]);
                 } else {
                     for (int r = 0; r < 4; ++r)
-                        if (n + r < Nv) ((float*)g.c)[ci + r] = act_fn(g.act, v[r] + bb[r]);
+                        if (n + r < Nv) ((float*)g.c)[ci + r] = v[r];
                 }
-            } else {
+            }
+        if (g.zpart != nullptr) {
+            // fused last layer: this tile's share of z2[m][o] = sum_n h[m][n] W2[o][n] on
+            // v_mfma_f32_16x16x4_f32.  The activations are already in the A operand's layout:
+            // for block (i, j) and component r, lane (rl, kg) holds h[row 16 i + rl][column
+            // 16 j + 4 kg + r], i.e. A[rl][kg] of a 16 x 4 slice; B[kg][o = rl] is W2 at the
+            // same column.  The 16 slices of each row block accumulate in (j, r) order, then the
+            // four waves of a row block (wn) are added in order through LDS (free after the
+            // loop's last barrier).
+            float* red = (float*)g2s;   // [wn][128 rows][16]
+            f4 zacc[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) zacc[i] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float4 wv = w2v[j];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    zacc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[i][j][0], wv.x, zacc[i], 0, 0, 0);
+                    zacc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[i][j][1], wv.y, zacc[i], 0, 0, 0);
+                    zacc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[i][j][2], wv.z, zacc[i], 0, 0, 0);
+                    zacc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[i][j][3], wv.w, zacc[i], 0, 0, 0);
+                }
+            }
+            // lane (rl, kg) holds z2 partial [row 16 i + 4 kg + r][output rl]
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) red[(wn * 128 + wm * 64 + i * 16 + kg * 4 + r) * 16 + rl] = zacc[i][r];
+            __syncthreads();
+            const int ntile = (g.N + 255) / 256;
+            for (int e = tid; e < 128 * 16; e += B3_THREADS) {
+                const int row = e >> 4, o = e & 15;
+                if (m0 + row >= g.M) continue;
+                float v = 0.f;
+                if (o < g.o2)
+                    v = ((red[row * 16 + o] + red[(128 + row) * 16 + o]) + red[(256 + row) * 16 + o]) +
+                        red[(384 + row) * 16 + o];
+                g.zpart[(((size_t)zz * ntile + bx) * g.M + m0 + row) * 16 + o] = v;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int m = m0 + wm * 64 + i * 16 + rl, n = n0 + wn * 64 + j * 16 + kg * 4;
+                if (m >= Mv || n >= Nv) continue;
+                const size_t ci = (size_t)zz * g.c_z + (size_t)m * g.c_ld + n;
+                const f4 v = acc[i][j];
                 for (int r = 0; r < 4; ++r)
                     if (n + r < Nv) ((float*)g.c)[ci + r] = v[r];
             }
-        }
+    }
 }
 
 // ------------------------------------------------------------------------------------
@@ -1485,8 +1578,85 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     B3Raw ra, na;
     xload(ra, 0);
 
-    // the strip's errors: 2 samples x 4 rows per thread and pass, split into the planes
-    {
+    // fused last layer: A holds the hidden activations x; the strip's errors are formed here,
+    // d[s][m] = (sum_o dout[s][o] W2[o][m]) phi'(x[s][m]) with the pre-update W2 (eq. (11)),
+    // and W2[o][m] -= scale sum_s dout[s][o] x[s][m] for the strip's columns (eq. (12)), both
+    // on v_mfma_f32_16x16x4_f32: wave w owns rows 16 w .. 16 w + 15 of the strip, in 16 x 16
+    // blocks of (samples, rows); dout and the strip's columns of W2 are staged in the second
+    // input stage (free until the loop)
+    if (g.dout != nullptr) {
+        constexpr int FDS = 17, FWS = 144;       // row strides (bank spread of the reads)
+        float* f_d = (float*)(xst + 3 * B3_PLANE);   // [128 samples][FDS]: dout
+        float* f_w = f_d + U3_KMAX * FDS;            // [16 outputs][FWS]: W2[o][m0 + m]
+        // this lane's activations: x[s = 16 sb + 4 kg + r][m0 + 16 w + rl] (zero past the samples
+        // and past M)
+        const int mloc = 16 * wave + rl;
+        const bool mval = m0 + mloc < Mv;
+        const float* xrow = (const float*)operand_row(g.a, 4, zz, cn, xbase, 0) + m0 + mloc;
+        float xv[8][4];
+#pragma unroll
+        for (int sb = 0; sb < 8; ++sb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int sm = 16 * sb + 4 * kg + r;
+                xv[sb][r] = (mval && sm < Kv) ? xrow[(size_t)sm * g.a.ld] : 0.f;
+            }
+        const float* dsrc = g.dout + (size_t)zz * g.step_rows * 16;
+        for (int e = tid; e < U3_KMAX * 4; e += B3_THREADS) {
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if ((e >> 2) < g.step_rows) v = *(const float4*)(dsrc + e * 4);
+            float* d = f_d + (e >> 2) * FDS + (e & 3) * 4;
+            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+        }
+        const float* w2r = g.w2 + (size_t)cn * g.w2_z;
+        for (int e = tid; e < MAX_OUT * 32; e += B3_THREADS) {
+            const int o = e >> 5, c = (e & 31) * 4;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (o < g.o2 && m0 + c < Mv) v = *(const float4*)(w2r + (size_t)o * g.M + m0 + c);
+            *(float4*)(f_w + o * FWS + c) = v;
+        }
+        __syncthreads();
+        const int nq = (g.o2 + 3) >> 2;   // 4-output steps of the contraction over outputs
+        f4 dacc = f4{0.f, 0.f, 0.f, 0.f};  // dW2[o = 4 kg + r][m = 16 w + rl]
+#pragma unroll
+        for (int sb = 0; sb < 8; ++sb) {
+            // S[s = 16 sb + 4 kg + r][m = 16 w + rl]: A[s][o] = dout, B[o][m] = W2
+            f4 sacc = f4{0.f, 0.f, 0.f, 0.f};
+            for (int q = 0; q < nq; ++q)
+                sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(f_d[(16 * sb + rl) * FDS + 4 * q + kg],
+                                                            f_w[(4 * q + kg) * FWS + mloc], sacc, 0, 0, 0);
+            // dW2 += dout^T x over this block's samples: A[o][s] = dout, B[s][m] = x
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(f_d[(16 * sb + 4 * kg + r) * FDS + rl], xv[sb][r], dacc, 0, 0, 0);
+            // the errors, split; sample pairs (r 0, 1) and (r 2, 3)
+#pragma unroll
+            for (int pr = 0; pr < 2; ++pr) {
+                const float d0 = sacc[2 * pr] * act_deriv(g.act2, xv[sb][2 * pr]);
+                const float d1 = sacc[2 * pr + 1] * act_deriv(g.act2, xv[sb][2 * pr + 1]);
+                uint32_t h, m, l;
+                split3_pk(d0, d1, h, m, l);
+                const int o = u3_off(mloc, 16 * sb + 4 * kg + 2 * pr);
+                *(uint32_t*)(dpl + o) = h;
+                *(uint32_t*)(dpl + U3_DPLANE + o) = m;
+                *(uint32_t*)(dpl + 2 * U3_DPLANE + o) = l;
+            }
+        }
+        // W2's strip columns (the staged copy holds the pre-update values: a store, no read back)
+        float* w2w = g.w2 + (size_t)cn * g.w2_z;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int o = 4 * kg + r;
+            if (o < g.o2 && mval) w2w[(size_t)o * g.M + m0 + mloc] = f_w[o * FWS + mloc] - scale * dacc[r];
+        }
+        // b2 (the first strip): sum over the samples in order
+        if (m0 == 0 && tid < g.o2) {
+            float sb = 0.f;
+            for (int r = 0; r < Kv; ++r) sb += f_d[r * FDS + tid];
+            g.b2[(size_t)cn * g.bias_z + tid] -= scale * sb;
+        }
+    } else {
+        // the strip's errors: 2 samples x 4 rows per thread and pass, split into the planes
         const B3Src ds = b3_src<false>(g.a, zz, cn, xbase, m0, Mv, Kv);
 #pragma unroll
         for (int pass = 0; pass < U3_KMAX * 128 / (8 * B3_THREADS); ++pass) {
@@ -1511,14 +1681,22 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     for (int u = 0; u < 2; ++u) b3_store_part<false>(xst, ra, u, tid);
     xload(ra, 2);
     __syncthreads();
-    // the bias gradient (h + m + l is delta exactly)
-    if (g.ubias != nullptr && tid < 128) {
+    // the bias gradient (h + m + l is delta exactly): four lanes per row, 32 samples each read
+    // as four 16-byte chunks per plane, then the lanes' sums added in a fixed order
+    if (g.ubias != nullptr) {
+        const int r = tid >> 2, part = tid & 3;
         float sr = 0.f;
-        for (int k = 0; k < U3_KMAX; ++k) {
-            const int o = u3_off(tid, k);
-            sr += (bf2f(dpl[o]) + bf2f(dpl[U3_DPLANE + o])) + bf2f(dpl[2 * U3_DPLANE + o]);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int o = u3_off(r, part * 32 + c * 8);
+            const bf8v h = *(const bf8v*)(dpl + o), m = *(const bf8v*)(dpl + U3_DPLANE + o),
+                       l = *(const bf8v*)(dpl + 2 * U3_DPLANE + o);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sr += ((float)h[e] + (float)m[e]) + (float)l[e];
         }
-        if (m0 + tid < Mv) g.ubias[(size_t)cn * g.bias_z + m0 + tid] -= scale * sr;
+        sr += __shfl_xor(sr, 1);
+        sr += __shfl_xor(sr, 2);
+        if (part == 0 && m0 + r < Mv) g.ubias[(size_t)cn * g.bias_z + m0 + r] -= scale * sr;
     }
 
     f4 acc[4][2];
@@ -1906,6 +2084,68 @@ __global__ __launch_bounds__(256) void fwd_reduce_kernel(FwdReduceArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
+// Output activation and output error of one (row, output) lane, the 16 lanes of a row taking
+// part together (softmax over them): eq. (3) / (5) and (9) / (10); zero on dead lanes (rows
+// past the step or outputs past O); rounded to the error type TD.
+
+template <typename TD>
+__device__ inline float out_error(float zv, bool live, int o, int label, int act_out, int loss) {
+    float xo;
+    if (act_out == ACT_SOFTMAX) {
+        float m = live ? zv : -INFINITY;
+#pragma unroll
+        for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
+        const float ex = live ? expf(zv - m) : 0.f;
+        float sm = ex;
+#pragma unroll
+        for (int sh = 1; sh < 16; sh <<= 1) sm += __shfl_xor(sm, sh, 16);
+        xo = ex * (1.0f / sm);
+    } else {
+        xo = act_fn(act_out, zv);
+    }
+    if (!live) return 0.f;
+    const float t1 = (o == label) ? 1.0f : 0.0f;
+    const float dd = (loss == LOSS_XENT) ? (xo - t1) : (xo - t1) * act_deriv(act_out, xo);
+    return to_f<TD>(from_f<TD>(dd));
+}
+
+// The last layer's outputs and errors when its products are fused into the hidden layer's
+// split-bf16 kernels: z2 = sum of the forward tiles' partial sums (tile order) + b2, then the
+// output error of each row, one lane per (row, output), into dout [z][rows][16] (zeros past O
+// and past the CN's rows).
+
+struct OutErrArgs {
+    const float* zpart;   // [z][ntile][step rows][16]
+    int ntile;
+    const float* bias;    // b2 (+ z * bias_z)
+    int64_t bias_z;
+    int O, act_out, loss;
+    int64_t n_total;
+    int k_rep;
+    int64_t r0;
+    int step_rows;
+    const int32_t* y;     // labels (data-set rows)
+    float* dout;          // [z][step rows][16]
+};
+
+__global__ __launch_bounds__(256) void out_err_kernel(OutErrArgs a) {
+    const int z = blockIdx.z, row = blockIdx.x * 16 + (threadIdx.x >> 4), o = threadIdx.x & 15;
+    if (row >= a.step_rows) return;   // (a whole row's 16 lanes)
+    const int64_t v = shard_len(a.n_total, a.k_rep, z) - a.r0;
+    const int valid = (int)(v < 0 ? 0 : (v > a.step_rows ? a.step_rows : v));
+    const bool live = row < valid && o < a.O;
+    float zv = 0.f;
+    if (live) {
+        const float* zp = a.zpart + ((size_t)z * a.ntile * a.step_rows + row) * 16 + o;
+        float sum = zp[0];
+        for (int t = 1; t < a.ntile; ++t) sum += zp[(size_t)t * a.step_rows * 16];
+        zv = sum + a.bias[(size_t)z * a.bias_z + o];
+    }
+    const int label = row < valid ? a.y[shard_start(a.n_total, a.k_rep, z) + a.r0 + row] : -1;
+    a.dout[((size_t)z * a.step_rows + row) * 16 + o] = out_error<float>(zv, live, o, label, a.act_out, a.loss);
+}
+
+// ------------------------------------------------------------------------------------
 // The narrow last layer of a mini-batch step, fused, one workgroup of 16 waves per CN
 // (eq. (3)-(5), (9)-(13) for a last layer of O <= 16 neurons behind a hidden layer of H
 // neurons).  The step's rows are taken in groups of RG rows; each group is loaded once,
@@ -2058,26 +2298,7 @@ __global__ __launch_bounds__(TAIL_THREADS) void tail_kernel(TailArgs a) {
                 for (int kp = 1; kp < KP; ++kp) s += part[(kp * nt * 16 + r) * 16 + eo];
                 zv = s + bo;
             }
-            float xo;
-            if (a.act_out == ACT_SOFTMAX) {
-                float m = live ? zv : -INFINITY;
-#pragma unroll
-                for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
-                const float ex = live ? expf(zv - m) : 0.f;
-                float sm = ex;
-#pragma unroll
-                for (int sh = 1; sh < 16; sh <<= 1) sm += __shfl_xor(sm, sh, 16);
-                xo = ex * (1.0f / sm);
-            } else {
-                xo = act_fn(a.act_out, zv);
-            }
-            float dv = 0.f;
-            if (live) {
-                const float t1 = (eo == yl[r]) ? 1.0f : 0.0f;
-                const float dd = (a.loss == LOSS_XENT) ? (xo - t1) : (xo - t1) * act_deriv(a.act_out, xo);
-                dv = to_f<TH>(from_f<TH>(dd));
-            }
-            dl[r * TAIL_DLS + eo] = dv;
+            dl[r * TAIL_DLS + eo] = out_error<TH>(zv, live, eo, live ? yl[r] : -1, a.act_out, a.loss);
         }
         __syncthreads();
         if (tid < O)

@@ -123,6 +123,11 @@ struct pnn_net {
     // fp32 products of the large GEMMs on the bf16 matrix cores (three-part split); false:
     // fp32 matrix instructions throughout (PNN_GEMM=fp32, read by pnn_init)
     bool gemm_x3 = true;
+    // mini-batch plan with the last layer fused into the split-bf16 products of one hidden
+    // layer: output-sum partials [K][ceil(H / 256)][B][16], output errors [K][B][16]
+    bool fx3 = false;
+    float* fx3_zpart = nullptr;
+    float* fx3_dout = nullptr;
     // bounded waits of the persistent kernels: polls before giving up; and a test hook that
     // makes their waits run into that bound (the mini-batch kernel's readers wait for share
     // tags that are never written, the per-sample kernel's for more tiles than exist)
@@ -362,6 +367,8 @@ pnn_status run_gemm(pnn_net* n, hipStream_t s, const GemmArgs& g, int Z, const c
                 return l.done();
             }
         }
+        if (g.zpart != nullptr || g.dout != nullptr)
+            return fail(n, PNN_EINVAL, "%s: the fused last layer needs the split-bf16 kernels for this shape", name);
         // other large fp32 shapes: 128 x 128 tiles on the bf16 matrix cores, each fp32 operand
         // split into three bf16 parts (gemm128x3_kernel)
         if (n->gemm_x3 && g.M >= 128 && g.N >= 128 && g.shadow == nullptr && (g.ksplit == 1 || g.kchunk % B3_BK == 0)) {
@@ -413,6 +420,7 @@ template <bool BF>
 pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t N, int64_t r0, hipStream_t s) {
     typedef typename std::conditional<BF, bf16_t, float>::type TH;  // hidden activations / errors
     const int L = n->L, B = n->cfg.batch, K = n->cfg.replicas;
+    const bool fx3 = !BF && n->fx3;  // last layer fused into the split-bf16 products
     const int64_t ps = n->pstride;
     const void* Wop = BF ? (const void*)n->shadow : (const void*)n->theta;  // operand weights
     const int64_t wz = ps;
@@ -443,15 +451,33 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
             TRY(lr.done());
             continue;
         }
+        if (fx3) {
+            g.w2 = n->theta + n->off_w[1]; g.w2_z = ps;
+            g.zpart = n->fx3_zpart; g.o2 = n->sizes[2];
+        }
         if (l == 1) TRY((run_gemm<BF, float, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
         else TRY((run_gemm<BF, TH, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
+    }
+    if (fx3) {
+        // the last layer's outputs and errors from the forward tiles' partial sums
+        OutErrArgs a;
+        memset(&a, 0, sizeof a);
+        a.zpart = n->fx3_zpart; a.ntile = (n->sizes[1] + 255) / 256;
+        a.bias = n->theta + n->off_b[1]; a.bias_z = ps;
+        a.O = n->sizes[2]; a.act_out = n->act[1]; a.loss = n->cfg.loss;
+        a.n_total = N; a.k_rep = K; a.r0 = r0; a.step_rows = B;
+        a.y = Y;
+        a.dout = n->fx3_dout;
+        Launch lc(n, s, "out_err");
+        out_err_kernel<<<dim3((B + 15) / 16, 1, K), 256, 0, s>>>(a);
+        TRY(lc.done());
     }
     // a narrow last layer behind a hidden layer: forward, output error, the hidden error
     // behind it and its update in one kernel per CN
     const int Hl = L >= 2 ? n->sizes[L - 1] : 0;
     const int trg = tail_rows(Hl, B);
     const size_t tail_smem = trg > 0 ? (size_t)tail_lds_floats(Hl, trg) * sizeof(float) : 0;
-    const bool fuse_tail = L >= 2 && n->sizes[L] <= MAX_OUT && trg > 0 && tail_smem <= 160 * 1024;
+    const bool fuse_tail = !fx3 && L >= 2 && n->sizes[L] <= MAX_OUT && trg > 0 && tail_smem <= 160 * 1024;
     if (fuse_tail) {
         TailArgs a;
         memset(&a, 0, sizeof a);
@@ -474,7 +500,7 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
         TRY(lc.done());
     }
     // output layer and output error (eq. (3), (5), (9)-(10))
-    if (!fuse_tail) {
+    if (!fuse_tail && !fx3) {
         RowArgs a;
         memset(&a, 0, sizeof a);
         if (L == 1) { a.x = X; a.x_xrows = 1; a.x_ld = n->sizes[0]; }
@@ -493,7 +519,7 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
     }
     // hidden errors, back to front, with the pre-update weights (eq. (11))
     for (int l = L - 1; l >= 1; --l) {
-        if (fuse_tail && l == L - 1) continue;  // (in the fused last layer)
+        if ((fuse_tail || fx3) && l == L - 1) continue;  // (in the fused last layer)
         const int Hl = n->sizes[l], On = n->sizes[l + 1];
         if (On <= MAX_OUT) {
             BwdSmallArgs a;
@@ -519,7 +545,7 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
     }
     // updates, eq. (12)-(13) averaged over the batch
     for (int l = 1; l <= L; ++l) {
-        if (fuse_tail && l == L) continue;  // (in the fused last layer)
+        if ((fuse_tail || fx3) && l == L) continue;  // (in the fused last layer)
         const int In = n->sizes[l - 1], Out = n->sizes[l];
         if (Out <= MAX_OUT) {
             UpdSmallArgs a;
@@ -546,6 +572,13 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
             g.ubias = n->theta + n->off_b[l - 1]; g.bias_z = ps;
             g.lr = n->cfg.lr; g.scale_per_batch = 1;
             g.shadow = BF ? n->shadow + n->off_w[l - 1] : nullptr;
+            if (fx3) {
+                // A: the hidden activations; the errors are formed from the output errors
+                g.a = opnd(n->act_ws[1], (int64_t)B * Out, Out, 0);
+                g.dout = n->fx3_dout;
+                g.w2 = n->theta + n->off_w[1]; g.b2 = n->theta + n->off_b[1]; g.w2_z = ps;
+                g.o2 = n->sizes[2]; g.act2 = n->act[0];
+            }
             if (l == 1) TRY((run_gemm<BF, TH, float, false, false, EPI_UPD, float>(n, s, g, K, "upd_gemm")));
             else TRY((run_gemm<BF, TH, TH, false, false, EPI_UPD, float>(n, s, g, K, "upd_gemm")));
         }
@@ -825,7 +858,7 @@ void free_all(pnn_net* n) {
     auto f = [](void* p) { if (p) (void)hipFree(p); };
     f(n->theta); f(n->merged); f(n->shadow); f(n->mshadow);
     for (int l = 0; l < 9; ++l) { f(n->act_ws[l]); f(n->del_ws[l]); f(n->inf_ws[l]); }
-    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ord_x); f(n->ord_y); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx); f(n->zpart);
+    f(n->d_correct); f(n->d_cost); f(n->d_cost_sum); f(n->d_mw); f(n->ord_x); f(n->ord_y); f(n->ppart); f(n->d1); f(n->gram); f(n->flags); f(n->qbuf); f(n->gramx); f(n->zpart); f(n->fx3_zpart); f(n->fx3_dout);
     if (n->abort_ev) (void)hipEventDestroy(n->abort_ev);
     for (auto& r : n->pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : n->free_events) (void)hipEventDestroy(e);
@@ -1091,6 +1124,20 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
                     if ((st = dev_alloc(n, &n->flags, (size_t)(K + 1))) != PNN_OK) return bail(st);
                 }
             }
+        }
+        // the last layer fused into the split-bf16 products of one hidden layer (fp32, batches
+        // of 128 rows, a hidden width of >= 256 neurons, <= 16 outputs): gemm256x3_kernel's
+        // epilogue writes the output sums' partials, out_err_kernel the output errors and
+        // upd128x3_kernel forms the hidden errors and updates W2 and b2 (no pass over the
+        // hidden layer's activations and errors of its own); PNN_MB_PLAN=launch keeps the
+        // separate last-layer kernel
+        if (!forced_launch && !n->mbp && !n->bf16 && n->gemm_x3 && n->L == 2 && B == 128 && n->ksplit == 1 &&
+            n->sizes[1] >= 256 && n->sizes[1] % 4 == 0 && n->sizes[2] <= MAX_OUT && n->sizes[0] >= 128 &&
+            n->sizes[0] % 4 == 0 && n->off_w[1] % 4 == 0 && n->off_b[1] % 4 == 0 && n->pstride % 4 == 0) {
+            const size_t ntile = (size_t)(n->sizes[1] + 255) / 256;
+            if ((st = dev_alloc(n, &n->fx3_zpart, (size_t)K * ntile * B * 16)) != PNN_OK) return bail(st);
+            if ((st = dev_alloc(n, &n->fx3_dout, (size_t)K * B * 16)) != PNN_OK) return bail(st);
+            n->fx3 = true;
         }
         // the fused last layer may stage up to 160 KiB of LDS
         const void* tk[3] = {(const void*)tail_kernel<float, 1>, (const void*)tail_kernel<float, 2>,
@@ -1401,7 +1448,7 @@ pnn_status pnn_eval_noalloc(pnn_net* n, int32_t which, const float* x_dev, const
 const char* pnn_plan(const pnn_net* n) {
     if (!n) return "";
     if (n->psgd) return n->persistent ? "per-sample persistent" : "per-sample chunked";
-    return n->mbp ? "mini-batch persistent" : "mini-batch";
+    return n->mbp ? "mini-batch persistent" : n->fx3 ? "mini-batch fused last layer" : "mini-batch";
 }
 
 pnn_status pnn_get_params(pnn_net* n, int32_t which, float* host_out) {

@@ -16,6 +16,10 @@ EPOCH_CASES = [
     (3, dict(replicas=8), 8 * 150 + 3, 2),                    # bf16, merge + broadcast each epoch
     (4, dict(replicas=16), 16 * 260 + 7, 2),                  # batches 128,128,4/5, merge each epoch
     (4, dict(replicas=4), 4 * 224 + 2, 2),                    # batches 128, 97/96 (one launch, zero padded)
+    # the fused last layer with softmax / cross-entropy over 16 outputs (tanh hidden layer), and
+    # with a single sigmoid output; batches 128 + 72/73 and 128 + 5/6
+    (4, dict(sizes=(784, 256, 16), acts=(I.TANH, I.SOFTMAX), loss=I.LOSS_XENT, replicas=3), 3 * 200 + 1, 1),
+    (4, dict(sizes=(784, 320, 1), replicas=2), 2 * 134 + 1, 1),
     (2, dict(sizes=(784, 64, 32, 10), acts=(I.RELU, I.TANH, I.SOFTMAX), loss=I.LOSS_XENT, batch=16,
              replicas=2, merge_every_epoch=True), 2 * 90 + 1, 2),   # deeper fp32 net
     (0, dict(sizes=(784, 32, 16, 10), acts=(I.TANH, I.SIGMOID, I.SIGMOID), replicas=2), 2 * 40, 1),  # B=1, L=3

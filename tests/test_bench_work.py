@@ -46,6 +46,22 @@ def test_minibatch_bytes_cover_every_weight_pass(idx):
     assert total >= K * bsteps * weights * 8.0
 
 
+def test_fused_last_layer_kernels_cover_the_method():
+    # plan "mini-batch fused last layer" (784-1024-10, K = 256, B = 128): the forward, out_err and
+    # update kernels together carry the last layer's multiply-adds that the separate kernel
+    # would (the output errors' own flops aside), and its weight and activation passes
+    w = I.WORKLOADS[4]
+    s, K, N, E = w.sizes, w.replicas, w.n_train, w.epochs
+    fused = sum(bench.kernel_work(w, n, 1, N, E, True)[0] for n in ("fwd_gemm", "upd_gemm"))
+    plain = sum(bench.kernel_work(w, n, 1, N, E)[0] for n in ("fwd_gemm", "bwd_gemm", "upd_gemm", "tail"))
+    assert fused == pytest.approx(plain, rel=1e-12)
+    bsteps = -(-(-(-N // K)) // w.batch) * E
+    b = sum(bench.kernel_work(w, n, 1, N, E, True)[1] for n in ("fwd_gemm", "out_err", "upd_gemm"))
+    weights = sum(s[l] * s[l + 1] for l in range(len(s) - 1))
+    assert b >= K * bsteps * weights * 8.0
+    assert bench.kernel_work(w, "out_err", 1, N, E)[0] == N * E * s[-1]
+
+
 def test_persistent_minibatch_effective_bytes():
     # one launch = one epoch: every batch step of every CN would read and write every parameter
     # once in a streaming implementation, and every input row is read once

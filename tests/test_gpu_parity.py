@@ -245,7 +245,10 @@ PLAN_CASES = [
     (2, dict(sizes=(784, 1024, 10)), "mini-batch"),           # 64 tiles of 16 neurons per CN
     (2, dict(batch=33), "mini-batch"),
     (3, dict(replicas=8), "mini-batch"),                      # bf16, two hidden layers
-    (4, dict(replicas=4), "mini-batch"),
+    (4, dict(replicas=4), "mini-batch fused last layer"),
+    (4, dict(sizes=(784, 256, 16), acts=(I.TANH, I.SOFTMAX), loss=I.LOSS_XENT), "mini-batch fused last layer"),
+    (4, dict(sizes=(784, 192, 10)), "mini-batch"),            # hidden width below 256
+    (4, dict(batch=64), "mini-batch"),                        # batch other than 128
 ]
 
 
@@ -257,19 +260,20 @@ def test_plan_selection(idx, over, plan, monkeypatch):
     net.close()
     monkeypatch.setenv("PNN_MB_PLAN", "launch")
     net = make_net(w, I.init_params(w))
-    assert net.plan == ("mini-batch" if plan == "mini-batch persistent" else plan)
+    assert net.plan == ("mini-batch" if plan in ("mini-batch persistent", "mini-batch fused last layer") else plan)
     net.close()
 
 
-@pytest.mark.parametrize("over,N,epochs", [
-    ({}, 16 * 100 + 5, 2),
-    (dict(sizes=(784, 56, 10), acts=(I.SIGMOID, I.SIGMOID), batch=7, replicas=5), 5 * 40 + 3, 1),
+@pytest.mark.parametrize("idx,over,N,epochs", [
+    (2, {}, 16 * 100 + 5, 2),
+    (2, dict(sizes=(784, 56, 10), acts=(I.SIGMOID, I.SIGMOID), batch=7, replicas=5), 5 * 40 + 3, 1),
+    (4, dict(replicas=4), 4 * 224 + 2, 1),     # the separate last-layer kernel behind the split-bf16 products
 ])
-def test_epochs_launch_plan(over, N, epochs, monkeypatch):
+def test_epochs_launch_plan(idx, over, N, epochs, monkeypatch):
     """The per-layer launch plan on nets that would otherwise get the persistent mini-batch
-    kernel, against the oracle."""
+    kernel or the fused last layer, against the oracle."""
     monkeypatch.setenv("PNN_MB_PLAN", "launch")
-    w = I.WORKLOADS[2].scaled(**over)
+    w = I.WORKLOADS[idx].scaled(**over)
     X, y = I.train_set(w, N)
     th0 = I.init_params(w)
     net = make_net(w, th0)
