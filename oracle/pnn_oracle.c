@@ -310,9 +310,9 @@ void or_train_replicas(const or_config* c, double* theta_sub, const int32_t* ids
     }
 }
 
-/* Combination by averaging (section "Implementation Details": the weights and biases of the
- * child networks are added onto the PNN and then scaled by the number of child networks).
- * Summation in long double, k ascending, then the division by K. */
+/* Combination by averaging (section "Implementation Details"): each parameter of the
+ * combined network is the sum of the K child networks' values divided by K.  Summation in long
+ * double, k ascending, then the division by K. */
 void or_merge(const or_config* c, const double* theta, double* merged)
 {
     const int64_t P = or_param_count(c);
