@@ -1447,6 +1447,7 @@ __global__ __launch_bounds__(B3_THREADS) void gemm256x3_kernel(GemmArgs g) {
             // four waves of a row block (wn) are added in order through LDS (free after the
             // loop's last barrier).
             float* red = (float*)g2s;   // [wn][128 rows][16]
+            static_assert(4 * 128 * 16 * sizeof(float) <= g2_lds_bytes(), "the partial sums fit the LDS stages");
             f4 zacc[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) zacc[i] = f4{0.f, 0.f, 0.f, 0.f};
@@ -1505,7 +1506,10 @@ __global__ __launch_bounds__(B3_THREADS) void gemm256x3_kernel(GemmArgs g) {
 // samples' input columns x[s][n0 ..] stream through two LDS stages in k-chunks of 32 samples
 // (loaded two chunks ahead, across tile boundaries), and each finished tile's targets, loaded
 // one tile ahead, take their update and go back.  A: NC operand (rows = samples), B: NC.
-// FULL: updates over 97 .. 128 samples, four k-chunks per tile (zero padded).
+// FULL: updates over 97 .. 128 samples, four k-chunks per tile (zero padded).  With dout set
+// (the last layer fused into this layer's products), A holds the layer's activations and the
+// prologue forms the strip's errors from them, the output errors and the pre-update last-layer
+// weights, and updates the last layer's columns of this strip.
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 constexpr int U3_KMAX = 128;   // samples of one update
@@ -1586,6 +1590,8 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     // input stage (free until the loop)
     if (g.dout != nullptr) {
         constexpr int FDS = 17, FWS = 144;       // row strides (bank spread of the reads)
+        static_assert((U3_KMAX * FDS + MAX_OUT * FWS) * sizeof(float) <= 3 * B3_PLANE * sizeof(bf16_t),
+                      "dout and W2 fit the second input stage");
         float* f_d = (float*)(xst + 3 * B3_PLANE);   // [128 samples][FDS]: dout
         float* f_w = f_d + U3_KMAX * FDS;            // [16 outputs][FWS]: W2[o][m0 + m]
         // this lane's activations: x[s = 16 sb + 4 kg + r][m0 + 16 w + rl] (zero past the samples
