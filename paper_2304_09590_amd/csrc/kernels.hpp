@@ -1623,7 +1623,9 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
         }
         __syncthreads();
         const int nq = (g.o2 + 3) >> 2;   // 4-output steps of the contraction over outputs
-        f4 dacc = f4{0.f, 0.f, 0.f, 0.f};  // dW2[o = 4 kg + r][m = 16 w + rl]
+        // dW2[o = 4 kg + r][m = 16 w + rl] in two chains (even and odd sample blocks, added at the
+        // end): half the dependent matrix-instruction latency
+        f4 dacc2[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
         for (int sb = 0; sb < 8; ++sb) {
             // S[s = 16 sb + 4 kg + r][m = 16 w + rl]: A[s][o] = dout, B[o][m] = W2
@@ -1634,7 +1636,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             // dW2 += dout^T x over this block's samples: A[o][s] = dout, B[s][m] = x
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                dacc = __builtin_amdgcn_mfma_f32_16x16x4f32(f_d[(16 * sb + 4 * kg + r) * FDS + rl], xv[sb][r], dacc, 0, 0, 0);
+                dacc2[sb & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_d[(16 * sb + 4 * kg + r) * FDS + rl], xv[sb][r], dacc2[sb & 1], 0, 0, 0);
             // the errors, split; sample pairs (r 0, 1) and (r 2, 3)
 #pragma unroll
             for (int pr = 0; pr < 2; ++pr) {
@@ -1648,6 +1650,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                 *(uint32_t*)(dpl + 2 * U3_DPLANE + o) = l;
             }
         }
+        const f4 dacc = dacc2[0] + dacc2[1];
         // W2's strip columns (the staged copy holds the pre-update values: a store, no read back)
         float* w2w = g.w2 + (size_t)cn * g.w2_z;
 #pragma unroll
