@@ -1542,6 +1542,10 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
     const int nkc = FULL ? 4 : (Kv + B3_BK - 1) / B3_BK;   // k-chunks per tile
     const int ntile = (Nv + 127) / 128;
+    // the strips of a CN walk their tiles from different starting tiles (strip by from tile
+    // by mod ntile), so that the chip's target loads and stores do not all come at once
+    const int rot = FULL ? by % ntile : 0;
+    auto tcol = [&](int t) { const int u = t + rot; return (u >= ntile ? u - ntile : u) * 128; };
     const int nsteps = ntile * nkc;
     const float scale = g.scale_per_batch ? g.lr / (float)Kv : g.lr;
     float* Wz = (float*)g.c + (size_t)zz * g.c_z;
@@ -1568,16 +1572,16 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                 w[i][j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(wsrc), woff(n0, i, j), 0, 0));
     };
     float4 wcur[4][2], wnext[4][2];
-    load_w(wcur, 0);
+    load_w(wcur, tcol(0));
 
     // the input stream: step q = (tile q / nkc, k-chunk q % nkc); zeros past the last step
     auto xsrc = [&](int q) {
-        const int n0 = min(q / nkc, ntile - 1) * 128;
+        const int n0 = tcol(min(q / nkc, ntile - 1));
         return b3_src<false>(g.b, zz, cn, xbase, n0, Nv, Kv);
     };
     auto xload = [&](B3Raw& r, int q) {
         const int kc = q % nkc;
-        b3_load<false>(r, xsrc(q), q < nsteps ? Nv - min(q / nkc, ntile - 1) * 128 : 0, kc * B3_BK, Kv, tid);
+        b3_load<false>(r, xsrc(q), q < nsteps ? Nv - tcol(min(q / nkc, ntile - 1)) : 0, kc * B3_BK, Kv, tid);
     };
     B3Raw ra, na;
     xload(ra, 0);
@@ -1782,7 +1786,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             xload(xl, q + 3);
             // (unconditional: past the last tile every column is out of range, the loads read
             // nothing and give zeros, and the wait counts stay exact)
-            if (kc == 0) load_w(wx, (tn + 1) * 128);
+            if (kc == 0) load_w(wx, tn + 1 < ntile ? tcol(tn + 1) : ntile * 128);
             const bf16_t* Bt = xst + (kc & 1) * 3 * B3_PLANE;
             bf16_t* Bn = xst + ((kc & 1) ^ 1) * 3 * B3_PLANE;
             bf8v av[3][4], bv[3][2];
@@ -1805,7 +1809,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                 if (t == 1 || t == 3) b3_store_part<false>(Bn, xa, t >> 1, tid);
             }
             if (kc == 3) {
-                const int n0 = tn * 128;
+                const int n0 = tcol(tn);
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
