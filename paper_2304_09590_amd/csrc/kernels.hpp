@@ -1542,9 +1542,10 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     const int64_t xbase = shard_start(g.n_total, g.k_rep, cn) + r0;
     const int nkc = FULL ? 4 : (Kv + B3_BK - 1) / B3_BK;   // k-chunks per tile
     const int ntile = (Nv + 127) / 128;
-    // the strips of a CN walk their tiles from different starting tiles (strip by from tile
-    // by mod ntile), so that the chip's target loads and stores do not all come at once
-    const int rot = FULL ? by % ntile : 0;
+    // CN k walks its tiles from tile k mod ntile, so that the tiles updated at one time spread
+    // over memory; the strips of a CN keep one order and so still share each input chunk in L2
+    // (strip-dependent starts spread further but re-read the chunks: +22 % HBM traffic)
+    const int rot = FULL ? cn % ntile : 0;
     auto tcol = [&](int t) { const int u = t + rot; return (u >= ntile ? u - ntile : u) * 128; };
     const int nsteps = ntile * nkc;
     const float scale = g.scale_per_batch ? g.lr / (float)Kv : g.lr;
