@@ -1573,7 +1573,6 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                 w[i][j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(b3_rsrc(wsrc), woff(n0, i, j), 0, 0));
     };
     float4 wcur[4][2], wnext[4][2];
-    load_w(wcur, tcol(0));
 
     // the input stream: step q = (tile q / nkc, k-chunk q % nkc); zeros past the last step
     auto xsrc = [&](int q) {
@@ -1585,7 +1584,10 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
         b3_load<false>(r, xsrc(q), q < nsteps ? Nv - tcol(min(q / nkc, ntile - 1)) : 0, kc * B3_BK, Kv, tid);
     };
     B3Raw ra, na;
-    xload(ra, 0);
+    // the bias of this lane's row, read now (updated after the prologue without a round trip)
+    float ub_old = 0.f;
+    const bool ub_lane = g.ubias != nullptr && (tid & 3) == 0 && m0 + (tid >> 2) < Mv;
+    if (ub_lane) ub_old = g.ubias[(size_t)cn * g.bias_z + m0 + (tid >> 2)];
 
     // fused last layer: A holds the hidden activations x; the strip's errors are formed here,
     // d[s][m] = (sum_o dout[s][o] W2[o][m]) phi'(x[s][m]) with the pre-update W2 (eq. (11)),
@@ -1599,6 +1601,17 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                       "dout and W2 fit the second input stage");
         float* f_d = (float*)(xst + 3 * B3_PLANE);   // [128 samples][FDS]: dout
         float* f_w = f_d + U3_KMAX * FDS;            // [16 outputs][FWS]: W2[o][m0 + m]
+        // issue order (vector-memory completions count in order): the staged values first, then
+        // this lane's activations in the order of use, then the first target tile and input chunk
+        // (needed only after the prologue)
+        const float* dsrc = g.dout + (size_t)zz * g.step_rows * 16;
+        static_assert(U3_KMAX * 4 == B3_THREADS && MAX_OUT * 32 == B3_THREADS, "one float4 of each per thread");
+        float4 dv4 = make_float4(0.f, 0.f, 0.f, 0.f);   // dout[tid >> 2][4 (tid & 3) ..]
+        if ((tid >> 2) < g.step_rows) dv4 = *(const float4*)(dsrc + tid * 4);
+        const float* w2r = g.w2 + (size_t)cn * g.w2_z;
+        const int wo = tid >> 5, wc4 = (tid & 31) * 4;   // W2[wo][m0 + wc4 ..]
+        float4 wv4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (wo < g.o2 && m0 + wc4 < Mv) wv4 = *(const float4*)(w2r + (size_t)wo * g.M + m0 + wc4);
         // this lane's activations: x[s = 16 sb + 4 kg + r][m0 + 16 w + rl] (zero past the samples
         // and past M)
         const int mloc = 16 * wave + rl;
@@ -1612,19 +1625,12 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                 const int sm = 16 * sb + 4 * kg + r;
                 xv[sb][r] = (mval && sm < Kv) ? xrow[(size_t)sm * g.a.ld] : 0.f;
             }
-        const float* dsrc = g.dout + (size_t)zz * g.step_rows * 16;
-        for (int e = tid; e < U3_KMAX * 4; e += B3_THREADS) {
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if ((e >> 2) < g.step_rows) v = *(const float4*)(dsrc + e * 4);
-            float* d = f_d + (e >> 2) * FDS + (e & 3) * 4;
-            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-        }
-        const float* w2r = g.w2 + (size_t)cn * g.w2_z;
-        for (int e = tid; e < MAX_OUT * 32; e += B3_THREADS) {
-            const int o = e >> 5, c = (e & 31) * 4;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (o < g.o2 && m0 + c < Mv) v = *(const float4*)(w2r + (size_t)o * g.M + m0 + c);
-            *(float4*)(f_w + o * FWS + c) = v;
+        load_w(wcur, tcol(0));
+        xload(ra, 0);
+        {
+            float* d = f_d + (tid >> 2) * FDS + (tid & 3) * 4;
+            d[0] = dv4.x; d[1] = dv4.y; d[2] = dv4.z; d[3] = dv4.w;
+            *(float4*)(f_w + wo * FWS + wc4) = wv4;
         }
         __syncthreads();
         const int nq = (g.o2 + 3) >> 2;   // 4-output steps of the contraction over outputs
@@ -1670,6 +1676,8 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             g.b2[(size_t)cn * g.bias_z + tid] -= scale * sb;
         }
     } else {
+        load_w(wcur, tcol(0));
+        xload(ra, 0);
         // the strip's errors: 2 samples x 4 rows per thread and pass, split into the planes
         const B3Src ds = b3_src<false>(g.a, zz, cn, xbase, m0, Mv, Kv);
 #pragma unroll
@@ -1710,7 +1718,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
         }
         sr += __shfl_xor(sr, 1);
         sr += __shfl_xor(sr, 2);
-        if (part == 0 && m0 + r < Mv) g.ubias[(size_t)cn * g.bias_z + m0 + r] -= scale * sr;
+        if (ub_lane) g.ubias[(size_t)cn * g.bias_z + m0 + r] = ub_old - scale * sr;
     }
 
     f4 acc[4][2];
