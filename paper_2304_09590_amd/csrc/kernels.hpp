@@ -100,6 +100,21 @@ __device__ inline float act_deriv(int a, float x) {
     }
 }
 
+// Activations of the sequential per-sample steps and of the split-bf16 forward's epilogue.
+// The sigmoid runs on the hardware exp2 and
+// reciprocal (relative error below |z| * 6e-8 + 2 ulp).  tanh takes the library function:
+// written as 1 - 2 / (e^{2z} + 1) it would lose its relative accuracy near z = 0 (cancellation:
+// about 1e-4 relative at z = 1e-3), which a cross-entropy output error then amplifies.
+__device__ inline float act_fast(int a, float z) {
+    switch (a) {
+    case ACT_SIGMOID: return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+    case ACT_TANH: return tanhf(z);
+    case ACT_RELU: return z >= 0.0f ? z + 0.0f : -0.0f;
+    case ACT_LEAKY: return z >= 0.0f ? z + 0.0f : 0.01f * z;
+    default: return z;
+    }
+}
+
 __device__ inline float wave_sum(float v) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
@@ -1405,7 +1420,9 @@ __global__ __launch_bounds__(B3_THREADS) void gemm256x3_kernel(GemmArgs g) {
                 }
             }
         }
-        // the activations, in place (columns past N zero), then stored
+        // the activations, in place: bias, then the activation in one straight loop per kind (a
+        // per-element switch on the kind cost 27 us of a 360 us launch; the sigmoid on the
+        // hardware exp2 and reciprocal another 13), then zero past N
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -1414,15 +1431,36 @@ __global__ __launch_bounds__(B3_THREADS) void gemm256x3_kernel(GemmArgs g) {
                 const float* bb = g.bias + (size_t)cn * g.bias_z + n;
                 if (vec && n + 3 < Nv) {
                     const float4 b4 = *(const float4*)bb;
-                    acc[i][j][0] = act_fn(g.act, acc[i][j][0] + b4.x);
-                    acc[i][j][1] = act_fn(g.act, acc[i][j][1] + b4.y);
-                    acc[i][j][2] = act_fn(g.act, acc[i][j][2] + b4.z);
-                    acc[i][j][3] = act_fn(g.act, acc[i][j][3] + b4.w);
+                    acc[i][j][0] += b4.x; acc[i][j][1] += b4.y; acc[i][j][2] += b4.z; acc[i][j][3] += b4.w;
                 } else {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) acc[i][j][r] = n + r < Nv ? act_fn(g.act, acc[i][j][r] + bb[r]) : 0.f;
+                    for (int r = 0; r < 4; ++r) acc[i][j][r] += n + r < Nv ? bb[r] : 0.f;
                 }
             }
+        auto act_all = [&](auto A) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[i][j][r] = act_fast(decltype(A)::value, acc[i][j][r]);
+        };
+        switch (g.act) {
+        case ACT_SIGMOID: act_all(std::integral_constant<int, ACT_SIGMOID>{}); break;
+        case ACT_TANH: act_all(std::integral_constant<int, ACT_TANH>{}); break;
+        case ACT_RELU: act_all(std::integral_constant<int, ACT_RELU>{}); break;
+        case ACT_LEAKY: act_all(std::integral_constant<int, ACT_LEAKY>{}); break;
+        default: break;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + wn * 64 + j * 16 + kg * 4;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (n + r >= Nv) acc[i][j][r] = 0.f;
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -2627,20 +2665,6 @@ __device__ inline float row_allsum16(float v) {
     return v + dpp<DPP_XOR1>(v);
 }
 __device__ inline float readlane_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
-
-// Activations of the sequential per-sample steps.  The sigmoid runs on the hardware exp2 and
-// reciprocal (relative error below |z| * 6e-8 + 2 ulp).  tanh takes the library function:
-// written as 1 - 2 / (e^{2z} + 1) it would lose its relative accuracy near z = 0 (cancellation:
-// about 1e-4 relative at z = 1e-3), which a cross-entropy output error then amplifies.
-__device__ inline float act_fast(int a, float z) {
-    switch (a) {
-    case ACT_SIGMOID: return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
-    case ACT_TANH: return tanhf(z);
-    case ACT_RELU: return z >= 0.0f ? z + 0.0f : -0.0f;
-    case ACT_LEAKY: return z >= 0.0f ? z + 0.0f : 0.01f * z;
-    default: return z;
-    }
-}
 
 // ------------------------------------------------------------------------------------
 // Bounded cross-workgroup waits (device-scope release/acquire on a counter in global
