@@ -1670,6 +1670,21 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             d[0] = dv4.x; d[1] = dv4.y; d[2] = dv4.z; d[3] = dv4.w;
             *(float4*)(f_w + wo * FWS + wc4) = wv4;
         }
+        // phi'(x) of this lane's activations, one loop per kind (the kind is a launch constant)
+        float xd[8][4];
+        auto deriv_all = [&](auto A) __attribute__((always_inline)) {
+#pragma unroll
+            for (int sb = 0; sb < 8; ++sb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) xd[sb][r] = act_deriv(decltype(A)::value, xv[sb][r]);
+        };
+        switch (g.act2) {
+        case ACT_SIGMOID: deriv_all(std::integral_constant<int, ACT_SIGMOID>{}); break;
+        case ACT_TANH: deriv_all(std::integral_constant<int, ACT_TANH>{}); break;
+        case ACT_RELU: deriv_all(std::integral_constant<int, ACT_RELU>{}); break;
+        case ACT_LEAKY: deriv_all(std::integral_constant<int, ACT_LEAKY>{}); break;
+        default: deriv_all(std::integral_constant<int, -1>{}); break;
+        }
         __syncthreads();
         const int nq = (g.o2 + 3) >> 2;   // 4-output steps of the contraction over outputs
         // dW2[o = 4 kg + r][m = 16 w + rl] in two chains (even and odd sample blocks, added at the
@@ -1689,8 +1704,8 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             // the errors, split; sample pairs (r 0, 1) and (r 2, 3)
 #pragma unroll
             for (int pr = 0; pr < 2; ++pr) {
-                const float d0 = sacc[2 * pr] * act_deriv(g.act2, xv[sb][2 * pr]);
-                const float d1 = sacc[2 * pr + 1] * act_deriv(g.act2, xv[sb][2 * pr + 1]);
+                const float d0 = sacc[2 * pr] * xd[sb][2 * pr];
+                const float d1 = sacc[2 * pr + 1] * xd[sb][2 * pr + 1];
                 uint32_t h, m, l;
                 split3_pk(d0, d1, h, m, l);
                 const int o = u3_off(mloc, 16 * sb + 4 * kg + 2 * pr);
