@@ -20,6 +20,9 @@ EPOCH_CASES = [
     # with a single sigmoid output; batches 128 + 72/73 and 128 + 5/6
     (4, dict(sizes=(784, 256, 16), acts=(I.TANH, I.SOFTMAX), loss=I.LOSS_XENT, replicas=3), 3 * 200 + 1, 1),
     (4, dict(sizes=(784, 320, 1), replicas=2), 2 * 134 + 1, 1),
+    # shards of 257 and 256 samples: the third batch step has one row for two CNs and none for
+    # the other two (fused last layer with empty CNs in a step)
+    (4, dict(sizes=(784, 256, 10), replicas=4), 4 * 256 + 2, 1),
     (2, dict(sizes=(784, 64, 32, 10), acts=(I.RELU, I.TANH, I.SOFTMAX), loss=I.LOSS_XENT, batch=16,
              replicas=2, merge_every_epoch=True), 2 * 90 + 1, 2),   # deeper fp32 net
     (0, dict(sizes=(784, 32, 16, 10), acts=(I.TANH, I.SIGMOID, I.SIGMOID), replicas=2), 2 * 40, 1),  # B=1, L=3
