@@ -1690,15 +1690,17 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
         default: deriv_all(std::integral_constant<int, -1>{}); break;
         }
         __syncthreads();
-        const int nq = (g.o2 + 3) >> 2;   // 4-output steps of the contraction over outputs
         // dW2[o = 4 kg + r][m = 16 w + rl] in two chains (even and odd sample blocks, added at the
         // end): half the dependent matrix-instruction latency
         f4 dacc2[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
         for (int sb = 0; sb < 8; ++sb) {
-            // S[s = 16 sb + 4 kg + r][m = 16 w + rl]: A[s][o] = dout, B[o][m] = W2
+            // S[s = 16 sb + 4 kg + r][m = 16 w + rl]: A[s][o] = dout, B[o][m] = W2, over all 16
+            // staged outputs (those past O are zero in both: exact zeros added, and a loop of
+            // known length whose LDS reads are not each waited for in turn)
             f4 sacc = f4{0.f, 0.f, 0.f, 0.f};
-            for (int q = 0; q < nq; ++q)
+#pragma unroll
+            for (int q = 0; q < MAX_OUT / 4; ++q)
                 sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(f_d[(16 * sb + rl) * FDS + 4 * q + kg],
                                                             f_w[(4 * q + kg) * FWS + mloc], sacc, 0, 0, 0);
             // dW2 += dout^T x over this block's samples: A[o][s] = dout, B[s][m] = x
@@ -1726,10 +1728,12 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             const int o = 4 * kg + r;
             if (o < g.o2 && mval) w2w[(size_t)o * g.M + m0 + mloc] = f_w[o * FWS + mloc] - scale * dacc[r];
         }
-        // b2 (the first strip): sum over the samples in order
+        // b2 (the first strip): sum over the samples in order (rows past the step's samples
+        // hold zero errors: all 128 rows, a loop of known length)
         if (m0 == 0 && tid < g.o2) {
             float sb = 0.f;
-            for (int r = 0; r < Kv; ++r) sb += f_d[r * FDS + tid];
+#pragma unroll
+            for (int r = 0; r < U3_KMAX; ++r) sb += f_d[r * FDS + tid];
             g.b2[(size_t)cn * g.bias_z + tid] -= scale * sb;
         }
     } else {
