@@ -90,7 +90,9 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int, fused
     rows (8 O + 4) bytes; upd_gemm adds the hidden error and the last layer's update, 4 rows O H
     flops and K bsteps (8 O H + 8 O) + rows O 4 bytes (it reads the activations in place of the
     errors: the same bytes).
-    merge: reads K*P floats and writes P (and K*P with broadcast).
+    merge: reads K*P floats and writes P (and K*P with broadcast, except in the fused plan, which
+      defers the broadcast to the next epoch's first step); broadcast (a deferred copy made on
+      demand): reads P, writes K*P.
     """
     if name.endswith("_x3"):
         name = name[:-3]
@@ -103,8 +105,13 @@ def kernel_work(w, name: str, launches: int, N: int, epochs_profiled: int, fused
         bsteps_epoch = float(-(-(-(-N // K)) // w.batch))
         return N * method_flops_per_sample(w), K * bsteps_epoch * 8.0 * w.param_count() + N * 4.0 * s[0]
     if name == "merge":
+        # (with the last layer fused the broadcast is deferred: the next epoch's first step reads
+        # the merged network and writes every CN)
         P = w.param_count()
-        return 0.0, (K * P + P + (K * P if w.merge_every_epoch else 0)) * 4.0
+        return 0.0, (K * P + P + (K * P if w.merge_every_epoch and not fused_last else 0)) * 4.0
+    if name == "broadcast":
+        P = w.param_count()
+        return 0.0, (P + K * P) * 4.0
     bf = w.precision == I.BF16_MIXED
     a = 2.0 if bf else 4.0           # hidden activations and errors
     wop = 2.0 if bf else 4.0         # operand weights

@@ -122,7 +122,9 @@ pnn_status pnn_train_epoch_order(pnn_net* net, const float* x_dev, const int32_t
 /* Combination by averaging (section "Implementation Details"): merged := (1/K) sum_k theta_k
  * for every weight and bias, accumulated in fp64 with k ascending, rounded once to fp32.
  * broadcast != 0 also copies the merged network back into every CN (model averaging
- * between epochs). */
+ * between epochs); with the fused last-layer plan (pnn_plan) that copy is made by the next
+ * epoch's first step, which reads the merged network, or on demand by the first other call
+ * that reads a CN's parameters: every call sees the CNs as copied. */
 pnn_status pnn_merge(pnn_net* net, int32_t broadcast, void* hip_stream);
 
 /* Weighted combination: the paper notes that CNs can be combined in several ways and leaves

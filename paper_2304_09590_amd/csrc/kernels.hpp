@@ -187,6 +187,13 @@ struct GemmArgs {
     const float* dout;      // [z][step rows][16] output errors, nullable
     int o2;                 // O2
     int act2;               // update: activation of this hidden layer (its derivative)
+    // update with the last layer fused, in the first step after a merge whose copy into the
+    // CNs was deferred: W, W2, b and b2 are read from these (the merged network: one slot, no
+    // CN stride) and the update is written to the CN's own (all nullable)
+    const float* rd_c;
+    const float* rd_w2;
+    const float* rd_ub;
+    const float* rd_b2;
 };
 
 template <bool BF> struct GemmTile;
@@ -1596,11 +1603,13 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     // the strip's targets through a buffer descriptor (rows past M and columns past N out of
     // range: loads give zero, stores are dropped; no branch, exact wait counters).  N and the
     // row stride are multiples of 4, so a valid float4 never crosses N.
-    B3Src wsrc;
+    B3Src wsrc, wdst;   // where the targets are read, and written
     {
-        wsrc.base = (uint64_t)(Wz + (size_t)m0 * g.c_ld);
+        wsrc.base = (uint64_t)((g.rd_c != nullptr ? g.rd_c : Wz) + (size_t)m0 * g.c_ld);
         wsrc.nbytes = (int)((int64_t)min(128, Mv - m0) * g.c_ld * 4);
         wsrc.ld4 = (uint32_t)(g.c_ld * 4);
+        wdst = wsrc;
+        wdst.base = (uint64_t)(Wz + (size_t)m0 * g.c_ld);
     }
     auto woff = [&](int n0, int i, int j) {
         const int n = n0 + wn * 32 + j * 16 + kg * 4;
@@ -1629,7 +1638,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
     // the bias of this lane's row, read now (updated after the prologue without a round trip)
     float ub_old = 0.f;
     const bool ub_lane = g.ubias != nullptr && (tid & 3) == 0 && m0 + (tid >> 2) < Mv;
-    if (ub_lane) ub_old = g.ubias[(size_t)cn * g.bias_z + m0 + (tid >> 2)];
+    if (ub_lane) ub_old = (g.rd_ub != nullptr ? g.rd_ub : g.ubias + (size_t)cn * g.bias_z)[m0 + (tid >> 2)];
 
     // fused last layer: A holds the hidden activations x; the strip's errors are formed here,
     // d[s][m] = (sum_o dout[s][o] W2[o][m]) phi'(x[s][m]) with the pre-update W2 (eq. (11)),
@@ -1650,7 +1659,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
         static_assert(U3_KMAX * 4 == B3_THREADS && MAX_OUT * 32 == B3_THREADS, "one float4 of each per thread");
         float4 dv4 = make_float4(0.f, 0.f, 0.f, 0.f);   // dout[tid >> 2][4 (tid & 3) ..]
         if ((tid >> 2) < g.step_rows) dv4 = *(const float4*)(dsrc + tid * 4);
-        const float* w2r = g.w2 + (size_t)cn * g.w2_z;
+        const float* w2r = g.rd_w2 != nullptr ? g.rd_w2 : g.w2 + (size_t)cn * g.w2_z;
         const int wo = tid >> 5, wc4 = (tid & 31) * 4;   // W2[wo][m0 + wc4 ..]
         float4 wv4 = make_float4(0.f, 0.f, 0.f, 0.f);
         if (wo < g.o2 && m0 + wc4 < Mv) wv4 = *(const float4*)(w2r + (size_t)wo * g.M + m0 + wc4);
@@ -1734,7 +1743,8 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
             float sb = 0.f;
 #pragma unroll
             for (int r = 0; r < U3_KMAX; ++r) sb += f_d[r * FDS + tid];
-            g.b2[(size_t)cn * g.bias_z + tid] -= scale * sb;
+            float* b2p = g.b2 + (size_t)cn * g.bias_z + tid;
+            *b2p = (g.rd_b2 != nullptr ? g.rd_b2[tid] : *b2p) - scale * sb;
         }
     } else {
         load_w(wcur, tcol(0));
@@ -1830,7 +1840,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                     const f4 v = acc[i][j];
                     float4 w = wcur[i][j];
                     w.x -= scale * v[0]; w.y -= scale * v[1]; w.z -= scale * v[2]; w.w -= scale * v[3];
-                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), b3_rsrc(wsrc), woff(n0, i, j), 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), b3_rsrc(wdst), woff(n0, i, j), 0, 0);
                     acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
                     wcur[i][j] = wnext[i][j];
                 }
@@ -1887,7 +1897,7 @@ __global__ __launch_bounds__(B3_THREADS) void upd128x3_kernel(GemmArgs g) {
                         const f4 v = acc[i][j];
                         float4 w = wc[i][j];
                         w.x -= scale * v[0]; w.y -= scale * v[1]; w.z -= scale * v[2]; w.w -= scale * v[3];
-                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), b3_rsrc(wsrc), woff(n0, i, j), 0, 0);
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), b3_rsrc(wdst), woff(n0, i, j), 0, 0);
                         acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
                     }
             }
@@ -2488,6 +2498,14 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
             }
         }
     }
+}
+
+// the merged network copied into every CN (a broadcast that a merge deferred), fp32 only
+__global__ __launch_bounds__(256) void bcast_kernel(float* theta, const float* merged, int64_t pstride, int K) {
+    const int64_t p = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (p >= pstride) return;
+    const float4 m = *(const float4*)(merged + p);
+    for (int k = 0; k < K; ++k) *(float4*)(theta + (size_t)k * pstride + p) = m;
 }
 
 // fp32 -> bf16 copy of a whole parameter block (shadow refresh after init / set)

@@ -126,6 +126,10 @@ struct pnn_net {
     // mini-batch plan with the last layer fused into the split-bf16 products of one hidden
     // layer: output-sum partials [K][ceil(H / 256)][B][16], output errors [K][B][16]
     bool fx3 = false;
+    // (fx3) a merge with broadcast left the copy of the merged network into the CNs to the next
+    // epoch's first step, which reads the merged slot; anything else that reads a CN's
+    // parameters first makes the copy (settle)
+    bool bcast_pending = false;
     float* fx3_zpart = nullptr;
     float* fx3_dout = nullptr;
     // bounded waits of the persistent kernels: polls before giving up; and a test hook that
@@ -417,10 +421,13 @@ Operand opnd(const void* p, int64_t zs, int64_t ld, int xrows, int64_t xshift = 
 // mini-batch plan: one batch step of every CN
 
 template <bool BF>
-pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t N, int64_t r0, hipStream_t s) {
+pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t N, int64_t r0, hipStream_t s,
+                          bool from_merged) {
     typedef typename std::conditional<BF, bf16_t, float>::type TH;  // hidden activations / errors
     const int L = n->L, B = n->cfg.batch, K = n->cfg.replicas;
     const bool fx3 = !BF && n->fx3;  // last layer fused into the split-bf16 products
+    // (fx3) every CN starts this step from the merged network, read from its one slot
+    from_merged = from_merged && fx3;
     const int64_t ps = n->pstride;
     const void* Wop = BF ? (const void*)n->shadow : (const void*)n->theta;  // operand weights
     const int64_t wz = ps;
@@ -454,6 +461,11 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
         if (fx3) {
             g.w2 = n->theta + n->off_w[1]; g.w2_z = ps;
             g.zpart = n->fx3_zpart; g.o2 = n->sizes[2];
+            if (from_merged) {
+                g.b = opnd(n->merged + n->off_w[0], 0, n->sizes[0], 0);
+                g.bias = n->merged + n->off_b[0]; g.bias_z = 0;
+                g.w2 = n->merged + n->off_w[1]; g.w2_z = 0;
+            }
         }
         if (l == 1) TRY((run_gemm<BF, float, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
         else TRY((run_gemm<BF, TH, TH, true, true, EPI_FWD, TH>(n, s, g, K, "fwd_gemm")));
@@ -464,6 +476,7 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
         memset(&a, 0, sizeof a);
         a.zpart = n->fx3_zpart; a.ntile = (n->sizes[1] + 255) / 256;
         a.bias = n->theta + n->off_b[1]; a.bias_z = ps;
+        if (from_merged) { a.bias = n->merged + n->off_b[1]; a.bias_z = 0; }
         a.O = n->sizes[2]; a.act_out = n->act[1]; a.loss = n->cfg.loss;
         a.n_total = N; a.k_rep = K; a.r0 = r0; a.step_rows = B;
         a.y = Y;
@@ -578,6 +591,10 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
                 g.dout = n->fx3_dout;
                 g.w2 = n->theta + n->off_w[1]; g.b2 = n->theta + n->off_b[1]; g.w2_z = ps;
                 g.o2 = n->sizes[2]; g.act2 = n->act[0];
+                if (from_merged) {
+                    g.rd_c = n->merged + n->off_w[0]; g.rd_w2 = n->merged + n->off_w[1];
+                    g.rd_ub = n->merged + n->off_b[0]; g.rd_b2 = n->merged + n->off_b[1];
+                }
             }
             if (l == 1) TRY((run_gemm<BF, TH, float, false, false, EPI_UPD, float>(n, s, g, K, "upd_gemm")));
             else TRY((run_gemm<BF, TH, TH, false, false, EPI_UPD, float>(n, s, g, K, "upd_gemm")));
@@ -1165,6 +1182,17 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
     return PNN_OK;
 }
 
+// the copy of the merged network into the CNs that a merge deferred, if one is pending
+static pnn_status settle(pnn_net* n, hipStream_t s) {
+    if (!n->bcast_pending) return PNN_OK;
+    const int64_t q = n->pstride / 4;
+    Launch l(n, s, "broadcast");
+    bcast_kernel<<<(unsigned)((q + 255) / 256), 256, 0, s>>>(n->theta, n->merged, n->pstride, n->cfg.replicas);
+    TRY(l.done());
+    n->bcast_pending = false;
+    return PNN_OK;
+}
+
 pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev, int64_t N, void* hip_stream) {
     TRY(usable(n));
     if (!x_dev || !y_dev) return fail(n, PNN_EINVAL, "x_dev / y_dev is NULL");
@@ -1172,12 +1200,16 @@ pnn_status pnn_train_epoch(pnn_net* n, const float* x_dev, const int32_t* y_dev,
     if (N < n->cfg.replicas) return fail(n, PNN_ESHAPE, "N = %lld < K = %d leaves a slice empty", (long long)N, n->cfg.replicas);
     TRY(check_abort(n, false));
     hipStream_t s = (hipStream_t)hip_stream;
+    if (!n->fx3) TRY(settle(n, s));
     if (n->psgd) return psgd_epoch(n, x_dev, y_dev, N, s);
     if (n->mbp) return mbp_epoch(n, x_dev, y_dev, N, s);
     const int64_t nmax = shard_len(N, n->cfg.replicas, 0);
     for (int64_t r0 = 0; r0 < nmax; r0 += n->cfg.batch) {
-        if (n->bf16) TRY(minibatch_step<true>(n, x_dev, y_dev, N, r0, s));
-        else TRY(minibatch_step<false>(n, x_dev, y_dev, N, r0, s));
+        // (the first step writes every parameter of every CN: each CN has rows in it)
+        const bool fm = r0 == 0 && n->bcast_pending;
+        if (n->bf16) TRY(minibatch_step<true>(n, x_dev, y_dev, N, r0, s, fm));
+        else TRY(minibatch_step<false>(n, x_dev, y_dev, N, r0, s, fm));
+        if (fm) n->bcast_pending = false;
     }
     return PNN_OK;
 }
@@ -1209,16 +1241,22 @@ pnn_status pnn_train_epoch_order(pnn_net* n, const float* x_dev, const int32_t* 
 }
 
 static pnn_status launch_merge(pnn_net* n, int32_t broadcast, const double* w_dev, double wsum, hipStream_t s) {
+    TRY(settle(n, s));
+    // with the fused last layer the broadcast is left to the next epoch's first step, which
+    // reads the merged slot and writes every CN (saving a write of K copies and their reads)
+    const bool defer = broadcast && n->fx3;
     MergeArgs a;
     a.theta = n->theta; a.merged = n->merged;
     a.shadow = n->bf16 ? n->shadow : nullptr;
     a.mshadow = n->bf16 ? n->mshadow : nullptr;
-    a.pstride = n->pstride; a.K = n->cfg.replicas; a.broadcast = broadcast ? 1 : 0;
+    a.pstride = n->pstride; a.K = n->cfg.replicas; a.broadcast = broadcast && !defer ? 1 : 0;
     a.w = w_dev; a.wsum = wsum;
     const int64_t q = n->pstride / 4;
     Launch l(n, s, "merge");
     merge_kernel<<<(unsigned)((q + 255) / 256), 256, 0, s>>>(a);
-    return l.done();
+    TRY(l.done());
+    n->bcast_pending = defer;
+    return PNN_OK;
 }
 
 pnn_status pnn_merge(pnn_net* n, int32_t broadcast, void* hip_stream) {
@@ -1370,6 +1408,7 @@ pnn_status pnn_infer(pnn_net* n, int32_t which, const float* x_dev, int64_t nrow
     if (!aligned16(x_dev)) return fail(n, PNN_EINVAL, "x_dev is not 16-byte aligned");
     TRY(check_abort(n, true));
     hipStream_t s = (hipStream_t)hip_stream;
+    if (which >= 0) TRY(settle(n, s));
     const bool count = correct_host && y_dev;
     TRY(grow_inference_ws(n, nrows, s));
     TRY(run_inference(n, which, x_dev, nrows, pred_dev, out_dev, count, y_dev, nullptr, n->inf_ws, n->d_correct, s));
@@ -1405,6 +1444,7 @@ pnn_status pnn_eval(pnn_net* n, int32_t which, const float* x_dev, const int32_t
         n->cost_rows = nrows;
     }
     TRY(grow_inference_ws(n, nrows, s));
+    if (which >= 0) TRY(settle(n, s));
     return eval_run(n, which, x_dev, y_dev, nrows, correct_host, cost_host, n->inf_ws, n->d_correct, n->d_cost,
                     n->d_cost_sum, s);
 }
@@ -1442,6 +1482,7 @@ pnn_status pnn_eval_noalloc(pnn_net* n, int32_t which, const float* x_dev, const
         o += round_up((int64_t)rows * n->sizes[l] * el, 256);
     }
     double* cost = cost_host ? (double*)(base + o) : nullptr;
+    if (which >= 0) TRY(settle(n, s));
     return eval_run(n, which, x_dev, y_dev, nrows, correct_host, cost_host, ws, correct, cost, cost_sum, s);
 }
 
@@ -1457,6 +1498,10 @@ pnn_status pnn_get_params(pnn_net* n, int32_t which, float* host_out) {
     if (which < -1 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
     HIP_TRY(n, hipDeviceSynchronize());
     TRY(check_abort(n, true));
+    if (which >= 0) {
+        TRY(settle(n, nullptr));
+        HIP_TRY(n, hipDeviceSynchronize());
+    }
     std::vector<float> padded(n->pstride);
     const float* src = which < 0 ? n->merged : n->theta + (size_t)which * n->pstride;
     HIP_TRY(n, hipMemcpy(padded.data(), src, n->pstride * sizeof(float), hipMemcpyDeviceToHost));
@@ -1470,6 +1515,7 @@ pnn_status pnn_set_params(pnn_net* n, int32_t which, const float* host_in) {
     if (which < -2 || which >= n->cfg.replicas) return fail(n, PNN_EINVAL, "which = %d out of range", which);
     HIP_TRY(n, hipDeviceSynchronize());
     TRY(check_abort(n, true));
+    TRY(settle(n, nullptr));
     std::vector<float> padded(n->pstride);
     unpack(n, host_in, padded.data());
     const size_t bytes = n->pstride * sizeof(float);

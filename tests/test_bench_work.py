@@ -92,3 +92,17 @@ def test_more_than_one_gpu_is_refused():
                        timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_merge_bytes_follow_the_deferred_broadcast():
+    """The merge writes the K copies of the merged network itself except with the last layer
+    fused, where the next epoch's first step writes them (the copy made on demand is priced as
+    the broadcast)."""
+    w = I.WORKLOADS[4]
+    K, P = w.replicas, w.param_count()
+    assert w.merge_every_epoch
+    _, b_plain = bench.kernel_work(w, "merge", 1, w.n_train, 1, False)
+    _, b_fused = bench.kernel_work(w, "merge", 1, w.n_train, 1, True)
+    assert b_plain == (2 * K * P + P) * 4.0
+    assert b_fused == (K * P + P) * 4.0
+    assert bench.kernel_work(w, "broadcast", 1, w.n_train, 1, True)[1] == (K * P + P) * 4.0

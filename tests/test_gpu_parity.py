@@ -289,6 +289,45 @@ def test_epochs_launch_plan(idx, over, N, epochs, monkeypatch):
     net.close()
 
 
+def test_deferred_broadcast():
+    """Fused last layer with a merge and broadcast after each epoch, nothing read in between: the
+    copy of the merged network into the CNs is left to the next epoch's first step, which reads
+    the merged slot and writes every CN.  Every CN and the merged network against the oracle
+    after each epoch; then a CN read, an evaluation of a CN and a second merge right after a
+    deferred merge see the merged network (the copy made on demand)."""
+    w = I.WORKLOADS[4].scaled(replicas=16)
+    N = 16 * 260 + 7                  # batches 128, 128, 4/5
+    X, y = I.train_set(w, N)
+    Xt, yt = I.test_set(w, 500)
+    th0 = I.init_params(w)
+    net = make_net(w, th0)
+    assert net.plan == "mini-batch fused last layer"
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    xd, yd = dev(X), dev(y)
+    for e in range(3):
+        net.train_epoch(xd, yd)
+        o.train_epoch(ref, X, y, threads=8)
+        net.merge(broadcast=True)
+        m = o.merge(ref)
+        ref[:] = m[None, :]
+    close_epoch(w, net.get_params(-1), m, "merged after three epochs")
+    merged = net.get_params(-1)
+    # a CN's evaluation first makes the deferred copy; then every CN holds the merged network
+    c_cn = net.evaluate(dev(Xt), dev(yt), which=3)
+    c_m = net.evaluate(dev(Xt), dev(yt), which=-1)
+    assert c_cn == c_m
+    for k in range(w.replicas):
+        assert np.array_equal(net.get_params(k), merged), k
+    # a merge of CNs that all hold the merged network gives it back exactly, with or without a
+    # pending copy before it
+    net.merge(broadcast=True)
+    net.merge(broadcast=False)
+    assert np.array_equal(net.get_params(-1), merged)
+    assert np.array_equal(net.get_params(5), merged)
+    net.close()
+
+
 def test_misaligned_input_rows_are_rejected():
     """x_dev must be 16-byte aligned (rows are read with 16-byte loads): a view one float into a
     buffer is refused by every call that reads rows, before any device work."""
