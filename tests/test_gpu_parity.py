@@ -325,6 +325,20 @@ def test_deferred_broadcast():
     net.merge(broadcast=False)
     assert np.array_equal(net.get_params(-1), merged)
     assert np.array_equal(net.get_params(5), merged)
+    # the allocation-free evaluation of a CN makes a pending copy too
+    net.merge(broadcast=True)
+    c7, cost7 = net.evaluate_noalloc(dev(Xt), dev(yt), which=7)
+    assert c7 == c_m[0] and abs(cost7 - c_m[1]) <= 1e-12 * abs(c_m[1])
+    # a weighted merge with broadcast defers the same way: one more epoch from it against the oracle
+    wts = np.linspace(1.0, 2.0, w.replicas)
+    net.merge_weighted(wts, broadcast=True)
+    mw = o.merge_weighted(ref, wts)
+    close_epoch(w, net.get_params(-1), mw, "weighted merge")
+    net.train_epoch(xd, yd)
+    ref[:] = mw[None, :]
+    o.train_epoch(ref, X, y, threads=8)
+    for k in (0, 9, w.replicas - 1):
+        close_epoch(w, net.get_params(k), ref[k], f"epoch after a weighted merge, replica {k}")
     net.close()
 
 
