@@ -205,16 +205,24 @@ template <> struct GemmTile<true> { static constexpr int BK = 32, LDK = 40; type
 // renumbered so that all tiles of one z run on one XCD, one z after another, and share that
 // XCD's L2 (the operand tiles of a CN are read by several tiles each).  (With fewer z per XCD
 // the plain order measured faster.)
-__device__ inline void gemm_tile(int& bx, int& by, int& bz) {
-    const int gx = gridDim.x, gy = gridDim.y, gz = gridDim.z;
-    bx = blockIdx.x; by = blockIdx.y; bz = blockIdx.z;
-    if (gz % 8 != 0 || gz < 64) return;
+// (p: the workgroup's place in the dispatch order of a gx x gy x gz grid)
+__device__ inline void gemm_tile_of(int p, int gx, int gy, int gz, int& bx, int& by, int& bz) {
     const int tpz = gx * gy;
-    const int p = bx + gx * (by + gy * bz);  // dispatch order
+    if (gz % 8 != 0 || gz < 64) {
+        bz = p / tpz;
+        const int t = p - bz * tpz;
+        by = t / gx;
+        bx = t - by * gx;
+        return;
+    }
     const int slot = p >> 3, zq = slot / tpz, t = slot - zq * tpz;
     bz = zq * 8 + (p & 7);
     by = t / gx;
     bx = t - by * gx;
+}
+__device__ inline void gemm_tile(int& bx, int& by, int& bz) {
+    const int gx = gridDim.x, gy = gridDim.y;
+    gemm_tile_of(blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z), gx, gy, gridDim.z, bx, by, bz);
 }
 
 __device__ inline void gemm_zinfo(const GemmArgs& g, int z, int& cn, int64_t& r0, int& valid) {
@@ -411,21 +419,30 @@ __device__ inline void store_tile32(float* lds, bool kc, const float4& v, int ti
 
 // WPRE (weight update with a short contraction): the update's targets are read before the
 // contraction, their latency behind it (16 more registers per lane)
-template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO, bool WPRE = false>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
+// the LDS of one workgroup: two buffers per operand (one barrier per k-tile) and the bias sums
+template <bool BF, bool A_KC, bool B_KC>
+struct GemmLds {
+    typedef typename GemmTile<BF>::T LT;
+    static constexpr int LDK = GemmTile<BF>::LDK;
+    static constexpr int ASZ = (BF || A_KC) ? 64 * LDK : 16 * GEMM_LDM, BSZ = (BF || B_KC) ? 64 * LDK : 16 * GEMM_LDM;
+    static constexpr int NBUF = 2;
+    __attribute__((aligned(16))) LT As[NBUF * ASZ];
+    __attribute__((aligned(16))) LT Bs[NBUF * BSZ];
+    float rowsum[64];
+};
+
+template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO, bool WPRE>
+__device__ __attribute__((always_inline)) inline void gemm_body(const GemmArgs& g, int bx, int by, int bz,
+                                                                GemmLds<BF, A_KC, B_KC>& lds) {
     typedef typename GemmTile<BF>::T LT;
     constexpr int BK = GemmTile<BF>::BK, LDK = GemmTile<BF>::LDK;
-    // two buffers per operand (one barrier per k-tile)
-    constexpr int ASZ = (BF || A_KC) ? 64 * LDK : 16 * GEMM_LDM, BSZ = (BF || B_KC) ? 64 * LDK : 16 * GEMM_LDM;
-    constexpr int NBUF = 2;
-    __shared__ __attribute__((aligned(16))) LT As[NBUF * ASZ];
-    __shared__ __attribute__((aligned(16))) LT Bs[NBUF * BSZ];
-    __shared__ float rowsum[64];
+    constexpr int ASZ = GemmLds<BF, A_KC, B_KC>::ASZ, BSZ = GemmLds<BF, A_KC, B_KC>::BSZ;
+    LT* As = lds.As;
+    LT* Bs = lds.Bs;
+    float* rowsum = lds.rowsum;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    int bx, by, bz;
-    gemm_tile(bx, by, bz);
     const int zz = bz / g.ksplit, slice = bz % g.ksplit;
     int cn, valid;
     int64_t r0;
@@ -690,6 +707,36 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     if (do_rowsum && tid < 64 && m0 + tid < Mv) {
         float* b = g.ubias + (size_t)cn * g.bias_z;
         b[m0 + tid] -= scale * rowsum[tid];
+    }
+}
+
+template <bool BF, typename TA, typename TB, bool A_KC, bool B_KC, int EPI, typename TO, bool WPRE = false>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
+    __shared__ GemmLds<BF, A_KC, B_KC> lds;
+    int bx, by, bz;
+    gemm_tile(bx, by, bz);
+    gemm_body<BF, TA, TB, A_KC, B_KC, EPI, TO, WPRE>(g, bx, by, bz, lds);
+}
+
+// Two independent weight updates of the bf16 mini-batch plan (two wide layers, samples along
+// the contraction, the targets read before it) in one launch: the first grid's workgroups,
+// then the second's, in one dispatch order (a one-dimensional grid of both counts; each part
+// is mapped to its tiles as gemm_tile maps a grid of its own, and the first part's count is a
+// multiple of 8, so that the XCD of a workgroup is as in a launch of its own).  The smaller
+// update's last round of workgroups then shares the chip with the larger one instead of
+// running alone, and one launch boundary goes.
+template <typename TB1, typename TB2>
+__global__ __launch_bounds__(256) void gemm_upd2_kernel(GemmArgs g1, GemmArgs g2, int gx1, int gy1, int gz1,
+                                                       int gx2, int gy2, int gz2) {
+    __shared__ GemmLds<true, false, false> lds;
+    const int p = blockIdx.x, n1 = gx1 * gy1 * gz1;
+    int bx, by, bz;
+    if (p < n1) {
+        gemm_tile_of(p, gx1, gy1, gz1, bx, by, bz);
+        gemm_body<true, bf16_t, TB1, false, false, EPI_UPD, float, true>(g1, bx, by, bz, lds);
+    } else {
+        gemm_tile_of(p - n1, gx2, gy2, gz2, bx, by, bz);
+        gemm_body<true, bf16_t, TB2, false, false, EPI_UPD, float, true>(g2, bx, by, bz, lds);
     }
 }
 

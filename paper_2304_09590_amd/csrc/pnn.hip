@@ -557,8 +557,35 @@ pnn_status minibatch_step(pnn_net* n, const float* X, const int32_t* Y, int64_t 
         }
     }
     // updates, eq. (12)-(13) averaged over the batch
+    // (bf16, two wide layers before a fused last layer: both weight updates in one launch)
+    const bool upd2 = BF && L == 3 && fuse_tail && n->sizes[1] > MAX_OUT && n->sizes[2] > MAX_OUT && B <= 64 &&
+                      K % 8 == 0 && n->sizes[0] % 4 == 0 && n->sizes[1] % 4 == 0 && n->sizes[2] % 4 == 0;
+    if constexpr (BF) if (upd2) {
+        GemmArgs gg[2];
+        int gd[2][3];
+        for (int l = 1; l <= 2; ++l) {
+            const int In = n->sizes[l - 1], Out = n->sizes[l];
+            GemmArgs g = gemm_base(n, Out, In, B, N, r0, B, 4);
+            g.a = opnd(n->del_ws[l], (int64_t)B * Out, Out, 0);
+            if (l == 1) g.b = opnd(X, 0, In, 1);
+            else g.b = opnd(n->act_ws[l - 1], (int64_t)B * In, In, 0);
+            g.c = n->theta + n->off_w[l - 1]; g.c_z = ps; g.c_ld = In;
+            g.ubias = n->theta + n->off_b[l - 1]; g.bias_z = ps;
+            g.lr = n->cfg.lr; g.scale_per_batch = 1;
+            g.shadow = n->shadow + n->off_w[l - 1];
+            gg[l - 1] = g;
+            gd[l - 1][0] = (In + 63) / 64; gd[l - 1][1] = (Out + 63) / 64; gd[l - 1][2] = K;
+        }
+        const int64_t nwg = (int64_t)gd[0][0] * gd[0][1] * K + (int64_t)gd[1][0] * gd[1][1] * K;
+        if (nwg > INT32_MAX) return fail(n, PNN_EINVAL, "upd_gemm: %lld workgroups", (long long)nwg);
+        Launch lu(n, s, "upd_gemm");
+        gemm_upd2_kernel<float, TH><<<(unsigned)nwg, 256, 0, s>>>(gg[0], gg[1], gd[0][0], gd[0][1], gd[0][2],
+                                                                  gd[1][0], gd[1][1], gd[1][2]);
+        TRY(lu.done());
+    }
     for (int l = 1; l <= L; ++l) {
         if ((fuse_tail || fx3) && l == L) continue;  // (in the fused last layer)
+        if (upd2 && l <= 2) continue;                // (above)
         const int In = n->sizes[l - 1], Out = n->sizes[l];
         if (Out <= MAX_OUT) {
             UpdSmallArgs a;
