@@ -14,6 +14,7 @@ EPOCH_CASES = [
     (1, dict(replicas=3), 3 * 140 + 1, 2),                    # uneven slices, two epochs
     (2, {}, 16 * 100 + 5, 2),                                 # batches 32,32,32,4/5
     (3, dict(replicas=8), 8 * 150 + 3, 2),                    # bf16, merge + broadcast each epoch
+    (3, dict(replicas=6), 6 * 150 + 5, 1),                    # bf16, K not a multiple of 8: two update launches
     (4, dict(replicas=16), 16 * 260 + 7, 2),                  # batches 128,128,4/5, merge each epoch
     (4, dict(replicas=4), 4 * 224 + 2, 2),                    # batches 128, 97/96 (one launch, zero padded)
     # the fused last layer with softmax / cross-entropy over 16 outputs (tanh hidden layer), and
@@ -102,4 +103,5 @@ def case_key(idx, over, N, epochs):
 
 BF16_ELEMENTWISE = {
     case_key(3, dict(replicas=8), 8 * 150 + 3, 2): {0: ("W1", "W3", "b3"), 1: ("W3",)},
+    case_key(3, dict(replicas=6), 6 * 150 + 5, 1): {0: ("W1", "W3", "b3")},
 }

@@ -79,8 +79,11 @@ def test_sensitive_fp32_cases_are_chaotic_elementwise_only(idx, over, N, epochs)
     assert worst_layer < EPOCH_TOL / 10, worst_layer
 
 
-def test_bf16_reduced_case_elementwise_tensors():
-    idx, over, N, epochs = 3, dict(replicas=8), 8 * 150 + 3, 2
+BF16_REDUCED = [(3, dict(replicas=8), 8 * 150 + 3, 2), (3, dict(replicas=6), 6 * 150 + 5, 1)]
+
+
+@pytest.mark.parametrize("idx,over,N,epochs", BF16_REDUCED)
+def test_bf16_reduced_case_elementwise_tensors(idx, over, N, epochs):
     w = I.WORKLOADS[idx].scaled(**over)
     table = BF16_ELEMENTWISE[case_key(idx, over, N, epochs)]
     X, y = I.train_set(w, N)
