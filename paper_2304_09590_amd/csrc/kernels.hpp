@@ -2856,12 +2856,15 @@ struct PsgdPArgs {
     int qstride;         // row stride (per neuron) within a slot
     int64_t qslot;
     float* d1;           // [2][K][H][T]  by chunk parity (transposed: one row per hidden neuron)
-    int* flags;          // qready[K], dready[K], abort (sticky: cleared only at allocation)
+    int* flags;          // qready[2][K] by chunk parity, dready[K], abort (sticky: cleared only at allocation)
     int H, O, In, act1, act2, loss, nrb;
     int cn0, k_launch;   // this launch trains CNs cn0 .. cn0 + k_launch - 1 (all K share the flags)
     int wait_skew;       // 0; a large value makes the first wait of every sequential workgroup
                          // wait for more tile signals than ever come (failure-handling test:
                          // the bound is reached)
+    int tile_delay;      // 0; n > 0 holds the upper half of every CN's tile workgroups back for
+                         // n sleeps before their first publish (ordering test: the CN must wait
+                         // for every tile's Q_0 however far the others run ahead)
     float lr;
     long spin_limit;
 };
@@ -3250,9 +3253,14 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     const int nchk = (nsteps + T - 1) / T;
     const int nblk = (nsteps + BS - 1) / BS;
     float* th = a.theta + (size_t)k * a.pstride;
-    int* qready = a.flags + k;
-    int* dready = a.flags + K + k;
-    int* gabort = a.flags + 2 * K;
+    // Q_c is complete when the counter of parity c & 1 reaches nrb (c / 2 + 1): no tile can
+    // publish Q_{c+2} before chunk c's errors exist, which take Q_c, so a tile's count on that
+    // parity reaches c / 2 + 1 only by publishing Q_c.  (A single counter for both parities
+    // could reach nrb (c + 1) with some tiles at Q_{c+1} and others still short of Q_c.)
+    auto qready = [&](int c) { return a.flags + (c & 1) * K + k; };
+    auto qtarget = [&](int c) { return a.nrb * (c / 2 + 1); };
+    int* dready = a.flags + 2 * K + k;
+    int* gabort = a.flags + 3 * K;
 
     // padding neurons h >= H read zero errors and zero input sums
     for (int i = tid; i < HW * TS; i += 256) hist[i] = 0.f;
@@ -3260,7 +3268,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
     if (tid < 12) lf[tid] = 0;
 
     // chunk 0: wait for Q_0 and stage it with the Gram block and labels
-    if (!wait_geq(qready, a.nrb + a.wait_skew, gabort, a.spin_limit)) return;
+    if (!wait_geq(qready(0), qtarget(0) + a.wait_skew, gabort, a.spin_limit)) return;
     {
         const float* Q = a.qbuf + (size_t)k * HW * TS;
         const float* G = a.gram + (size_t)k * a.nch * T * GS;
@@ -3603,7 +3611,7 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                     fold_acc<GS, TS, MT, NT>(accN, GX, hist, 0, BS * b, -lr, nt0, lane);
                     if (b >= NB - 2) {
                         if (!qn) {
-                            if (!wait_geq_wave(qready, a.nrb * (c + 2), gabort, a.spin_limit)) {
+                            if (!wait_geq_wave(qready(c + 1), qtarget(c + 1), gabort, a.spin_limit)) {
                                 lds_publish(lab, 1);
                                 break;
                             }
@@ -3631,8 +3639,8 @@ __device__ __attribute__((always_inline)) inline void psgd_rec(const PsgdPArgs& 
                 // ---- Q of accN's chunk, as soon as the tiles have published it
                 const int cq = fn / NB + 1;
                 const int qv = __builtin_amdgcn_readfirstlane(
-                    __hip_atomic_load(qready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-                if (qv >= a.nrb * (cq + 1)) {
+                    __hip_atomic_load(qready(cq), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                if (qv >= qtarget(cq)) {
                     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
                     add_q<TS, MT, NT>(accN, qrows(cq), nt0, lane);
                     qn = true;
@@ -3678,9 +3686,8 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
     }
     const int64_t nz = shard_len(a.n_total, K, k), xs = shard_start(a.n_total, K, k);
     const int nchk = (int)((nz + T - 1) / T);
-    int* qready = a.flags + k;
-    int* dready = a.flags + K + k;
-    int* abort = a.flags + 2 * K;
+    int* dready = a.flags + 2 * K + k;
+    int* abort = a.flags + 3 * K;
     constexpr int NMT = T / 16;
     float* red4 = smem;  // [4 waves][NMT][RT][64][4]
 
@@ -3726,7 +3733,7 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
             const int t = mt * 16 + 4 * (ln >> 4) + rr, hh = hb + r * 16 + (ln & 15);
             if (t < tc && hh < H) Q[(size_t)hh * a.qstride + t] = sum;
         }
-        signal_add(qready, 1);
+        signal_add(a.flags + (c & 1) * K + k, 1);  // one counter per chunk parity
     };
     // W1 tile -= eta * sum_t d1_t x_t^T over the rows of chunk c (errors stored [h][T])
     auto update = [&](int c) {
@@ -3776,6 +3783,8 @@ __device__ __attribute__((always_inline)) inline void psgd_tile(const PsgdPArgs&
     // Q_0 and Q_1 use the initial weights; afterwards chunk c's errors (c >= 0) are applied
     // before Q_{c+2} is computed.  One call site each keeps the code compact.
     bool ok = true;
+    if (a.tile_delay > 0 && 2 * rb >= a.nrb)
+        for (int i = 0; i < a.tile_delay; ++i) __builtin_amdgcn_s_sleep(127);
     for (int step = 0; step <= nchk && ok; ++step) {
         // step 0: publish Q_0 (and Q_1); step s >= 1: apply the errors of chunk s-1, then
         // publish Q_{s+1}
@@ -3807,7 +3816,7 @@ __global__ __launch_bounds__(256) void psgd_persistent_kernel(PsgdPArgs a) {
     extern __shared__ float smem[];
     const int b = blockIdx.x, K = a.k_rep, KL = a.k_launch;
     // an earlier launch gave up waiting: the parameters are unspecified, train no further
-    if (__hip_atomic_load(a.flags + 2 * K, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+    if (__hip_atomic_load(a.flags + 3 * K, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
     if (b < KL) psgd_rec<T, NH, A1, A2, LS, OC>(a, a.cn0 + b, smem);
     else {
         const int j = b - KL;

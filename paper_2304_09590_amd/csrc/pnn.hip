@@ -108,7 +108,7 @@ struct pnn_net {
     int nrb = 0;             // tile workgroups per CN
     int kgroup = 0;          // CNs per launch of a persistent plan (all K, or groups that fit the CUs)
     int prt = 1;             // 16-row sub-tiles per tile workgroup
-    int* flags = nullptr;    // qready[K], dready[K], abort
+    int* flags = nullptr;    // per-sample plan: qready[2][K] (by chunk parity), dready[K], abort
     float* qbuf = nullptr;   // [2][K][T][H]
     float* gramx = nullptr;  // [K][nch-1][T][T]
     size_t gramx_elems = 0;
@@ -138,6 +138,7 @@ struct pnn_net {
     long spin_limit = 0;
     unsigned tag_skew = 0;
     int wait_skew = 0;
+    int tile_delay = 0;  // PNN_TEST_TILE_DELAY: late tile workgroups in the per-sample kernel
     // the abort flag of the last persistent launch has not been read yet; abort_ev follows
     // that launch on its stream
     bool abort_pending = false;
@@ -696,9 +697,9 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
         TRY((run_gemm<false, float, float, true, true, EPI_STORE, float>(n, s, g, K * (nch - 1), "psgd_gram")));
     }
     {
-        // (the abort slot flags[2K] is sticky: a launch after an abort ends at once)
+        // (the abort slot flags[3K] is sticky: a launch after an abort ends at once)
         Launch l(n, s, "zero_flags");
-        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, 2 * K);
+        zero_ints_kernel<<<(3 * K + 255) / 256, 256, 0, s>>>(n->flags, 3 * K);
         TRY(l.done());
     }
     PsgdPArgs a;
@@ -712,6 +713,7 @@ pnn_status psgd_persistent_epoch(pnn_net* n, const float* X, const int32_t* Y, i
     a.H = H; a.O = n->sizes[2]; a.In = In; a.act1 = n->act[0]; a.act2 = n->act[1]; a.loss = n->cfg.loss;
     a.nrb = n->nrb;
     a.wait_skew = n->wait_skew;
+    a.tile_delay = n->tile_delay;
     a.lr = n->cfg.lr;
     a.spin_limit = n->spin_limit;
     void* params[] = {&a};
@@ -755,7 +757,7 @@ pnn_status mbp_epoch(pnn_net* n, const float* X, const int32_t* Y, int64_t N, hi
     {
         // (the abort slot flags[K] is sticky: a launch after an abort ends at once)
         Launch l(n, s, "zero_flags");
-        zero_ints_kernel<<<1, 256, 0, s>>>(n->flags, K);
+        zero_ints_kernel<<<(K + 255) / 256, 256, 0, s>>>(n->flags, K);
         TRY(l.done());
     }
     MbpArgs a;
@@ -928,7 +930,7 @@ pnn_status check_abort(pnn_net* n, bool wait) {
         HIP_TRY(n, hipEventSynchronize(n->abort_ev));
     }
     int ab = 0;
-    const int at = n->persistent ? 2 * n->cfg.replicas : n->cfg.replicas;
+    const int at = n->persistent ? 3 * n->cfg.replicas : n->cfg.replicas;
     HIP_TRY(n, hipMemcpy(&ab, n->flags + at, sizeof(int), hipMemcpyDeviceToHost));
     n->abort_pending = false;
     if (ab) {
@@ -1021,7 +1023,13 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
     if (const char* e = getenv("PNN_TEST_STALL_WAITS")) {
         const bool on = strcmp(e, "1") == 0;
         n->tag_skew = on ? 1u : 0u;
-        n->wait_skew = on ? (1 << 29) : 0;  // (the tiles count up to nrb per chunk, and run a chunk ahead)
+        n->wait_skew = on ? (1 << 29) : 0;  // (the tiles count up to nrb per chunk parity)
+    }
+    // PNN_TEST_TILE_DELAY=n: half of every CN's tile workgroups start n sleeps late (the
+    // per-sample kernel's results must not change)
+    if (const char* e = getenv("PNN_TEST_TILE_DELAY")) {
+        const long v = strtol(e, nullptr, 10);
+        n->tile_delay = v > 0 && v < (1 << 20) ? (int)v : 0;
     }
     const int K = cfg->replicas, B = cfg->batch;
     pnn_status st;
@@ -1083,7 +1091,7 @@ pnn_status pnn_init(const pnn_config* cfg, const float* theta0_host, void* hip_s
             if (hipMemset(n->qbuf, 0, sizeof(float) * qn) != hipSuccess)
                 return bail(fail(n, PNN_EHIP, "hipMemset of the input-sum buffer failed"));
             if ((st = dev_alloc(n, &n->d1, (size_t)2 * K * PT * H)) != PNN_OK) return bail(st);
-            if ((st = dev_alloc(n, &n->flags, (size_t)(2 * K + 1))) != PNN_OK) return bail(st);
+            if ((st = dev_alloc(n, &n->flags, (size_t)(3 * K + 1))) != PNN_OK) return bail(st);
         }
     }
     if (n->psgd && !n->persistent) {

@@ -425,6 +425,67 @@ def test_persistent_kernel_abort_path(idx, over, plan, first, monkeypatch):
     net.close()
 
 
+@pytest.mark.parametrize("over,N", [(dict(sizes=(784, 64, 10), acts=(1, 0), replicas=3), 302),
+                                     (dict(replicas=2), 2 * 150 + 7)])
+def test_per_sample_tiles_out_of_order(over, N, monkeypatch):
+    """Ordering forced from the host: the upper half of every CN's tile workgroups start a few
+    milliseconds late, so that the others publish Q_0 and Q_1 (the input sums of the first two
+    chunks) before they publish anything.  The sequential workgroup must still wait for every
+    tile's share of each Q (one readiness counter per chunk parity).  Over two epochs both runs
+    match the oracle at the epoch tolerance.  (They need not agree bit for bit: Q joins the next
+    chunk's accumulated input sums as soon as it is complete, between folds whose number
+    depends on timing.)  With a single counter the first rows would start from stale input
+    sums, errors of order 0.1 and more."""
+    w = I.WORKLOADS[1].scaled(**over)
+    K = w.replicas
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    xd, yd = dev(X), dev(y)
+    got = {}
+    for delay in (0, 2000):
+        if delay:
+            monkeypatch.setenv("PNN_TEST_TILE_DELAY", str(delay))
+        log(f"tiles out of order: {w.name} {over} N={N} delay {delay}")
+        net = make_net(w, th0)
+        assert net.plan == "per-sample persistent"
+        for _ in range(2):
+            net.train_epoch(xd, yd)
+        got[delay] = [net.get_params(k) for k in range(K)]
+        net.close()
+    monkeypatch.delenv("PNN_TEST_TILE_DELAY")
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    for _ in range(2):
+        o.train_epoch(ref, X, y, threads=4)
+    for k in range(K):
+        close_epoch(w, got[0][k], ref[k], f"replica {k}")
+        close_epoch(w, got[2000][k], ref[k], f"replica {k}, late tiles")
+
+
+def test_per_sample_many_cns_flag_reset():
+    """More CNs than one workgroup of the flag-reset kernel covers (3 K counters > 256): every
+    epoch starts with every CN's readiness counters at zero, so the second epoch matches the
+    oracle too."""
+    w = I.WORKLOADS[0].scaled(replicas=90)
+    K = w.replicas
+    N = K * 150 + 5  # three chunks of input sums per CN
+    X, y = I.train_set(w, N)
+    th0 = I.init_params(w)
+    log(f"many CNs, per-sample: {w.name} K={K} N={N}")
+    net = make_net(w, th0)
+    log(f"plan: {net.plan}")
+    assert net.plan == "per-sample persistent"
+    xd, yd = dev(X), dev(y)
+    o = O.Oracle.from_workload(w)
+    ref = o.replicate(th0)
+    for e in range(2):
+        net.train_epoch(xd, yd)
+        o.train_epoch(ref, X, y, threads=8)
+        for k in (0, 1, K // 2, K - 2, K - 1):
+            close_epoch(w, net.get_params(k), ref[k], f"epoch {e} replica {k}")
+    net.close()
+
+
 # ------------------------------------------------------------------------------------
 # step-by-step trajectory: before every step the oracle restarts from the GPU's state
 
