@@ -226,7 +226,9 @@ int32_t pnn_profile_read(pnn_net* net, const char** names, double* total_ms, int
  * pnn_train_epoch (which does not wait: it sees the failure once that launch has ended, and a
  * persistent launch enqueued after the failed one ends at once) -- returns PNN_EHIP and marks
  * the handle unusable (PNN_ESTATE from then on).  PNN_TEST_STALL_WAITS=1 (tests of that path
- * only) makes the persistent kernels' waits run into the bound. */
+ * only) makes the persistent kernels' waits run into the bound.  PNN_TEST_TILE_DELAY=n (n sleeps
+ * of about 3 us, ordering tests only) starts half of every CN's tile workgroups late in the
+ * per-sample persistent kernel; the results stay within rounding of an undelayed run. */
 const char* pnn_plan(const pnn_net* net);
 
 /* Releases the handle and everything it owns (NULL is ignored). */
