@@ -426,7 +426,11 @@ def test_persistent_kernel_abort_path(idx, over, plan, first, monkeypatch):
 
 
 @pytest.mark.parametrize("over,N", [(dict(sizes=(784, 64, 10), acts=(1, 0), replicas=3), 302),
-                                     (dict(replicas=2), 2 * 150 + 7)])
+                                     (dict(replicas=2), 2 * 150 + 7),
+                                     # 32-row tiles (40 CNs fit one launch with them)
+                                     (dict(replicas=40), 40 * 70 + 3),
+                                     # 16-row tiles, the CNs in three launches sharing the flags
+                                     (dict(replicas=60), 60 * 70 + 3)])
 def test_per_sample_tiles_out_of_order(over, N, monkeypatch):
     """Ordering forced from the host: the upper half of every CN's tile workgroups start a few
     milliseconds late, so that the others publish Q_0 and Q_1 (the input sums of the first two
